@@ -1,0 +1,190 @@
+/*
+ * moe_offload.h - C ABI of the MI355X (gfx950) library for Mixture-of-Experts
+ * decode under expert offloading.
+ *
+ * The operation (Sec. 2.2, Sec. 3, Sec. 4.2-4.3 of "In-Depth Analysis on
+ * Caching and Pre-fetching in Mixture of Experts Offloading"):
+ *   - every layer has a gate W_g [E x d] and E SwiGLU experts; a token's
+ *     hidden state h is routed to the top-K experts of z = W_g h and the
+ *     layer adds sum_r g_r FFN_{i_r}(h / rms(h)) to h (Sec. 2.2, Sec. 4.3);
+ *   - all experts live in pinned host memory; each layer keeps S of them in
+ *     HBM slots and loads a missing one on demand (Sec. 2.2, Sec. 3.1);
+ *   - the resident set is managed with LRU (Sec. 3.1) or LFU (Sec. 4.2);
+ *   - optionally, layer l+1's gate applied to layer l's hidden state guesses
+ *     layer l+1's experts, which are then fetched early (Sec. 3.2, Sec. 4.3).
+ *
+ * Conventions
+ *   - All functions return MOE_OK (0) or a negative MOE_ERR_* code; no C++
+ *     exception or abort crosses this boundary.  moe_last_error() gives a
+ *     thread-local message for the last failure on the calling thread.
+ *   - Pointers marked "device" are HBM addresses; "pinned host" is memory
+ *     from hipHostMalloc (or moe_host_alloc); "host" is ordinary memory.
+ *   - The caller owns every buffer it passes (gates, host store, arena,
+ *     workspace, trace, hidden states) and both streams; they must outlive
+ *     the handle.  The library owns the handle, its HIP events and a small
+ *     pinned mirror; it never frees caller memory.
+ *   - Decode, prefetch, prefill and access calls only enqueue work on the
+ *     streams; errors found while enqueuing are returned at once.  Faults of
+ *     device work are sticky: they are reported by the next synchronising
+ *     call (sync, stats, read_trace, read_state, last_routing, reset) and
+ *     every later call then fails with MOE_ERR_STATE until moe_cache_reset
+ *     succeeds.
+ *   - One handle is used from one host thread at a time.
+ */
+#ifndef MOE_OFFLOAD_H
+#define MOE_OFFLOAD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct moe_cache moe_cache_t; /* opaque, library-owned */
+
+enum { MOE_POLICY_LRU = 0, MOE_POLICY_LFU = 1 };
+enum { MOE_DTYPE_F32 = 0, MOE_DTYPE_BF16 = 1 };
+enum { MOE_OK = 0, MOE_ERR_ARG = -1, MOE_ERR_STATE = -2, MOE_ERR_HIP = -3, MOE_ERR_NOMEM = -4 };
+/* flags of moe_decode_layer */
+enum { MOE_PREFETCH_NEXT = 1 };
+/* how missed experts are copied from the pinned host store into HBM slots */
+enum {
+  MOE_FETCH_KERNEL = 0, /* a copy kernel on the copy stream reads the host store
+                           directly; no host round trip per layer            */
+  MOE_FETCH_DMA = 1     /* the host waits for the routing decision, then issues
+                           one DMA-engine copy per missed expert              */
+};
+
+/* Limits of this build. */
+#define MOE_MAX_EXPERTS 64
+#define MOE_MAX_TOPK 16
+
+typedef struct {
+  int d_model;            /* hidden size d; multiple of 8                            */
+  int d_ff;               /* expert inner size; multiple of 8                        */
+  int top_k;              /* K experts per token, 1 <= K <= min(E, 16)               */
+  int dtype;              /* MOE_DTYPE_* of gates and experts                        */
+  int prefetch_max;       /* at most this many guesses fetched per layer, 0..K      */
+  int fetch_mode;         /* MOE_FETCH_*                                             */
+  int max_prefill_tokens; /* largest T passed to moe_prefill_layer (0: no prefill)   */
+  int reserved;
+  const void *gate_w;        /* device [L][E][d], dtype, row-major                     */
+  const void *host_experts;  /* pinned host [L][E][W1|W3|W2]; W1, W3 [d_ff x d],
+                                W2 [d x d_ff], each row-major (out x in), dtype;
+                                16-byte aligned                                       */
+  void *arena;               /* device [L][S][W1|W3|W2], 16-byte aligned              */
+  void *workspace;           /* device, >= moe_cache_workspace_bytes(), 256-aligned   */
+  size_t workspace_bytes;
+  void *trace;               /* device ring of moe_trace_rec, or NULL for no trace   */
+  size_t trace_cap;          /* records in the ring                                  */
+  void *compute_stream;      /* hipStream_t for router and FFN work (NULL: default)  */
+  void *copy_stream;         /* hipStream_t for expert copies (NULL: compute stream) */
+} moe_model_desc;
+
+/* One trace record.  kind 0 (access): a token's lookup of one of its K
+ * experts; flags bit0 hit, bit1 the hit was a prefetched expert's first use;
+ * slot = slot used, victim = expert evicted (-1 on a hit).
+ * kind 1 (prefetch): one next-layer guess; layer = the guessed layer; flags
+ * bit0 already resident, bit1 fetched now; slot = its slot (-1 if neither),
+ * victim = expert evicted (-1 if none).
+ * kind 2 (prefill): one record per expert after a batched prefill; token =
+ * first token of the batch, rank = tokens routed to the expert, flags bit0
+ * resident before, bit1 resident after, bit2 bytes fetched for it; slot =
+ * slot after (-1 if not resident), victim = expert it replaced (-1 if none).
+ * token is the layer's lookup index (0 for the first token after reset). */
+typedef struct {
+  int32_t kind, token, layer, rank, expert, flags, slot, victim;
+} moe_trace_rec;
+
+typedef struct {
+  uint64_t hits, misses, evictions;                   /* demand lookups           */
+  uint64_t pf_guesses, pf_issued, pf_useful, pf_wasted; /* speculative prefetch   */
+  uint64_t lookups;                                   /* tokens seen by the layer */
+  uint64_t bytes_fetched;                             /* demand + prefetch bytes  */
+} moe_layer_stats;
+
+/* Create a handle for `layers` layers of `experts` experts with `slots` HBM
+ * slots per layer, evicting by `policy` (Sec. 3.1 LRU, Sec. 4.2 LFU).
+ * MOE_ERR_ARG: layers < 1, experts < 1 or > 64, slots < 1 or > experts, bad
+ * policy, out == NULL.  No GPU work. */
+int moe_cache_create(int layers, int experts, int slots, int policy, moe_cache_t **out);
+
+/* Device workspace the handle needs for this model description (bytes);
+ * 0 if the description is invalid. */
+size_t moe_cache_workspace_bytes(const moe_cache_t *c, const moe_model_desc *d);
+
+/* Record buffers, shapes and streams; create events.  MOE_ERR_ARG for an
+ * invalid description (see the field comments; also slots < top_k, a NULL
+ * buffer, a small workspace, misaligned pointers).  Does not reset state:
+ * call moe_cache_reset before the first decode. */
+int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d);
+
+/* Warm start (synchronous): slot s of every layer holds expert s, counts 0,
+ * clocks 0, statistics and trace cleared; experts 0..S-1 are copied into the
+ * slots.  Clears a sticky error. */
+int moe_cache_reset(moe_cache_t *c);
+
+/* One token through one layer (Sec. 2.2): route h [d] (device fp32, updated
+ * in place: h += sum_r g_r FFN_{i_r}(h / rms(h))), look the K experts up in the
+ * layer's cache, fetch the misses from the host store, run the SwiGLU experts.
+ * With MOE_PREFETCH_NEXT and layer + 1 < L, also guess layer+1's experts from
+ * this h and fetch up to prefetch_max of them (Sec. 3.2).  Enqueue only. */
+int moe_decode_layer(moe_cache_t *c, int layer, float *h, int flags);
+
+/* The speculative part alone: guess next_layer's experts from h (device fp32
+ * [d], read only) with next_layer's gate and fetch up to max_experts of them
+ * (0..K).  MOE_ERR_ARG if next_layer is 0 or >= L. Enqueue only. */
+int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts);
+
+/* A batch of `tokens` rows H [tokens][d] (device fp32, in place) through one
+ * layer: every row is routed and computed as a decode token would be; the
+ * layer's cache takes the batch's routing at once (counts += per-expert
+ * routings, then the S highest-ranked experts stay resident).  tokens must be
+ * in 1..max_prefill_tokens. Enqueue only. */
+int moe_prefill_layer(moe_cache_t *c, int layer, float *H, int tokens);
+
+/* Injected routing (test hook): run layer `layer`'s cache lookup, fetches and
+ * trace for the K expert ids at `ids` (device int32 [K], rank order, distinct,
+ * each in [0, E)).  Invalid ids are detected on the device, nothing is
+ * changed, and the next synchronising call returns MOE_ERR_ARG. */
+int moe_cache_access(moe_cache_t *c, int layer, const int *ids);
+
+/* Wait for both streams; report sticky errors. */
+int moe_cache_sync(moe_cache_t *c);
+
+/* Per-layer statistics into out[0..n_layers) (host); n_layers <= L. Syncs. */
+int moe_cache_stats(moe_cache_t *c, moe_layer_stats *out, int n_layers);
+
+/* Copy the trace (oldest first) into out (host, cap records); *n = records
+ * copied.  If more were recorded than the ring holds, the oldest are lost and
+ * *dropped (if non-NULL) says how many.  Syncs. */
+int moe_cache_read_trace(moe_cache_t *c, moe_trace_rec *out, size_t cap, size_t *n,
+                         uint64_t *dropped);
+
+/* One layer's table (host outputs, any may be NULL): slot_expert [S],
+ * expert_slot [E] (-1 if not resident), count [E], last [E], clock. Syncs. */
+int moe_cache_read_state(moe_cache_t *c, int layer, int32_t *slot_expert,
+                         int32_t *expert_slot, uint32_t *count, int64_t *last,
+                         int64_t *clock);
+
+/* Routing of the last decode (K entries) or prefill (tokens * K entries,
+ * token-major) on the compute stream: ids (host int32) and combine weights
+ * g (host fp32), each up to cap entries; *n = entries available. Syncs. */
+int moe_cache_last_routing(moe_cache_t *c, int32_t *ids, float *g, size_t cap, size_t *n);
+
+/* Drain the streams, release events; NULL-safe. */
+void moe_cache_destroy(moe_cache_t *c);
+
+/* Pinned host memory for the expert store (hipHostMalloc); *out is usable
+ * from both host and device.  moe_host_free(NULL) is a no-op. */
+int moe_host_alloc(size_t bytes, void **out);
+int moe_host_free(void *p);
+
+/* Thread-local message of the last failure on this thread ("" if none). */
+const char *moe_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_OFFLOAD_H */

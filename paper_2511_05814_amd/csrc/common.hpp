@@ -1,0 +1,133 @@
+// Internal layout shared by the kernels and the host engine of the MoE
+// offloading library.  Everything here lives in the caller's device
+// workspace; the host engine carves the workspace into these regions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+constexpr int kMaxE = 64;   // experts per layer: one lane per expert in the table wave
+constexpr int kMaxK = 16;   // experts per token
+constexpr int kWave = 64;   // CDNA wavefront
+
+// One layer's cache table.  slot_expert[s] = expert held by slot s;
+// expert_slot[e] = slot of expert e or -1; count = LFU use count (persists
+// across eviction); last = clock tick of the last use or insertion;
+// pf = 1 while a prefetched expert has not yet been used.
+struct LayerTable {
+  int64_t clock;
+  int64_t lookups;
+  int32_t slot_expert[kMaxE];
+  int32_t expert_slot[kMaxE];
+  uint32_t count[kMaxE];
+  int32_t pf[kMaxE];
+  int64_t last[kMaxE];
+};
+
+enum StatIdx {
+  ST_HITS = 0, ST_MISSES, ST_EVICT, ST_PF_GUESS, ST_PF_ISSUED, ST_PF_USEFUL,
+  ST_PF_WASTED, ST_LOOKUPS, ST_BYTES, ST_COUNT
+};
+struct LayerStats {
+  uint64_t v[16];
+};
+
+// Copies the router decided: expert e of `layer` from the host store into
+// slot s of `layer` in the arena.
+struct FetchList {
+  int32_t n;
+  int32_t layer;
+  int32_t expert[kMaxK];
+  int32_t slot[kMaxK];
+  int32_t pad[2];
+};
+
+// Router output consumed by the decode FFN on the compute stream.
+struct RouteOut {
+  int32_t ids[kMaxK];
+  int32_t slot[kMaxK];
+  int32_t hit[kMaxK];
+  float g[kMaxK];
+  float inv_r;
+  int32_t k;
+  int32_t pad[2];
+};
+
+struct TraceRec {
+  int32_t kind, token, layer, rank, expert, flags, slot, victim;
+};
+
+enum { REC_ACCESS = 0, REC_PREFETCH = 1, REC_PREFILL = 2 };
+enum { ERR_NONE = 0, ERR_BAD_IDS = 1, ERR_BAD_LIST = 2 };
+
+struct RouterArgs {
+  const void *gate;        // [L][E][d]
+  const float *h;          // [d]
+  const int32_t *inj_ids;  // injected routing (test hook) or nullptr
+  LayerTable *tables;
+  LayerStats *stats;
+  FetchList *dlists;       // demand list of each layer
+  FetchList *plists;       // prefetch list targeting each layer
+  RouteOut *route;
+  TraceRec *trace;
+  int32_t *err;
+  uint64_t *trace_count;   // records written so far (ring position = count % cap)
+  uint64_t trace_cap;
+  uint64_t expert_bytes;
+  int layer, L, E, S, K, d, dtype, policy;
+  int demand;              // 1: route + look up `layer`
+  int spec_layer;          // >= 0: guess that layer's experts from h and prefetch
+  int pmax;                // prefetch at most this many guesses
+};
+
+struct FfnArgs {
+  const uint8_t *arena;
+  const RouteOut *route;
+  float *h;                // in/out [d]
+  float *act;              // [K][d_ff]
+  float *part;             // [chunks][d]
+  uint32_t *counters;      // [row blocks]
+  uint64_t expert_bytes;
+  int layer, S, K, d, d_ff;
+  int phase;               // up: 0 all ranks, 1 hit ranks, 2 missed ranks
+};
+
+// launchers (one per translation unit that owns the kernel)
+hipError_t launch_router(const RouterArgs &a, hipStream_t s);
+hipError_t launch_fetch(const FetchList *list, const uint8_t *host, uint8_t *arena, int L, int E,
+                        int S, int K, uint64_t expert_bytes, int32_t *err, hipStream_t s);
+hipError_t launch_ffn_up(const FfnArgs &a, int dtype, hipStream_t s);
+hipError_t launch_ffn_down(const FfnArgs &a, int dtype, hipStream_t s);
+int ffn_down_chunks(int K, int d_ff);
+int ffn_down_row_blocks(int d);
+
+// ---------------------------------------------------------------------------
+// device helpers
+
+// 8 bf16 (one 16-byte load) -> 8 fp32; bf16 is the top half of an fp32.
+__device__ __forceinline__ void bf16x8_to_f32(const uint4 v, float *f) {
+  f[0] = __uint_as_float(v.x << 16);
+  f[1] = __uint_as_float(v.x & 0xFFFF0000u);
+  f[2] = __uint_as_float(v.y << 16);
+  f[3] = __uint_as_float(v.y & 0xFFFF0000u);
+  f[4] = __uint_as_float(v.z << 16);
+  f[5] = __uint_as_float(v.z & 0xFFFF0000u);
+  f[6] = __uint_as_float(v.w << 16);
+  f[7] = __uint_as_float(v.w & 0xFFFF0000u);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+}  // namespace moe

@@ -1,0 +1,592 @@
+// Host engine behind the C ABI: argument checks, workspace layout, stream and
+// event choreography, fetch issue, readback of statistics, trace and tables.
+//
+// Per decoded token and layer the engine only enqueues work:
+//   compute stream: router (routing + table update + fetch lists)
+//   copy stream:    wait(router) -> fetch demand misses -> event D[l]
+//                   -> fetch next-layer prefetches -> event P[l+1]
+//   compute stream: wait(D[l]) [, wait(P[l]) if layer l had prefetches]
+//                   -> FFN up -> FFN down (h += y)
+// Every copy waits for the router that chose it, and that router runs after
+// all compute that read the victim slot earlier (stream order), so a slot is
+// never overwritten while an FFN still reads it.  Every FFN waits for the
+// copies that filled its slots (Sec. 6.1 asks for transfers overlapped with
+// compute; here copies of one layer run while other work is queued behind).
+#include "common.hpp"
+#include "moe_offload.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace moe;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Layout {
+  size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, act = 0, part = 0,
+         counters = 0, prefill = 0, total = 0;
+};
+
+bool misaligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) != 0; }
+
+}  // namespace
+
+// prefill support lives in prefill.hip
+namespace moe {
+size_t prefill_workspace_bytes(int K, int d, int d_ff, int E, int T);
+}
+
+struct moe_cache {
+  int L = 0, E = 0, S = 0, policy = 0;
+  bool bound = false;
+  moe_model_desc desc{};
+  int K = 0, d = 0, dff = 0, dtype = 0, pmax = 0, fetch_mode = 0, max_T = 0;
+  uint64_t B = 0;
+  hipStream_t cs = nullptr, xs = nullptr;
+  bool one_stream = true;
+  Layout lay;
+  uint8_t *ws = nullptr;
+  LayerTable *tables = nullptr;
+  LayerStats *stats = nullptr;
+  FetchList *dl = nullptr, *pl = nullptr;
+  RouteOut *route = nullptr;
+  int32_t *err = nullptr;
+  uint64_t *trace_count = nullptr;  // device: records written to the trace ring
+  float *act = nullptr, *part = nullptr;
+  uint32_t *cnt = nullptr;
+  uint8_t *prefill_ws = nullptr;
+  const uint8_t *host_dev = nullptr;  // device address of the pinned host store
+  std::vector<hipEvent_t> ev_demand, ev_pf;
+  hipEvent_t ev_router = nullptr;
+  std::vector<uint8_t> demand_pending, pf_pending;
+  int sticky = MOE_OK;
+  FetchList *mirror = nullptr;  // pinned host copies of two fetch lists (DMA mode)
+  int last_route_kind = 0;      // 0 none, 1 decode, 2 prefill
+  int last_prefill_T = 0;
+};
+
+namespace moe {
+int prefill_enqueue(moe_cache *c, int layer, float *H, int T);
+int prefill_routing(moe_cache *c, int32_t *ids, float *g, size_t cap, size_t *n);
+}  // namespace moe
+
+#define HIP_TRY(c, expr)                                                                  \
+  do {                                                                                    \
+    hipError_t _e = (expr);                                                               \
+    if (_e != hipSuccess) {                                                               \
+      if (c) (c)->sticky = MOE_ERR_HIP;                                                   \
+      return fail(MOE_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(_e));            \
+    }                                                                                     \
+  } while (0)
+
+#define HIP_TRY0(expr)                                                                    \
+  do {                                                                                    \
+    hipError_t _e = (expr);                                                               \
+    if (_e != hipSuccess) return fail(MOE_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(_e)); \
+  } while (0)
+
+static int check_ready(const moe_cache *c) {
+  if (!c) return fail(MOE_ERR_ARG, "NULL handle");
+  if (!c->bound) return fail(MOE_ERR_STATE, "handle is not bound (call moe_cache_bind)");
+  if (c->sticky != MOE_OK)
+    return fail(MOE_ERR_STATE, "an earlier device error is pending; call moe_cache_reset");
+  return MOE_OK;
+}
+
+static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
+  if (!c || !d) return fail(MOE_ERR_ARG, "NULL handle or description");
+  if (d->d_model < 8 || d->d_model % 8 || d->d_model > 16384)
+    return fail(MOE_ERR_ARG, "d_model must be a multiple of 8 in [8, 16384]");
+  if (d->d_ff < 8 || d->d_ff % 8) return fail(MOE_ERR_ARG, "d_ff must be a positive multiple of 8");
+  if (d->top_k < 1 || d->top_k > MOE_MAX_TOPK || d->top_k > c->E)
+    return fail(MOE_ERR_ARG, "top_k must be in [1, min(experts, %d)]", MOE_MAX_TOPK);
+  if (c->S < d->top_k) return fail(MOE_ERR_ARG, "slots (%d) < top_k (%d)", c->S, d->top_k);
+  if (d->dtype != MOE_DTYPE_F32 && d->dtype != MOE_DTYPE_BF16) return fail(MOE_ERR_ARG, "bad dtype");
+  if (d->prefetch_max < 0 || d->prefetch_max > d->top_k)
+    return fail(MOE_ERR_ARG, "prefetch_max must be in [0, top_k]");
+  if (d->fetch_mode != MOE_FETCH_KERNEL && d->fetch_mode != MOE_FETCH_DMA)
+    return fail(MOE_ERR_ARG, "bad fetch_mode");
+  if (d->max_prefill_tokens < 0) return fail(MOE_ERR_ARG, "max_prefill_tokens < 0");
+  return MOE_OK;
+}
+
+static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
+  Layout l;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  l.tables = take(sizeof(LayerTable) * c->L);
+  l.stats = take(sizeof(LayerStats) * c->L);
+  l.dlists = take(sizeof(FetchList) * c->L);
+  l.plists = take(sizeof(FetchList) * c->L);
+  l.route = take(sizeof(RouteOut));
+  l.err = take(256);
+  l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
+  l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff) * d->d_model);
+  l.counters = take(sizeof(uint32_t) * (size_t)ffn_down_row_blocks(d->d_model));
+  l.prefill = take(d->max_prefill_tokens > 0
+                       ? prefill_workspace_bytes(d->top_k, d->d_model, d->d_ff, c->E,
+                                                 d->max_prefill_tokens)
+                       : 0);
+  l.total = off;
+  return l;
+}
+
+extern "C" {
+
+const char *moe_last_error(void) { return g_err.c_str(); }
+
+int moe_cache_create(int layers, int experts, int slots, int policy, moe_cache_t **out) {
+  if (!out) return fail(MOE_ERR_ARG, "out is NULL");
+  *out = nullptr;
+  if (layers < 1) return fail(MOE_ERR_ARG, "layers must be >= 1");
+  if (experts < 1 || experts > MOE_MAX_EXPERTS)
+    return fail(MOE_ERR_ARG, "experts must be in [1, %d]", MOE_MAX_EXPERTS);
+  if (slots < 1 || slots > experts) return fail(MOE_ERR_ARG, "slots must be in [1, experts]");
+  if (policy != MOE_POLICY_LRU && policy != MOE_POLICY_LFU) return fail(MOE_ERR_ARG, "bad policy");
+  moe_cache *c = new (std::nothrow) moe_cache();
+  if (!c) return fail(MOE_ERR_NOMEM, "out of host memory");
+  c->L = layers;
+  c->E = experts;
+  c->S = slots;
+  c->policy = policy;
+  *out = c;
+  return MOE_OK;
+}
+
+size_t moe_cache_workspace_bytes(const moe_cache_t *c, const moe_model_desc *d) {
+  if (validate_desc(c, d) != MOE_OK) return 0;
+  return make_layout(c, d).total;
+}
+
+int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
+  int rc = validate_desc(c, d);
+  if (rc != MOE_OK) return rc;
+  if (c->bound) return fail(MOE_ERR_STATE, "handle is already bound");
+  if (!d->gate_w || !d->host_experts || !d->arena || !d->workspace)
+    return fail(MOE_ERR_ARG, "gate_w, host_experts, arena and workspace must be non-NULL");
+  if (misaligned(d->gate_w, 16) || misaligned(d->host_experts, 16) || misaligned(d->arena, 16))
+    return fail(MOE_ERR_ARG, "gate_w, host_experts and arena must be 16-byte aligned");
+  if (misaligned(d->workspace, 256)) return fail(MOE_ERR_ARG, "workspace must be 256-byte aligned");
+  if (d->trace && (d->trace_cap == 0 || misaligned(d->trace, 16)))
+    return fail(MOE_ERR_ARG, "trace needs trace_cap > 0 and 16-byte alignment");
+  const Layout lay = make_layout(c, d);
+  if (d->workspace_bytes < lay.total)
+    return fail(MOE_ERR_ARG, "workspace too small: %zu < %zu bytes", d->workspace_bytes, lay.total);
+
+  void *dev_host = nullptr;
+  if (d->fetch_mode == MOE_FETCH_KERNEL) {
+    hipError_t e = hipHostGetDevicePointer(&dev_host, const_cast<void *>(d->host_experts), 0);
+    if (e != hipSuccess || !dev_host) {
+      (void)hipGetLastError();
+      return fail(MOE_ERR_ARG, "host_experts is not pinned host memory mapped for the device (%s)",
+                  hipGetErrorString(e));
+    }
+  }
+  c->desc = *d;
+  c->K = d->top_k;
+  c->d = d->d_model;
+  c->dff = d->d_ff;
+  c->dtype = d->dtype;
+  c->pmax = d->prefetch_max;
+  c->fetch_mode = d->fetch_mode;
+  c->max_T = d->max_prefill_tokens;
+  c->B = 3ull * d->d_model * d->d_ff * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
+  c->cs = static_cast<hipStream_t>(d->compute_stream);
+  c->xs = d->copy_stream ? static_cast<hipStream_t>(d->copy_stream) : c->cs;
+  c->one_stream = (c->xs == c->cs);
+  c->lay = lay;
+  c->ws = static_cast<uint8_t *>(d->workspace);
+  c->tables = reinterpret_cast<LayerTable *>(c->ws + lay.tables);
+  c->stats = reinterpret_cast<LayerStats *>(c->ws + lay.stats);
+  c->dl = reinterpret_cast<FetchList *>(c->ws + lay.dlists);
+  c->pl = reinterpret_cast<FetchList *>(c->ws + lay.plists);
+  c->route = reinterpret_cast<RouteOut *>(c->ws + lay.route);
+  c->err = reinterpret_cast<int32_t *>(c->ws + lay.err);
+  c->trace_count = reinterpret_cast<uint64_t *>(c->ws + lay.err + 8);
+  c->act = reinterpret_cast<float *>(c->ws + lay.act);
+  c->part = reinterpret_cast<float *>(c->ws + lay.part);
+  c->cnt = reinterpret_cast<uint32_t *>(c->ws + lay.counters);
+  c->prefill_ws = c->ws + lay.prefill;
+  c->host_dev = static_cast<const uint8_t *>(dev_host);
+
+  c->ev_demand.assign(c->L, nullptr);
+  c->ev_pf.assign(c->L, nullptr);
+  c->demand_pending.assign(c->L, 0);
+  c->pf_pending.assign(c->L, 0);
+  for (int l = 0; l < c->L; ++l) {
+    HIP_TRY0(hipEventCreateWithFlags(&c->ev_demand[l], hipEventDisableTiming));
+    HIP_TRY0(hipEventCreateWithFlags(&c->ev_pf[l], hipEventDisableTiming));
+  }
+  HIP_TRY0(hipEventCreateWithFlags(&c->ev_router, hipEventDisableTiming));
+  HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->mirror), 2 * sizeof(FetchList),
+                                 hipHostMallocDefault));
+  c->bound = true;
+  c->sticky = MOE_ERR_STATE;  // decode needs a reset first
+  return MOE_OK;
+}
+
+int moe_cache_reset(moe_cache_t *c) {
+  if (!c) return fail(MOE_ERR_ARG, "NULL handle");
+  if (!c->bound) return fail(MOE_ERR_STATE, "handle is not bound");
+  (void)hipStreamSynchronize(c->cs);
+  if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
+  (void)hipGetLastError();
+
+  std::vector<LayerTable> t(c->L);
+  std::memset(t.data(), 0, sizeof(LayerTable) * t.size());
+  for (int l = 0; l < c->L; ++l) {
+    for (int s = 0; s < kMaxE; ++s) t[l].slot_expert[s] = s < c->S ? s : -1;
+    for (int e = 0; e < kMaxE; ++e) {
+      const bool res = e < c->S;
+      t[l].expert_slot[e] = res ? e : -1;
+      t[l].last[e] = res ? (int64_t)e - c->S : -(int64_t)c->S - 1;
+    }
+  }
+  HIP_TRY(c, hipMemcpyAsync(c->tables, t.data(), sizeof(LayerTable) * c->L, hipMemcpyHostToDevice, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.stats, 0, c->lay.route - c->lay.stats, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.route, 0, c->lay.act - c->lay.route, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.counters, 0, c->lay.prefill - c->lay.counters, c->cs));
+  HIP_TRY(c, hipStreamSynchronize(c->cs));
+  const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
+  uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
+  for (int l = 0; l < c->L; ++l)
+    for (int s = 0; s < c->S; ++s)
+      HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)l * c->S + s) * c->B, host + ((size_t)l * c->E + s) * c->B,
+                                c->B, hipMemcpyHostToDevice, c->xs));
+  HIP_TRY(c, hipStreamSynchronize(c->xs));
+  std::fill(c->demand_pending.begin(), c->demand_pending.end(), 0);
+  std::fill(c->pf_pending.begin(), c->pf_pending.end(), 0);
+  c->last_route_kind = 0;
+  c->last_prefill_T = 0;
+  c->sticky = MOE_OK;
+  return MOE_OK;
+}
+
+}  // extern "C"
+
+// Issue the copies for one fetch list that the router just wrote.
+static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_t q) {
+  if (c->fetch_mode == MOE_FETCH_KERNEL) {
+    HIP_TRY(c, launch_fetch(list, c->host_dev, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
+                            c->K, c->B, c->err, q));
+    return MOE_OK;
+  }
+  const FetchList &m = c->mirror[mirror_idx];
+  if (m.n < 0 || m.n > c->K || m.layer < 0 || m.layer >= c->L) {
+    c->sticky = MOE_ERR_HIP;
+    return fail(MOE_ERR_HIP, "inconsistent fetch list from the device");
+  }
+  const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
+  uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
+  for (int i = 0; i < m.n; ++i) {
+    const int e = m.expert[i], s = m.slot[i];
+    if (e < 0 || e >= c->E || s < 0 || s >= c->S) {
+      c->sticky = MOE_ERR_HIP;
+      return fail(MOE_ERR_HIP, "inconsistent fetch entry from the device");
+    }
+    HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)m.layer * c->S + s) * c->B,
+                              host + ((size_t)m.layer * c->E + e) * c->B, c->B, hipMemcpyHostToDevice, q));
+  }
+  return MOE_OK;
+}
+
+// Router (+ fetches, + FFN) for one call.  spec_layer < 0: no speculation.
+static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, int demand,
+                         int spec_layer, int pmax, bool ffn) {
+  if (!c->one_stream) {
+    if (demand && c->demand_pending[layer]) HIP_TRY(c, hipStreamWaitEvent(c->cs, c->ev_demand[layer], 0));
+    if (spec_layer >= 0 && c->pf_pending[spec_layer])
+      HIP_TRY(c, hipStreamWaitEvent(c->cs, c->ev_pf[spec_layer], 0));
+  }
+  RouterArgs a{};
+  a.gate = c->desc.gate_w;
+  a.h = h;
+  a.inj_ids = inj;
+  a.tables = c->tables;
+  a.stats = c->stats;
+  a.dlists = c->dl;
+  a.plists = c->pl;
+  a.route = c->route;
+  a.trace = static_cast<TraceRec *>(c->desc.trace);
+  a.err = c->err;
+  a.trace_count = c->trace_count;
+  a.trace_cap = c->desc.trace ? c->desc.trace_cap : 0;
+  a.expert_bytes = c->B;
+  a.layer = layer;
+  a.L = c->L;
+  a.E = c->E;
+  a.S = c->S;
+  a.K = c->K;
+  a.d = c->d;
+  a.dtype = c->dtype;
+  a.policy = c->policy;
+  a.demand = demand;
+  a.spec_layer = spec_layer;
+  a.pmax = pmax;
+  HIP_TRY(c, launch_router(a, c->cs));
+
+  hipStream_t q = c->xs;
+  if (c->fetch_mode == MOE_FETCH_KERNEL) {
+    if (!c->one_stream) {
+      HIP_TRY(c, hipEventRecord(c->ev_router, c->cs));
+      HIP_TRY(c, hipStreamWaitEvent(q, c->ev_router, 0));
+    }
+  } else {
+    if (demand) HIP_TRY(c, hipMemcpyAsync(&c->mirror[0], c->dl + layer, sizeof(FetchList), hipMemcpyDeviceToHost, c->cs));
+    if (spec_layer >= 0)
+      HIP_TRY(c, hipMemcpyAsync(&c->mirror[1], c->pl + spec_layer, sizeof(FetchList), hipMemcpyDeviceToHost, c->cs));
+    HIP_TRY(c, hipStreamSynchronize(c->cs));
+    int32_t e = 0;
+    HIP_TRY(c, hipMemcpy(&e, c->err, sizeof e, hipMemcpyDeviceToHost));
+    if (e != ERR_NONE) return MOE_OK;  // reported at the next synchronising call
+  }
+  if (demand) {
+    int rc = issue_fetch(c, c->dl + layer, 0, q);
+    if (rc != MOE_OK) return rc;
+    if (!c->one_stream) {
+      HIP_TRY(c, hipEventRecord(c->ev_demand[layer], q));
+      c->demand_pending[layer] = 1;
+    }
+  }
+  if (spec_layer >= 0) {
+    int rc = issue_fetch(c, c->pl + spec_layer, 1, q);
+    if (rc != MOE_OK) return rc;
+    if (!c->one_stream) {
+      HIP_TRY(c, hipEventRecord(c->ev_pf[spec_layer], q));
+      c->pf_pending[spec_layer] = 1;
+    }
+  }
+  if (ffn) {
+    if (!c->one_stream) {
+      if (c->demand_pending[layer]) HIP_TRY(c, hipStreamWaitEvent(c->cs, c->ev_demand[layer], 0));
+      if (c->pf_pending[layer]) HIP_TRY(c, hipStreamWaitEvent(c->cs, c->ev_pf[layer], 0));
+      c->demand_pending[layer] = 0;
+      c->pf_pending[layer] = 0;
+    }
+    FfnArgs f{};
+    f.arena = static_cast<const uint8_t *>(c->desc.arena);
+    f.route = c->route;
+    f.h = h;
+    f.act = c->act;
+    f.part = c->part;
+    f.counters = c->cnt;
+    f.expert_bytes = c->B;
+    f.layer = layer;
+    f.S = c->S;
+    f.K = c->K;
+    f.d = c->d;
+    f.d_ff = c->dff;
+    f.phase = 0;
+    HIP_TRY(c, launch_ffn_up(f, c->dtype, c->cs));
+    HIP_TRY(c, launch_ffn_down(f, c->dtype, c->cs));
+    c->last_route_kind = 1;
+  }
+  return MOE_OK;
+}
+
+extern "C" {
+
+int moe_decode_layer(moe_cache_t *c, int layer, float *h, int flags) {
+  int rc = check_ready(c);
+  if (rc != MOE_OK) return rc;
+  if (layer < 0 || layer >= c->L) return fail(MOE_ERR_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (!h || misaligned(h, 16)) return fail(MOE_ERR_ARG, "h must be a non-NULL 16-byte aligned device pointer");
+  if (flags & ~MOE_PREFETCH_NEXT) return fail(MOE_ERR_ARG, "unknown flags 0x%x", flags);
+  const int spec = (flags & MOE_PREFETCH_NEXT) && layer + 1 < c->L ? layer + 1 : -1;
+  return enqueue_layer(c, layer, h, nullptr, 1, spec, c->pmax, true);
+}
+
+int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts) {
+  int rc = check_ready(c);
+  if (rc != MOE_OK) return rc;
+  if (next_layer <= 0 || next_layer >= c->L)
+    return fail(MOE_ERR_ARG, "next_layer %d out of range [1, %d)", next_layer, c->L);
+  if (!h || misaligned(h, 16)) return fail(MOE_ERR_ARG, "h must be a non-NULL 16-byte aligned device pointer");
+  if (max_experts < 0 || max_experts > c->K) return fail(MOE_ERR_ARG, "max_experts must be in [0, top_k]");
+  return enqueue_layer(c, next_layer - 1, const_cast<float *>(h), nullptr, 0, next_layer, max_experts, false);
+}
+
+int moe_cache_access(moe_cache_t *c, int layer, const int *ids) {
+  int rc = check_ready(c);
+  if (rc != MOE_OK) return rc;
+  if (layer < 0 || layer >= c->L) return fail(MOE_ERR_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (!ids) return fail(MOE_ERR_ARG, "ids is NULL");
+  return enqueue_layer(c, layer, nullptr, reinterpret_cast<const int32_t *>(ids), 1, -1, 0, false);
+}
+
+int moe_prefill_layer(moe_cache_t *c, int layer, float *H, int tokens) {
+  int rc = check_ready(c);
+  if (rc != MOE_OK) return rc;
+  if (layer < 0 || layer >= c->L) return fail(MOE_ERR_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (!H || misaligned(H, 16)) return fail(MOE_ERR_ARG, "H must be a non-NULL 16-byte aligned device pointer");
+  if (tokens <= 0 || tokens > c->max_T)
+    return fail(MOE_ERR_ARG, "tokens must be in [1, max_prefill_tokens=%d]", c->max_T);
+  return prefill_enqueue(c, layer, H, tokens);
+}
+
+int moe_cache_sync(moe_cache_t *c) {
+  if (!c) return fail(MOE_ERR_ARG, "NULL handle");
+  if (!c->bound) return fail(MOE_ERR_STATE, "handle is not bound");
+  hipError_t e1 = hipStreamSynchronize(c->cs);
+  hipError_t e2 = c->one_stream ? hipSuccess : hipStreamSynchronize(c->xs);
+  if (e1 != hipSuccess || e2 != hipSuccess) {
+    c->sticky = MOE_ERR_HIP;
+    return fail(MOE_ERR_HIP, "stream synchronize failed: %s",
+                hipGetErrorString(e1 != hipSuccess ? e1 : e2));
+  }
+  if (c->sticky == MOE_ERR_STATE) return fail(MOE_ERR_STATE, "handle needs moe_cache_reset");
+  if (c->sticky != MOE_OK) return fail(c->sticky, "an earlier device error is pending");
+  int32_t e = 0;
+  HIP_TRY(c, hipMemcpy(&e, c->err, sizeof e, hipMemcpyDeviceToHost));
+  if (e == ERR_BAD_IDS) {
+    const int32_t zero = 0;
+    HIP_TRY(c, hipMemcpy(c->err, &zero, sizeof zero, hipMemcpyHostToDevice));
+    return fail(MOE_ERR_ARG, "injected expert ids were invalid (out of range or repeated); nothing changed");
+  }
+  if (e != ERR_NONE) {
+    c->sticky = MOE_ERR_HIP;
+    return fail(MOE_ERR_HIP, "device reported an inconsistent fetch list (code %d)", e);
+  }
+  return MOE_OK;
+}
+
+int moe_cache_stats(moe_cache_t *c, moe_layer_stats *out, int n_layers) {
+  int rc = moe_cache_sync(c);
+  if (rc != MOE_OK) return rc;
+  if (!out || n_layers < 0 || n_layers > c->L) return fail(MOE_ERR_ARG, "bad output or n_layers");
+  std::vector<LayerStats> s(c->L);
+  HIP_TRY(c, hipMemcpy(s.data(), c->stats, sizeof(LayerStats) * c->L, hipMemcpyDeviceToHost));
+  for (int l = 0; l < n_layers; ++l) {
+    moe_layer_stats &o = out[l];
+    o.hits = s[l].v[ST_HITS];
+    o.misses = s[l].v[ST_MISSES];
+    o.evictions = s[l].v[ST_EVICT];
+    o.pf_guesses = s[l].v[ST_PF_GUESS];
+    o.pf_issued = s[l].v[ST_PF_ISSUED];
+    o.pf_useful = s[l].v[ST_PF_USEFUL];
+    o.pf_wasted = s[l].v[ST_PF_WASTED];
+    o.lookups = s[l].v[ST_LOOKUPS];
+    o.bytes_fetched = s[l].v[ST_BYTES];
+  }
+  return MOE_OK;
+}
+
+int moe_cache_read_trace(moe_cache_t *c, moe_trace_rec *out, size_t cap, size_t *n, uint64_t *dropped) {
+  int rc = moe_cache_sync(c);
+  if (rc != MOE_OK) return rc;
+  if (!n || (!out && cap)) return fail(MOE_ERR_ARG, "bad output pointers");
+  *n = 0;
+  if (dropped) *dropped = 0;
+  if (!c->desc.trace) return MOE_OK;
+  uint64_t total = 0;
+  HIP_TRY(c, hipMemcpy(&total, c->trace_count, sizeof total, hipMemcpyDeviceToHost));
+  const uint64_t ring = c->desc.trace_cap;
+  const uint64_t avail = total < ring ? total : ring;
+  const uint64_t start = total - avail;
+  const uint64_t want = avail < cap ? avail : cap;
+  const moe_trace_rec *dev = static_cast<const moe_trace_rec *>(c->desc.trace);
+  uint64_t done = 0;
+  while (done < want) {
+    const uint64_t at = (start + done) % ring;
+    uint64_t chunk = ring - at;
+    if (chunk > want - done) chunk = want - done;
+    HIP_TRY(c, hipMemcpy(out + done, dev + at, chunk * sizeof(moe_trace_rec), hipMemcpyDeviceToHost));
+    done += chunk;
+  }
+  *n = (size_t)want;
+  if (dropped) *dropped = start;
+  return MOE_OK;
+}
+
+int moe_cache_read_state(moe_cache_t *c, int layer, int32_t *slot_expert, int32_t *expert_slot,
+                         uint32_t *count, int64_t *last, int64_t *clock) {
+  int rc = moe_cache_sync(c);
+  if (rc != MOE_OK) return rc;
+  if (layer < 0 || layer >= c->L) return fail(MOE_ERR_ARG, "layer out of range");
+  LayerTable t;
+  HIP_TRY(c, hipMemcpy(&t, c->tables + layer, sizeof t, hipMemcpyDeviceToHost));
+  if (slot_expert) std::memcpy(slot_expert, t.slot_expert, sizeof(int32_t) * c->S);
+  if (expert_slot) std::memcpy(expert_slot, t.expert_slot, sizeof(int32_t) * c->E);
+  if (count) std::memcpy(count, t.count, sizeof(uint32_t) * c->E);
+  if (last) std::memcpy(last, t.last, sizeof(int64_t) * c->E);
+  if (clock) *clock = t.clock;
+  return MOE_OK;
+}
+
+int moe_cache_last_routing(moe_cache_t *c, int32_t *ids, float *g, size_t cap, size_t *n) {
+  int rc = moe_cache_sync(c);
+  if (rc != MOE_OK) return rc;
+  if (!n) return fail(MOE_ERR_ARG, "n is NULL");
+  *n = 0;
+  if (c->last_route_kind == 1) {
+    RouteOut r;
+    HIP_TRY(c, hipMemcpy(&r, c->route, sizeof r, hipMemcpyDeviceToHost));
+    const size_t m = (size_t)c->K < cap ? (size_t)c->K : cap;
+    if (ids) std::memcpy(ids, r.ids, m * sizeof(int32_t));
+    if (g) std::memcpy(g, r.g, m * sizeof(float));
+    *n = (size_t)c->K;
+    return MOE_OK;
+  }
+  if (c->last_route_kind == 2) return prefill_routing(c, ids, g, cap, n);
+  return MOE_OK;
+}
+
+void moe_cache_destroy(moe_cache_t *c) {
+  if (!c) return;
+  if (c->bound) {
+    (void)hipStreamSynchronize(c->cs);
+    if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
+    for (hipEvent_t e : c->ev_demand)
+      if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : c->ev_pf)
+      if (e) (void)hipEventDestroy(e);
+    if (c->ev_router) (void)hipEventDestroy(c->ev_router);
+    if (c->mirror) (void)hipHostFree(c->mirror);
+    (void)hipGetLastError();
+  }
+  delete c;
+}
+
+int moe_host_alloc(size_t bytes, void **out) {
+  if (!out || bytes == 0) return fail(MOE_ERR_ARG, "bad arguments");
+  *out = nullptr;
+  hipError_t e = hipHostMalloc(out, bytes, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *out = nullptr;
+    return fail(MOE_ERR_NOMEM, "hipHostMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+  }
+  return MOE_OK;
+}
+
+int moe_host_free(void *p) {
+  if (!p) return MOE_OK;
+  hipError_t e = hipHostFree(p);
+  if (e != hipSuccess) return fail(MOE_ERR_HIP, "hipHostFree failed: %s", hipGetErrorString(e));
+  return MOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,214 @@
+// Decode expert FFN (SwiGLU) over the experts resident in HBM slots.
+//
+// For a batch-1 token the K selected experts are matrix-vector products, so
+// the work is bound by streaming the expert weights from HBM: 3 d d_ff
+// elements per expert against 2 flops per element.  MFMA is no help here;
+// the kernels are built for bandwidth instead: every lane issues 16-byte
+// loads, each wave streams several rows at once, the activation vector sits
+// in LDS, and both ranks (all K experts) go into one launch.
+//
+//   up:   act_r = SiLU(W1_r x) * (W3_r x),  x = h / rms(h)      (per rank r)
+//   down: h  += sum_r g_r W2_r act_r
+//
+// The down projection is split along its reduction axis (rank, column chunk)
+// so that enough workgroups stream at once; each chunk writes a partial row
+// sum and the last workgroup to finish a row block adds the partials in a
+// fixed order, so the result does not depend on scheduling.
+#include "common.hpp"
+
+namespace moe {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWavesPerBlock = kThreads / kWave;
+constexpr int kRowsPerWave = 4;
+constexpr int kRowsPerBlock = kWavesPerBlock * kRowsPerWave;  // 16
+constexpr int kDownChunk = 2048;                              // columns per down chunk
+
+template <int DT>
+struct Elem;
+template <>
+struct Elem<0> {  // fp32
+  using T = float;
+  static constexpr int kVec = 4;
+  __device__ static __forceinline__ void load(const float *p, float *f) {
+    const float4 v = *reinterpret_cast<const float4 *>(p);
+    f[0] = v.x;
+    f[1] = v.y;
+    f[2] = v.z;
+    f[3] = v.w;
+  }
+};
+template <>
+struct Elem<1> {  // bf16 stored as raw 16-bit patterns
+  using T = uint16_t;
+  static constexpr int kVec = 8;
+  __device__ static __forceinline__ void load(const uint16_t *p, float *f) {
+    bf16x8_to_f32(*reinterpret_cast<const uint4 *>(p), f);
+  }
+};
+
+__device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void ffn_up_kernel(FfnArgs a) {
+  using E = Elem<DT>;
+  using T = typename E::T;
+  constexpr int V = E::kVec;
+  extern __shared__ float xs[];
+  const int bpr = (a.d_ff + kRowsPerBlock - 1) / kRowsPerBlock;
+  const int rank = blockIdx.x / bpr;
+  const int rb = blockIdx.x - rank * bpr;
+  if (rank >= a.route->k) return;
+  const int hit = a.route->hit[rank];
+  if ((a.phase == 1 && !hit) || (a.phase == 2 && hit)) return;
+  const int slot = a.route->slot[rank];
+  if (slot < 0 || slot >= a.S) return;
+
+  const int d = a.d, d_ff = a.d_ff;
+  const float inv_r = a.route->inv_r;
+  for (int i = threadIdx.x; i < d; i += kThreads) xs[i] = a.h[i] * inv_r;
+  __syncthreads();
+
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const T *w1 = reinterpret_cast<const T *>(a.arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes);
+  const T *w3 = w1 + (size_t)d_ff * d;
+  const int row0 = rb * kRowsPerBlock + wave * kRowsPerWave;
+  int nrows = d_ff - row0;
+  nrows = nrows < 0 ? 0 : (nrows > kRowsPerWave ? kRowsPerWave : nrows);
+
+  float acc1[kRowsPerWave] = {}, acc3[kRowsPerWave] = {};
+  for (int c = lane * V; c < d; c += kWave * V) {
+    float x[V];
+#pragma unroll
+    for (int v = 0; v < V; v += 4) {
+      const float4 t = *reinterpret_cast<const float4 *>(xs + c + v);
+      x[v] = t.x;
+      x[v + 1] = t.y;
+      x[v + 2] = t.z;
+      x[v + 3] = t.w;
+    }
+#pragma unroll
+    for (int q = 0; q < kRowsPerWave; ++q) {
+      if (q < nrows) {
+        float f1[V], f3[V];
+        E::load(w1 + (size_t)(row0 + q) * d + c, f1);
+        E::load(w3 + (size_t)(row0 + q) * d + c, f3);
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          acc1[q] = fmaf(f1[v], x[v], acc1[q]);
+          acc3[q] = fmaf(f3[v], x[v], acc3[q]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kRowsPerWave; ++q) {
+    const float s1 = wave_sum(acc1[q]);
+    const float s3 = wave_sum(acc3[q]);
+    if (lane == 0 && q < nrows) a.act[(size_t)rank * d_ff + row0 + q] = silu(s1) * s3;
+  }
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void ffn_down_kernel(FfnArgs a) {
+  using E = Elem<DT>;
+  using T = typename E::T;
+  constexpr int V = E::kVec;
+  __shared__ float as[kDownChunk];
+  __shared__ int s_last;
+  const int d = a.d, d_ff = a.d_ff, K = a.route->k;
+  const int cpr = (d_ff + kDownChunk - 1) / kDownChunk;
+  const int nch = a.K * cpr;
+  const int rb = blockIdx.x / nch;
+  const int ch = blockIdx.x - rb * nch;
+  const int rank = ch / cpr;
+  const int c0 = (ch - rank * cpr) * kDownChunk;
+  const int c1 = min(c0 + kDownChunk, d_ff);
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int row0 = rb * kRowsPerBlock + wave * kRowsPerWave;
+  int nrows = d - row0;
+  nrows = nrows < 0 ? 0 : (nrows > kRowsPerWave ? kRowsPerWave : nrows);
+
+  const int slot = rank < K ? a.route->slot[rank] : -1;
+  const bool valid = rank < K && slot >= 0 && slot < a.S;
+  float acc[kRowsPerWave] = {};
+  if (valid) {
+    const float g = a.route->g[rank];
+    const float *act = a.act + (size_t)rank * d_ff + c0;
+    for (int i = threadIdx.x; i < c1 - c0; i += kThreads) as[i] = g * act[i];
+    __syncthreads();
+    const T *w2 = reinterpret_cast<const T *>(a.arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes) +
+                  2 * (size_t)d_ff * d;
+    for (int c = c0 + lane * V; c < c1; c += kWave * V) {
+      float x[V];
+#pragma unroll
+      for (int v = 0; v < V; v += 4) {
+        const float4 t = *reinterpret_cast<const float4 *>(as + (c - c0) + v);
+        x[v] = t.x;
+        x[v + 1] = t.y;
+        x[v + 2] = t.z;
+        x[v + 3] = t.w;
+      }
+#pragma unroll
+      for (int q = 0; q < kRowsPerWave; ++q) {
+        if (q < nrows) {
+          float f[V];
+          E::load(w2 + (size_t)(row0 + q) * d_ff + c, f);
+#pragma unroll
+          for (int v = 0; v < V; ++v) acc[q] = fmaf(f[v], x[v], acc[q]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kRowsPerWave; ++q) {
+    const float s = wave_sum(acc[q]);
+    if (lane == 0 && q < nrows) a.part[(size_t)ch * d + row0 + q] = s;
+  }
+  // Publish this chunk's partials; the last chunk of the row block sums them.
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned prev = atomicAdd(a.counters + rb, 1u);
+    s_last = (prev == (unsigned)(nch - 1));
+  }
+  __syncthreads();
+  if (s_last) {
+    __threadfence();
+    const int row = rb * kRowsPerBlock + threadIdx.x;
+    if (threadIdx.x < kRowsPerBlock && row < d) {
+      float sum = 0.0f;
+      for (int c = 0; c < nch; ++c) sum += a.part[(size_t)c * d + row];
+      a.h[row] += sum;
+    }
+    if (threadIdx.x == 0) a.counters[rb] = 0u;
+  }
+}
+
+}  // namespace
+
+int ffn_down_chunks(int K, int d_ff) { return K * ((d_ff + kDownChunk - 1) / kDownChunk); }
+int ffn_down_row_blocks(int d) { return (d + kRowsPerBlock - 1) / kRowsPerBlock; }
+
+hipError_t launch_ffn_up(const FfnArgs &a, int dtype, hipStream_t s) {
+  const int bpr = (a.d_ff + kRowsPerBlock - 1) / kRowsPerBlock;
+  const dim3 grid(a.K * bpr);
+  const size_t lds = (size_t)a.d * sizeof(float);
+  if (dtype == 1)
+    hipLaunchKernelGGL(ffn_up_kernel<1>, grid, dim3(kThreads), lds, s, a);
+  else
+    hipLaunchKernelGGL(ffn_up_kernel<0>, grid, dim3(kThreads), lds, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ffn_down(const FfnArgs &a, int dtype, hipStream_t s) {
+  const dim3 grid(ffn_down_row_blocks(a.d) * ffn_down_chunks(a.K, a.d_ff));
+  if (dtype == 1)
+    hipLaunchKernelGGL(ffn_down_kernel<1>, grid, dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(ffn_down_kernel<0>, grid, dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace moe

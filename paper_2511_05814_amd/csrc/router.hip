@@ -1,0 +1,405 @@
+// Router and cache-table kernel for batch-1 decode.
+//
+// One workgroup per call.  All 16 waves first compute the gate logits
+// z = W_g h (Sec. 4.3: the gate is a linear map [len_hidden, num_experts]) for
+// the layer being decoded and, when speculating, for the next layer (Sec. 3.2:
+// the next layer's gate applied to the current hidden state).  Each product
+// of a bf16/fp32 weight and an fp32 activation is exact in fp64, and the sums
+// are accumulated in fp64 so that the top-K decision is the one an fp64
+// evaluation makes.
+//
+// Then one wave owns each cache table: lane e holds expert e's slot, use count,
+// last-use tick and prefetched flag, and the K lookups of the token are
+// applied in rank order with wave-wide argmin reductions choosing the victim
+// (LRU, Sec. 3.1: smallest last-use tick; LFU, Sec. 4.2: smallest count, then
+// last-use tick; then lower slot).  Wave 0 serves the demand lookup of this
+// layer, wave 1 the speculative insertion into the next layer's table; the
+// tables are disjoint, so the two run concurrently.
+#include "common.hpp"
+
+#include <math.h>
+
+namespace moe {
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / kWave;
+
+__device__ double gate_row_dot(const void *gate, int dtype, size_t row_off, const float *h, int d,
+                               int lane) {
+  double acc = 0.0;
+  if (dtype == 1) {  // bf16
+    const uint16_t *w = static_cast<const uint16_t *>(gate) + row_off;
+    for (int c = lane * 8; c < d; c += kWave * 8) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(w + c);
+      float f[8];
+      bf16x8_to_f32(v, f);
+      const float4 h0 = *reinterpret_cast<const float4 *>(h + c);
+      const float4 h1 = *reinterpret_cast<const float4 *>(h + c + 4);
+      acc = fma((double)f[0], (double)h0.x, acc);
+      acc = fma((double)f[1], (double)h0.y, acc);
+      acc = fma((double)f[2], (double)h0.z, acc);
+      acc = fma((double)f[3], (double)h0.w, acc);
+      acc = fma((double)f[4], (double)h1.x, acc);
+      acc = fma((double)f[5], (double)h1.y, acc);
+      acc = fma((double)f[6], (double)h1.z, acc);
+      acc = fma((double)f[7], (double)h1.w, acc);
+    }
+  } else {  // fp32
+    const float *w = static_cast<const float *>(gate) + row_off;
+    for (int c = lane * 4; c < d; c += kWave * 4) {
+      const float4 v = *reinterpret_cast<const float4 *>(w + c);
+      const float4 hv = *reinterpret_cast<const float4 *>(h + c);
+      acc = fma((double)v.x, (double)hv.x, acc);
+      acc = fma((double)v.y, (double)hv.y, acc);
+      acc = fma((double)v.z, (double)hv.z, acc);
+      acc = fma((double)v.w, (double)hv.w, acc);
+    }
+  }
+  return wave_sum_d(acc);
+}
+
+// Top-K over lanes < E holding z (rank order: larger z first, lower id on
+// ties; NaN ranks as -inf).  Lane r < K receives the id of rank r.
+__device__ int wave_topk(double z, int E, int K, int lane) {
+  const double NEG = -INFINITY;
+  bool avail = lane < E;
+  const double key = (z != z) ? NEG : z;
+  int mine = -1;
+  for (int r = 0; r < K; ++r) {
+    double bz = avail ? key : NEG;
+    int bl = avail ? lane : 1000 + lane;
+    int bv = avail ? 1 : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const double oz = __shfl_xor(bz, o, kWave);
+      const int ol = __shfl_xor(bl, o, kWave);
+      const int ov = __shfl_xor(bv, o, kWave);
+      const bool take = (ov && !bv) || (ov == bv && (oz > bz || (oz == bz && ol < bl)));
+      if (take) {
+        bz = oz;
+        bl = ol;
+        bv = ov;
+      }
+    }
+    if (lane == r) mine = bl;
+    if (lane == bl) avail = false;
+  }
+  return mine;
+}
+
+// Lane of the resident, unpinned expert with the smallest policy key
+// (LFU: count, last, slot; LRU: last, slot), or -1 if there is none.
+__device__ int wave_victim(bool cand, int policy, uint32_t count, int64_t last, int slot) {
+  uint32_t k1 = (cand && policy == 1) ? count : 0u;
+  int64_t k2 = last;
+  int k3 = slot;
+  int bl = threadIdx.x & (kWave - 1);
+  int bv = cand ? 1 : 0;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t o1 = __shfl_xor(k1, o, kWave);
+    const int64_t o2 = __shfl_xor(k2, o, kWave);
+    const int o3 = __shfl_xor(k3, o, kWave);
+    const int ol = __shfl_xor(bl, o, kWave);
+    const int ov = __shfl_xor(bv, o, kWave);
+    bool less;
+    if (ov != bv) {
+      less = ov > bv;
+    } else {
+      less = (o1 < k1) || (o1 == k1 && (o2 < k2 || (o2 == k2 && (o3 < k3 || (o3 == k3 && ol < bl)))));
+    }
+    if (less) {
+      k1 = o1;
+      k2 = o2;
+      k3 = o3;
+      bl = ol;
+      bv = ov;
+    }
+  }
+  return bv ? bl : -1;
+}
+
+__device__ void put_rec(const RouterArgs &a, uint64_t idx, int kind, int64_t token, int layer,
+                        int rank, int expert, int flags, int slot, int victim) {
+  if (a.trace == nullptr || a.trace_cap == 0) return;
+  TraceRec r;
+  r.kind = kind;
+  r.token = (int32_t)token;
+  r.layer = layer;
+  r.rank = rank;
+  r.expert = expert;
+  r.flags = flags;
+  r.slot = slot;
+  r.victim = victim;
+  a.trace[idx % a.trace_cap] = r;
+}
+
+// Wave 0: the token's K lookups in layer a.layer, in rank order.
+// `idreg` on lane r < K holds the expert of rank r.
+__device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t rec_base) {
+  LayerTable *T = a.tables + a.layer;
+  LayerStats *st = a.stats + a.layer;
+  FetchList *fl = a.dlists + a.layer;
+  const int E = a.E, K = a.K;
+  const bool in_range = lane < E;
+  int my_slot = in_range ? T->expert_slot[lane] : -1;
+  uint32_t my_count = in_range ? T->count[lane] : 0u;
+  int64_t my_last = in_range ? T->last[lane] : 0;
+  int my_pf = in_range ? T->pf[lane] : 0;
+  int64_t clock = T->clock;
+  const int64_t token = T->lookups;
+
+  bool pinned = false;
+  for (int r = 0; r < K; ++r) pinned |= (__shfl(idreg, r, kWave) == lane);
+
+  int n_miss = 0, hits = 0, useful = 0, wasted = 0;
+  for (int r = 0; r < K; ++r) {
+    const int j = __shfl(idreg, r, kWave);
+    clock += 1;
+    const int slot_j = __shfl(my_slot, j, kWave);
+    const int pf_j = __shfl(my_pf, j, kWave);
+    if (lane == j) {
+      my_count += 1;
+      my_last = clock;
+    }
+    int flags, slot, victim;
+    if (slot_j >= 0) {
+      flags = 1 | (pf_j ? 2 : 0);
+      if (pf_j) {
+        useful += 1;
+        if (lane == j) my_pf = 0;
+      }
+      slot = slot_j;
+      victim = -1;
+      hits += 1;
+    } else {
+      const bool cand = in_range && my_slot >= 0 && !pinned;
+      const int v = wave_victim(cand, a.policy, my_count, my_last, my_slot);
+      if (v < 0) {  // cannot happen with slots >= K; refuse rather than corrupt
+        if (lane == 0) *a.err = ERR_BAD_LIST;
+        break;
+      }
+      const int s = __shfl(my_slot, v, kWave);
+      const int pf_v = __shfl(my_pf, v, kWave);
+      if (pf_v) wasted += 1;
+      if (lane == v) {
+        my_slot = -1;
+        my_pf = 0;
+      }
+      if (lane == j) my_slot = s;
+      if (lane == 0) {
+        T->slot_expert[s] = j;
+        fl->expert[n_miss] = j;
+        fl->slot[n_miss] = s;
+      }
+      n_miss += 1;
+      flags = 0;
+      slot = s;
+      victim = v;
+    }
+    if (lane == 0) {
+      a.route->ids[r] = j;
+      a.route->slot[r] = slot;
+      a.route->hit[r] = flags & 1;
+      put_rec(a, rec_base + r, REC_ACCESS, token, a.layer, r, j, flags, slot, victim);
+    }
+  }
+  // prefetched experts this token did not use are wasted
+  const unsigned long long left = __ballot(in_range && my_pf != 0);
+  wasted += __popcll(left);
+  my_pf = 0;
+
+  if (in_range) {
+    T->expert_slot[lane] = my_slot;
+    T->count[lane] = my_count;
+    T->last[lane] = my_last;
+    T->pf[lane] = my_pf;
+  }
+  if (lane == 0) {
+    T->clock = clock;
+    T->lookups += 1;
+    fl->n = n_miss;
+    fl->layer = a.layer;
+    a.route->k = K;
+    st->v[ST_HITS] += hits;
+    st->v[ST_MISSES] += n_miss;
+    st->v[ST_EVICT] += n_miss;
+    st->v[ST_PF_USEFUL] += useful;
+    st->v[ST_PF_WASTED] += wasted;
+    st->v[ST_LOOKUPS] += 1;
+    st->v[ST_BYTES] += (uint64_t)n_miss * a.expert_bytes;
+  }
+}
+
+// Wave 1: insert up to pmax of the K guesses (lane r holds rank r's guess)
+// into the table of a.spec_layer, all guesses pinned.
+__device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_t rec_base) {
+  const int L2 = a.spec_layer;
+  LayerTable *T = a.tables + L2;
+  LayerStats *st = a.stats + L2;
+  FetchList *fl = a.plists + L2;
+  const int E = a.E, K = a.K;
+  const bool in_range = lane < E;
+  int my_slot = in_range ? T->expert_slot[lane] : -1;
+  uint32_t my_count = in_range ? T->count[lane] : 0u;
+  int64_t my_last = in_range ? T->last[lane] : 0;
+  int my_pf = in_range ? T->pf[lane] : 0;
+  int64_t clock = T->clock;
+  const int64_t token = T->lookups;
+
+  bool pinned = false;
+  for (int r = 0; r < K; ++r) pinned |= (__shfl(greg, r, kWave) == lane);
+
+  int issued = 0, wasted = 0;
+  for (int r = 0; r < K; ++r) {
+    const int j = __shfl(greg, r, kWave);
+    const int slot_j = __shfl(my_slot, j, kWave);
+    int flags = 0, slot = -1, victim = -1;
+    if (slot_j >= 0) {
+      flags = 1;
+      slot = slot_j;
+    } else if (issued < a.pmax) {
+      clock += 1;
+      const bool cand = in_range && my_slot >= 0 && !pinned;
+      const int v = wave_victim(cand, a.policy, my_count, my_last, my_slot);
+      if (v < 0) {
+        if (lane == 0) *a.err = ERR_BAD_LIST;
+        break;
+      }
+      const int s = __shfl(my_slot, v, kWave);
+      const int pf_v = __shfl(my_pf, v, kWave);
+      if (pf_v) wasted += 1;
+      if (lane == v) {
+        my_slot = -1;
+        my_pf = 0;
+      }
+      if (lane == j) {
+        my_slot = s;
+        my_last = clock;
+        my_pf = 1;
+      }
+      if (lane == 0) {
+        T->slot_expert[s] = j;
+        fl->expert[issued] = j;
+        fl->slot[issued] = s;
+      }
+      issued += 1;
+      flags = 2;
+      slot = s;
+      victim = v;
+    }
+    if (lane == 0) put_rec(a, rec_base + r, REC_PREFETCH, token, L2, r, j, flags, slot, victim);
+  }
+  if (in_range) {
+    T->expert_slot[lane] = my_slot;
+    T->last[lane] = my_last;
+    T->pf[lane] = my_pf;
+  }
+  if (lane == 0) {
+    T->clock = clock;
+    fl->n = issued;
+    fl->layer = L2;
+    st->v[ST_PF_GUESS] += K;
+    st->v[ST_PF_ISSUED] += issued;
+    st->v[ST_PF_WASTED] += wasted;
+    st->v[ST_BYTES] += (uint64_t)issued * a.expert_bytes;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
+  __shared__ double zs[2 * kMaxE];
+  __shared__ double red[kWaves];
+  __shared__ double s_rms;
+  __shared__ uint64_t s_tbase;
+  __shared__ int s_demand_ok;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int E = a.E, d = a.d;
+  const bool route_here = a.demand && a.inj_ids == nullptr;
+  const bool spec = a.spec_layer >= 0;
+
+  for (int row = wave; row < 2 * E; row += kWaves) {
+    const bool first = row < E;
+    if (first && !route_here) continue;
+    if (!first && !spec) continue;
+    const int gl = first ? a.layer : a.spec_layer;
+    const int e = first ? row : row - E;
+    const double z = gate_row_dot(a.gate, a.dtype, ((size_t)gl * E + e) * (size_t)d, a.h, d, lane);
+    if (lane == 0) zs[row] = z;
+  }
+  if (tid == 0) {
+    s_tbase = a.trace ? *a.trace_count : 0;
+    s_demand_ok = 0;
+  }
+  if (route_here) {
+    double ss = 0.0;
+    for (int i = tid; i < d; i += kThreads) {
+      const double v = a.h[i];
+      ss = fma(v, v, ss);
+    }
+    ss = wave_sum_d(ss);
+    if (lane == 0) red[wave] = ss;
+  }
+  __syncthreads();
+  if (route_here && tid == 0) {
+    double t = 0.0;
+    for (int w = 0; w < kWaves; ++w) t += red[w];
+    s_rms = sqrt(t / (double)d + 1e-5);
+  }
+  __syncthreads();
+
+  if (wave == 0 && a.demand) {
+    int idreg;
+    if (route_here) {
+      idreg = wave_topk(lane < E ? zs[lane] : 0.0, E, a.K, lane);
+      // renormalised softmax over the selected logits z / rms (rank 0 is the max)
+      double zr = (lane < a.K) ? zs[idreg < 0 ? 0 : idreg] : 0.0;
+      const double r = s_rms;
+      const double z0 = __shfl(zr, 0, kWave);
+      const double ex = (lane < a.K) ? exp((zr - z0) / r) : 0.0;
+      const double den = wave_sum_d(ex);
+      if (lane < a.K) a.route->g[lane] = (float)(ex / den);
+      if (lane == 0) a.route->inv_r = (float)(1.0 / r);
+    } else {
+      idreg = (lane < a.K) ? a.inj_ids[lane] : -1;
+      bool ok = true;
+      for (int r = 0; r < a.K; ++r) {
+        const int j = __shfl(idreg, r, kWave);
+        const unsigned long long same = __ballot(lane < a.K && idreg == j);
+        ok = ok && j >= 0 && j < E && __popcll(same) == 1;
+      }
+      if (!ok) {
+        if (lane == 0) {
+          *a.err = ERR_BAD_IDS;
+          a.dlists[a.layer].n = 0;
+          a.dlists[a.layer].layer = a.layer;
+          a.route->k = 0;
+        }
+        idreg = -1;
+      } else {
+        if (lane < a.K) a.route->g[lane] = 0.0f;
+        if (lane == 0) a.route->inv_r = 0.0f;
+      }
+    }
+    if (__shfl(idreg, 0, kWave) >= 0) {
+      demand_lookup(a, idreg, lane, s_tbase);
+      if (lane == 0) s_demand_ok = 1;
+    }
+  }
+  if (wave == 1 && spec) {
+    const int greg = wave_topk(lane < E ? zs[E + lane] : 0.0, E, a.K, lane);
+    prefetch_insert(a, greg, lane, s_tbase + (a.demand ? (uint64_t)a.K : 0));
+  }
+  __syncthreads();
+  if (tid == 0 && a.trace)
+    *a.trace_count = s_tbase + (s_demand_ok ? (uint64_t)a.K : 0) + (spec ? (uint64_t)a.K : 0);
+}
+
+}  // namespace
+
+hipError_t launch_router(const RouterArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(router_kernel, dim3(1), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,181 @@
+"""Buffers and streams around the C ABI, allocated with PyTorch (plumbing only).
+
+* `HostStore`  pinned host memory holding every expert, [L][E][W1|W3|W2]
+* `DeviceGates` the gate tensor [L][E][d] in HBM
+* `OffloadedMoE` one cache handle: its HBM slot arena, workspace, trace ring
+  and two streams (compute and copy), plus thin loops that call
+  moe_decode_layer / moe_prefill_layer for every layer.
+
+All arithmetic of the decode path runs in the HIP library; this module only
+allocates, fills inputs and calls the binding.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional
+
+import numpy as np
+
+from . import binding as b
+from . import workload as wl
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        raise RuntimeError("a ROCm GPU is required for the HIP decode path")
+    return torch
+
+
+class HostStore:
+    """Pinned host store of all experts, filled from the seeded generator."""
+
+    def __init__(self, cfg: wl.Config, fill: bool = True, workers: Optional[int] = None):
+        self.cfg = cfg
+        self.nbytes = cfg.layers * cfg.experts * cfg.expert_bytes
+        self.ptr = b.moe_host_alloc(self.nbytes)
+        self.array = np.ctypeslib.as_array((ctypes.c_uint8 * self.nbytes).from_address(self.ptr))
+        if fill:
+            wl.fill_host_store(cfg, self.array, workers=workers)
+
+    def expert(self, layer: int, expert: int) -> np.ndarray:
+        """Storage-dtype view of one expert (W1|W3|W2)."""
+        cfg = self.cfg
+        off = (layer * cfg.experts + expert) * cfg.expert_bytes
+        raw = self.array[off:off + cfg.expert_bytes]
+        return raw.view(np.float32 if cfg.dtype == "f32" else np.uint16)
+
+    def close(self):
+        if self.ptr:
+            self.array = None
+            b.moe_host_free(self.ptr)
+            self.ptr = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class DeviceGates:
+    def __init__(self, cfg: wl.Config, gates: Optional[np.ndarray] = None):
+        torch = _torch()
+        self.host = gates if gates is not None else wl.gate_weights(cfg)
+        raw = np.ascontiguousarray(self.host).view(np.uint8).reshape(-1)
+        self.tensor = torch.from_numpy(raw.copy()).to("cuda")
+
+    @property
+    def ptr(self) -> int:
+        return self.tensor.data_ptr()
+
+
+class OffloadedMoE:
+    """One expert cache over a whole stack (one handle of the C ABI)."""
+
+    def __init__(self, cfg: wl.Config, store: HostStore, gates: DeviceGates, slots: int,
+                 policy: str, prefetch_max: int = 0, fetch_mode: int = b.MOE_FETCH_KERNEL,
+                 trace_cap: Optional[int] = None, max_prefill_tokens: int = 0,
+                 separate_copy_stream: bool = True):
+        torch = _torch()
+        self.cfg, self.store, self.gates = cfg, store, gates
+        self.L, self.E, self.S, self.K = cfg.layers, cfg.experts, slots, cfg.top_k
+        self.handle = b.moe_cache_create(cfg.layers, cfg.experts, slots, b.POLICIES[policy])
+        try:
+            self.compute = torch.cuda.Stream()
+            self.copy = torch.cuda.Stream() if separate_copy_stream else self.compute
+            self.arena = torch.empty(cfg.layers * slots * cfg.expert_bytes, dtype=torch.uint8,
+                                     device="cuda")
+            if trace_cap is None:
+                trace_cap = max(1024, 2 * self.K * self.L * (cfg.tokens + cfg.prefill_tokens + 8))
+            self.trace_cap = trace_cap
+            self.trace = (torch.empty(trace_cap * 32, dtype=torch.uint8, device="cuda")
+                          if trace_cap > 0 else None)
+            d = b.moe_model_desc()
+            d.d_model, d.d_ff, d.top_k = cfg.d_model, cfg.d_ff, cfg.top_k
+            d.dtype = b.DTYPES[cfg.dtype]
+            d.prefetch_max = prefetch_max
+            d.fetch_mode = fetch_mode
+            d.max_prefill_tokens = max_prefill_tokens
+            d.gate_w = gates.ptr
+            d.host_experts = store.ptr
+            d.arena = self.arena.data_ptr()
+            d.trace = self.trace.data_ptr() if self.trace is not None else None
+            d.trace_cap = trace_cap if self.trace is not None else 0
+            d.compute_stream = self.compute.cuda_stream
+            d.copy_stream = self.copy.cuda_stream
+            ws = b.moe_cache_workspace_bytes(self.handle, d)
+            if ws == 0:
+                raise b.MoeError(b.MOE_ERR_ARG, "moe_cache_workspace_bytes", b.moe_last_error())
+            self.workspace = torch.empty(ws, dtype=torch.uint8, device="cuda")
+            d.workspace = self.workspace.data_ptr()
+            d.workspace_bytes = ws
+            self.desc = d
+            torch.cuda.synchronize()
+            b.moe_cache_bind(self.handle, d)
+            b.moe_cache_reset(self.handle)
+        except Exception:
+            b.moe_cache_destroy(self.handle)
+            self.handle = 0
+            raise
+
+    # -- driving the stack ------------------------------------------------------
+    def reset(self):
+        b.moe_cache_reset(self.handle)
+
+    def decode(self, H, flags: int = 0, snapshots=None):
+        """Decode tokens H [T][d] (fp32, device) in place, token by token.
+
+        snapshots (optional, device [T][L+1][d]) receives h entering every layer
+        and the final output, copied on the compute stream."""
+        torch = _torch()
+        self.compute.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(self.compute):
+            for t in range(H.shape[0]):
+                row = H[t]
+                p = row.data_ptr()
+                for l in range(self.L):
+                    if snapshots is not None:
+                        snapshots[t, l].copy_(row)
+                    b.moe_decode_layer(self.handle, l, p, flags)
+                if snapshots is not None:
+                    snapshots[t, self.L].copy_(row)
+
+    def decode_layer(self, layer: int, h, flags: int = 0):
+        b.moe_decode_layer(self.handle, layer, h.data_ptr(), flags)
+
+    def prefill(self, H, snapshots=None):
+        """All layers over the token batch H [T][d] (fp32, device) in place."""
+        torch = _torch()
+        self.compute.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(self.compute):
+            for l in range(self.L):
+                if snapshots is not None:
+                    snapshots[l].copy_(H)
+                b.moe_prefill_layer(self.handle, l, H.data_ptr(), H.shape[0])
+            if snapshots is not None:
+                snapshots[self.L].copy_(H)
+
+    def sync(self):
+        b.moe_cache_sync(self.handle)
+
+    def stats(self):
+        return b.moe_cache_stats(self.handle, self.L)
+
+    def trace_records(self):
+        recs, dropped = b.moe_cache_read_trace(self.handle, self.trace_cap)
+        return recs, dropped
+
+    def state(self, layer: int):
+        return b.moe_cache_read_state(self.handle, layer, self.S, self.E)
+
+    def close(self):
+        if self.handle:
+            b.moe_cache_destroy(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
