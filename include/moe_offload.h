@@ -173,6 +173,21 @@ int moe_cache_read_state(moe_cache_t *c, int layer, int32_t *slot_expert,
  * g (host fp32), each up to cap entries; *n = entries available. Syncs. */
 int moe_cache_last_routing(moe_cache_t *c, int32_t *ids, float *g, size_t cap, size_t *n);
 
+typedef struct {
+  double router_ms, fetch_ms, ffn_up_ms, ffn_down_ms, prefill_ms, gemm_up_ms, gemm_down_ms;
+  uint64_t router_n, fetch_n, ffn_up_n, ffn_down_n, prefill_n, gemm_up_n, gemm_down_n;
+  double gemm_up_flop, gemm_down_flop; /* algorithmic flops of the timed GEMM launches */
+} moe_timing;
+
+/* Kernel timing with HIP events, off by default.  While enabled, every router,
+ * fetch, decode FFN and prefill grouped-GEMM launch is bracketed by a pair of
+ * events on the stream it runs on (prefill_ms spans a whole layer's prefill on
+ * the compute stream, waits for streamed experts included).
+ * moe_cache_read_timing syncs, returns the summed durations (ms), launch
+ * counts and GEMM flops since the previous read, and clears them. */
+int moe_cache_set_timing(moe_cache_t *c, int enable);
+int moe_cache_read_timing(moe_cache_t *c, moe_timing *out);
+
 /* Drain the streams, release events; NULL-safe. */
 void moe_cache_destroy(moe_cache_t *c);
 

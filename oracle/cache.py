@@ -208,6 +208,16 @@ class LayerCache:
         self.stats.hits += hits
         self.stats.misses += routed - hits
 
+        # a prefetched expert the batch routes to was used (even if the new
+        # residency then drops it); one it does not route to was wasted
+        for e in range(self.E):
+            if self.prefetched[e]:
+                self.prefetched[e] = False
+                if n[e] > 0:
+                    self.stats.pf_useful += 1
+                else:
+                    self.stats.pf_wasted += 1
+
         if self.policy == LFU:
             prio = lambda e: (-self.count[e], 0 if e in start else 1, e)
         else:
@@ -228,13 +238,6 @@ class LayerCache:
             self.slot_expert[s] = e
             self.expert_slot[e] = s
             victim_of[e] = v
-        for e in range(self.E):
-            if self.prefetched[e]:
-                self.prefetched[e] = False
-                if n[e] > 0:
-                    self.stats.pf_useful += 1
-                else:
-                    self.stats.pf_wasted += 1
         out = []
         for e in range(self.E):
             fl = (F_RES_START if e in start else 0) | (F_RES_AFTER if e in rstar else 0)

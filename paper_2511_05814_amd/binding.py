@@ -56,6 +56,16 @@ class moe_layer_stats(ctypes.Structure):
                  "pf_wasted", "lookups", "bytes_fetched")]
 
 
+class moe_timing(ctypes.Structure):
+    _fields_ = ([(n, ctypes.c_double) for n in
+                 ("router_ms", "fetch_ms", "ffn_up_ms", "ffn_down_ms", "prefill_ms", "gemm_up_ms",
+                  "gemm_down_ms")]
+                + [(n, ctypes.c_uint64) for n in
+                   ("router_n", "fetch_n", "ffn_up_n", "ffn_down_n", "prefill_n", "gemm_up_n",
+                    "gemm_down_n")]
+                + [(n, ctypes.c_double) for n in ("gemm_up_flop", "gemm_down_flop")])
+
+
 # (name, restype, argtypes) of every exported function, in header order
 _SIGNATURES = [
     ("moe_cache_create", ctypes.c_int,
@@ -78,6 +88,8 @@ _SIGNATURES = [
     ("moe_cache_last_routing", ctypes.c_int,
      [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
       ctypes.POINTER(ctypes.c_size_t)]),
+    ("moe_cache_set_timing", ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
+    ("moe_cache_read_timing", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(moe_timing)]),
     ("moe_cache_destroy", None, [ctypes.c_void_p]),
     ("moe_host_alloc", ctypes.c_int, [ctypes.c_size_t, ctypes.POINTER(ctypes.c_void_p)]),
     ("moe_host_free", ctypes.c_int, [ctypes.c_void_p]),
@@ -185,6 +197,16 @@ def moe_cache_last_routing(cache: int, cap: int):
     _check(lib().moe_cache_last_routing(cache, ids, g, cap, ctypes.byref(n)), "moe_cache_last_routing")
     m = min(n.value, cap)
     return list(ids[:m]), list(g[:m]), n.value
+
+
+def moe_cache_set_timing(cache: int, enable: bool) -> None:
+    _check(lib().moe_cache_set_timing(cache, int(bool(enable))), "moe_cache_set_timing")
+
+
+def moe_cache_read_timing(cache: int) -> dict:
+    t = moe_timing()
+    _check(lib().moe_cache_read_timing(cache, ctypes.byref(t)), "moe_cache_read_timing")
+    return {n: getattr(t, n) for n, _ in moe_timing._fields_}
 
 
 def moe_cache_destroy(cache: int) -> None:

@@ -88,10 +88,54 @@ struct FfnArgs {
   float *h;                // in/out [d]
   float *act;              // [K][d_ff]
   float *part;             // [chunks][d]
-  uint32_t *counters;      // [row blocks]
   uint64_t expert_bytes;
   int layer, S, K, d, d_ff;
   int phase;               // up: 0 all ranks, 1 hit ranks, 2 missed ranks
+};
+
+// ---- batched prefill ------------------------------------------------------
+struct PrefillPlan {
+  int32_t n;           // pairs routed to the expert
+  int32_t off;         // first sorted position
+  int32_t slot_start;  // slot before the batch, -1 if not resident
+  int32_t slot_after;  // slot after the batch, -1 if not resident
+  int32_t newcomer;    // became resident in this batch
+  int32_t pad[3];
+};
+
+struct GemmJob {
+  const uint16_t *w;  // expert base (W1 | W3 | W2), bf16
+  int32_t row0;       // first sorted row of the expert
+  int32_t nrows;      // rows routed to it
+};
+
+struct GemmTile {
+  int32_t job, m0, n0, pad;
+};
+
+struct PrefillArgs {
+  const void *gate;  // layer's gate [E][d]
+  const float *H;    // [T][d]
+  int32_t *ids;      // [T][K]
+  float *g;          // [T][K]
+  float *inv_r;      // [T]
+  uint16_t *xn;      // [T][d] bf16
+  int T, d, E, K, dtype;
+};
+
+struct PlanArgs {
+  const int32_t *ids;
+  int32_t *perm_tok;  // [T*K] sorted position -> token
+  int32_t *pos_of;    // [T*K] (token, rank) -> sorted position
+  PrefillPlan *plan;  // [E]
+  LayerTable *table;
+  LayerStats *stats;
+  TraceRec *trace;
+  uint64_t *trace_count;
+  uint64_t trace_cap;
+  int32_t *err;
+  uint64_t expert_bytes;
+  int T, K, E, S, layer, policy;
 };
 
 // launchers (one per translation unit that owns the kernel)
@@ -101,7 +145,15 @@ hipError_t launch_fetch(const FetchList *list, const uint8_t *host, uint8_t *are
 hipError_t launch_ffn_up(const FfnArgs &a, int dtype, hipStream_t s);
 hipError_t launch_ffn_down(const FfnArgs &a, int dtype, hipStream_t s);
 int ffn_down_chunks(int K, int d_ff);
-int ffn_down_row_blocks(int d);
+hipError_t launch_prefill_gate(const PrefillArgs &a, hipStream_t s);
+hipError_t launch_prefill_plan(const PlanArgs &a, hipStream_t s);
+hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, hipStream_t s);
+hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
+                               float *Y, int d, int d_ff, hipStream_t s);
+hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
+                                    int d, int K, hipStream_t s);
+int prefill_tile_rows();
 
 // ---------------------------------------------------------------------------
 // device helpers

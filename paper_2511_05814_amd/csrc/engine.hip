@@ -43,17 +43,53 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
   size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, act = 0, part = 0,
-         counters = 0, prefill = 0, total = 0;
+         prefill = 0, total = 0;
 };
 
 bool misaligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) != 0; }
 
 }  // namespace
 
-// prefill support lives in prefill.hip
 namespace moe {
-size_t prefill_workspace_bytes(int K, int d, int d_ff, int E, int T);
+// Prefill workspace for batches of up to T tokens (offsets from its base).
+struct PrefillLayout {
+  size_t ids = 0, g = 0, inv_r = 0, xn = 0, perm = 0, pos = 0, plan = 0, jobs = 0, tiles = 0, act = 0,
+         y = 0, staging = 0, total = 0;
+  int tile_cap = 0;  // GEMM tiles the schedule can hold
+  int ring = 0;      // staging slots for experts streamed through the batch
+};
+
+static PrefillLayout prefill_layout(int K, int d, int d_ff, int E, int S, int T, uint64_t B) {
+  PrefillLayout p;
+  if (T <= 0) return p;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  const size_t P = (size_t)T * K;
+  const int rows = 64;
+  p.tile_cap = (int)((P + rows - 1) / rows + E) * ((d_ff + rows - 1) / rows + (d + rows - 1) / rows);
+  int half = (E - S + 1) / 2;
+  half = half < 1 ? 1 : (half > 4 ? 4 : half);
+  p.ring = 2 * half;
+  p.ids = take(P * 4);
+  p.g = take(P * 4);
+  p.inv_r = take((size_t)T * 4);
+  p.xn = take((size_t)T * d * 2);
+  p.perm = take(P * 4);
+  p.pos = take(P * 4);
+  p.plan = take(sizeof(PrefillPlan) * kMaxE);
+  p.jobs = take(sizeof(GemmJob) * kMaxE);
+  p.tiles = take(sizeof(GemmTile) * (size_t)p.tile_cap);
+  p.act = take(P * d_ff * 2);
+  p.y = take(P * d * 4);
+  p.staging = take((size_t)p.ring * B);
+  p.total = off;
+  return p;
 }
+}  // namespace moe
 
 struct moe_cache {
   int L = 0, E = 0, S = 0, policy = 0;
@@ -72,7 +108,6 @@ struct moe_cache {
   int32_t *err = nullptr;
   uint64_t *trace_count = nullptr;  // device: records written to the trace ring
   float *act = nullptr, *part = nullptr;
-  uint32_t *cnt = nullptr;
   uint8_t *prefill_ws = nullptr;
   const uint8_t *host_dev = nullptr;  // device address of the pinned host store
   std::vector<hipEvent_t> ev_demand, ev_pf;
@@ -82,7 +117,57 @@ struct moe_cache {
   FetchList *mirror = nullptr;  // pinned host copies of two fetch lists (DMA mode)
   int last_route_kind = 0;      // 0 none, 1 decode, 2 prefill
   int last_prefill_T = 0;
+  // batched prefill
+  PrefillLayout play;
+  PrefillPlan *h_plan = nullptr;   // pinned: plan of the last prefill layer
+  uint8_t *h_sched = nullptr;      // pinned: GEMM jobs + tiles uploaded per layer
+  std::vector<hipEvent_t> pf_ev;   // prefill ordering events
+  // kernel timing (moe_cache_set_timing)
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  struct Span {
+    int kind;
+    hipEvent_t a, b;
+    double flop;
+  };
+  std::vector<Span> spans;
 };
+
+namespace moe {
+enum SpanKind {
+  SPAN_ROUTER = 0, SPAN_FETCH, SPAN_UP, SPAN_DOWN, SPAN_PREFILL, SPAN_GEMM_UP, SPAN_GEMM_DOWN, SPAN_KINDS
+};
+
+// Start/stop a timed span on stream s (no-op unless timing is on).
+hipError_t span_begin(moe_cache *c, hipStream_t s, hipEvent_t *out) {
+  *out = nullptr;
+  if (!c->timing) return hipSuccess;
+  hipEvent_t e;
+  if (!c->ev_pool.empty()) {
+    e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+  } else {
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+  }
+  *out = e;
+  return hipEventRecord(e, s);
+}
+
+hipError_t span_end(moe_cache *c, hipStream_t s, int kind, hipEvent_t begin, double flop = 0.0) {
+  if (!c->timing || !begin) return hipSuccess;
+  hipEvent_t e;
+  if (!c->ev_pool.empty()) {
+    e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+  } else {
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+  }
+  c->spans.push_back({kind, begin, e, flop});
+  return hipEventRecord(e, s);
+}
+}  // namespace moe
 
 namespace moe {
 int prefill_enqueue(moe_cache *c, int layer, float *H, int T);
@@ -126,6 +211,10 @@ static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
   if (d->fetch_mode != MOE_FETCH_KERNEL && d->fetch_mode != MOE_FETCH_DMA)
     return fail(MOE_ERR_ARG, "bad fetch_mode");
   if (d->max_prefill_tokens < 0) return fail(MOE_ERR_ARG, "max_prefill_tokens < 0");
+  if (d->max_prefill_tokens > 0 && d->dtype != MOE_DTYPE_BF16)
+    return fail(MOE_ERR_ARG, "batched prefill runs on bf16 experts (matrix cores); dtype must be bf16");
+  if ((int64_t)d->max_prefill_tokens * d->top_k > (1 << 28))
+    return fail(MOE_ERR_ARG, "max_prefill_tokens * top_k too large");
   return MOE_OK;
 }
 
@@ -145,11 +234,8 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.err = take(256);
   l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff) * d->d_model);
-  l.counters = take(sizeof(uint32_t) * (size_t)ffn_down_row_blocks(d->d_model));
-  l.prefill = take(d->max_prefill_tokens > 0
-                       ? prefill_workspace_bytes(d->top_k, d->d_model, d->d_ff, c->E,
-                                                 d->max_prefill_tokens)
-                       : 0);
+  const uint64_t B = 3ull * d->d_model * d->d_ff * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
+  l.prefill = take(prefill_layout(d->top_k, d->d_model, d->d_ff, c->E, c->S, d->max_prefill_tokens, B).total);
   l.total = off;
   return l;
 }
@@ -228,7 +314,6 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->trace_count = reinterpret_cast<uint64_t *>(c->ws + lay.err + 8);
   c->act = reinterpret_cast<float *>(c->ws + lay.act);
   c->part = reinterpret_cast<float *>(c->ws + lay.part);
-  c->cnt = reinterpret_cast<uint32_t *>(c->ws + lay.counters);
   c->prefill_ws = c->ws + lay.prefill;
   c->host_dev = static_cast<const uint8_t *>(dev_host);
 
@@ -243,6 +328,16 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   HIP_TRY0(hipEventCreateWithFlags(&c->ev_router, hipEventDisableTiming));
   HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->mirror), 2 * sizeof(FetchList),
                                  hipHostMallocDefault));
+  if (c->max_T > 0) {
+    c->play = prefill_layout(c->K, c->d, c->dff, c->E, c->S, c->max_T, c->B);
+    HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->h_plan), sizeof(PrefillPlan) * kMaxE,
+                           hipHostMallocDefault));
+    HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->h_sched),
+                           sizeof(GemmJob) * kMaxE + sizeof(GemmTile) * (size_t)c->play.tile_cap,
+                           hipHostMallocDefault));
+    c->pf_ev.assign(2 * kMaxE + 4, nullptr);
+    for (auto &e : c->pf_ev) HIP_TRY0(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  }
   c->bound = true;
   c->sticky = MOE_ERR_STATE;  // decode needs a reset first
   return MOE_OK;
@@ -268,7 +363,6 @@ int moe_cache_reset(moe_cache_t *c) {
   HIP_TRY(c, hipMemcpyAsync(c->tables, t.data(), sizeof(LayerTable) * c->L, hipMemcpyHostToDevice, c->cs));
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.stats, 0, c->lay.route - c->lay.stats, c->cs));
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.route, 0, c->lay.act - c->lay.route, c->cs));
-  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.counters, 0, c->lay.prefill - c->lay.counters, c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
@@ -290,8 +384,11 @@ int moe_cache_reset(moe_cache_t *c) {
 // Issue the copies for one fetch list that the router just wrote.
 static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_t q) {
   if (c->fetch_mode == MOE_FETCH_KERNEL) {
+    hipEvent_t t0;
+    HIP_TRY(c, span_begin(c, q, &t0));
     HIP_TRY(c, launch_fetch(list, c->host_dev, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
                             c->K, c->B, c->err, q));
+    HIP_TRY(c, span_end(c, q, SPAN_FETCH, t0));
     return MOE_OK;
   }
   const FetchList &m = c->mirror[mirror_idx];
@@ -301,6 +398,9 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
   }
   const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
+  if (m.n == 0) return MOE_OK;
+  hipEvent_t t0;
+  HIP_TRY(c, span_begin(c, q, &t0));
   for (int i = 0; i < m.n; ++i) {
     const int e = m.expert[i], s = m.slot[i];
     if (e < 0 || e >= c->E || s < 0 || s >= c->S) {
@@ -310,6 +410,7 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
     HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)m.layer * c->S + s) * c->B,
                               host + ((size_t)m.layer * c->E + e) * c->B, c->B, hipMemcpyHostToDevice, q));
   }
+  HIP_TRY(c, span_end(c, q, SPAN_FETCH, t0));
   return MOE_OK;
 }
 
@@ -346,7 +447,10 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.demand = demand;
   a.spec_layer = spec_layer;
   a.pmax = pmax;
+  hipEvent_t t0;
+  HIP_TRY(c, span_begin(c, c->cs, &t0));
   HIP_TRY(c, launch_router(a, c->cs));
+  HIP_TRY(c, span_end(c, c->cs, SPAN_ROUTER, t0));
 
   hipStream_t q = c->xs;
   if (c->fetch_mode == MOE_FETCH_KERNEL) {
@@ -392,7 +496,6 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     f.h = h;
     f.act = c->act;
     f.part = c->part;
-    f.counters = c->cnt;
     f.expert_bytes = c->B;
     f.layer = layer;
     f.S = c->S;
@@ -400,12 +503,236 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     f.d = c->d;
     f.d_ff = c->dff;
     f.phase = 0;
+    hipEvent_t t0, t1;
+    HIP_TRY(c, span_begin(c, c->cs, &t0));
     HIP_TRY(c, launch_ffn_up(f, c->dtype, c->cs));
+    HIP_TRY(c, span_end(c, c->cs, SPAN_UP, t0));
+    HIP_TRY(c, span_begin(c, c->cs, &t1));
     HIP_TRY(c, launch_ffn_down(f, c->dtype, c->cs));
+    HIP_TRY(c, span_end(c, c->cs, SPAN_DOWN, t1));
     c->last_route_kind = 1;
   }
   return MOE_OK;
 }
+
+namespace moe {
+
+// Batched prefill of one layer.  Routing and the cache decision run on the
+// device; the host then waits for the plan (a few hundred bytes), because it
+// has to issue one copy per streamed expert and size the grouped GEMMs:
+//   compute: GEMMs on experts resident at the start  -> event A
+//   copy:    per batch of streamed experts: [wait the GEMMs that last used the
+//            staging half] [wait A before the first copy into a freed slot]
+//            copies -> event C_j
+//   compute: wait C_j -> GEMMs of batch j -> event G_j
+//   copy:    newcomers nobody routed (wait A) -> event F; compute waits F
+//   compute: unpermute (h += sum_r g Y)
+int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
+  const PrefillLayout &p = c->play;
+  uint8_t *base = c->prefill_ws;
+  int32_t *ids = reinterpret_cast<int32_t *>(base + p.ids);
+  float *g = reinterpret_cast<float *>(base + p.g);
+  float *inv_r = reinterpret_cast<float *>(base + p.inv_r);
+  uint16_t *xn = reinterpret_cast<uint16_t *>(base + p.xn);
+  int32_t *perm = reinterpret_cast<int32_t *>(base + p.perm);
+  int32_t *pos = reinterpret_cast<int32_t *>(base + p.pos);
+  PrefillPlan *plan = reinterpret_cast<PrefillPlan *>(base + p.plan);
+  GemmJob *jobs = reinterpret_cast<GemmJob *>(base + p.jobs);
+  GemmTile *tiles = reinterpret_cast<GemmTile *>(base + p.tiles);
+  uint16_t *act = reinterpret_cast<uint16_t *>(base + p.act);
+  float *Y = reinterpret_cast<float *>(base + p.y);
+  uint8_t *staging = base + p.staging;
+  const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
+  uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
+  const int gate_elem = c->dtype == MOE_DTYPE_BF16 ? 2 : 4;
+
+  hipEvent_t tp;
+  HIP_TRY(c, span_begin(c, c->cs, &tp));
+  PrefillArgs ga{};
+  ga.gate = static_cast<const uint8_t *>(c->desc.gate_w) + (size_t)layer * c->E * c->d * gate_elem;
+  ga.H = H;
+  ga.ids = ids;
+  ga.g = g;
+  ga.inv_r = inv_r;
+  ga.xn = xn;
+  ga.T = T;
+  ga.d = c->d;
+  ga.E = c->E;
+  ga.K = c->K;
+  ga.dtype = c->dtype;
+  HIP_TRY(c, launch_prefill_gate(ga, c->cs));
+  PlanArgs pa{};
+  pa.ids = ids;
+  pa.perm_tok = perm;
+  pa.pos_of = pos;
+  pa.plan = plan;
+  pa.table = c->tables + layer;
+  pa.stats = c->stats + layer;
+  pa.trace = static_cast<TraceRec *>(c->desc.trace);
+  pa.trace_count = c->trace_count;
+  pa.trace_cap = c->desc.trace ? c->desc.trace_cap : 0;
+  pa.err = c->err;
+  pa.expert_bytes = c->B;
+  pa.T = T;
+  pa.K = c->K;
+  pa.E = c->E;
+  pa.S = c->S;
+  pa.layer = layer;
+  pa.policy = c->policy;
+  HIP_TRY(c, launch_prefill_plan(pa, c->cs));
+  HIP_TRY(c, hipMemcpyAsync(c->h_plan, plan, sizeof(PrefillPlan) * c->E, hipMemcpyDeviceToHost, c->cs));
+  HIP_TRY(c, hipStreamSynchronize(c->cs));
+  {
+    int32_t e = 0;
+    HIP_TRY(c, hipMemcpy(&e, c->err, sizeof e, hipMemcpyDeviceToHost));
+    if (e != ERR_NONE) {
+      c->sticky = MOE_ERR_HIP;
+      return fail(MOE_ERR_HIP, "prefill routing produced an invalid expert id (code %d)", e);
+    }
+  }
+  c->last_route_kind = 2;
+  c->last_prefill_T = T;
+
+  // jobs: weights of every routed expert, where the GEMMs will find them
+  const int E = c->E;
+  const PrefillPlan *pl = c->h_plan;
+  GemmJob *hj = reinterpret_cast<GemmJob *>(c->h_sched);
+  GemmTile *ht = reinterpret_cast<GemmTile *>(c->h_sched + sizeof(GemmJob) * kMaxE);
+  std::vector<int> resident, streamed, unrouted_new;
+  for (int e = 0; e < E; ++e) {
+    if (pl[e].n < 0 || pl[e].off < 0 || pl[e].off + pl[e].n > T * c->K || pl[e].slot_start >= c->S ||
+        pl[e].slot_after >= c->S) {
+      c->sticky = MOE_ERR_HIP;
+      return fail(MOE_ERR_HIP, "inconsistent prefill plan from the device");
+    }
+    hj[e].w = nullptr;
+    hj[e].row0 = pl[e].off;
+    hj[e].nrows = pl[e].n;
+    if (pl[e].n > 0 && pl[e].slot_start >= 0) {
+      resident.push_back(e);
+      hj[e].w = reinterpret_cast<const uint16_t *>(arena + ((size_t)layer * c->S + pl[e].slot_start) * c->B);
+    } else if (pl[e].n == 0 && pl[e].newcomer) {
+      unrouted_new.push_back(e);
+    }
+  }
+  for (int pass = 0; pass < 2; ++pass)  // staging-bound experts first, then newcomers
+    for (int e = 0; e < E; ++e)
+      if (pl[e].n > 0 && pl[e].slot_start < 0 && (pl[e].slot_after >= 0) == (pass == 1)) streamed.push_back(e);
+
+  const int half = p.ring / 2;
+  std::vector<std::vector<int>> batches;
+  for (size_t i = 0; i < streamed.size(); i += half)
+    batches.emplace_back(streamed.begin() + i, streamed.begin() + std::min(streamed.size(), i + half));
+  // staging slots and tile lists
+  std::vector<int> ring_of(E, -1);
+  for (size_t bi = 0; bi < batches.size(); ++bi) {
+    int used = 0;
+    for (int e : batches[bi]) {
+      if (pl[e].slot_after >= 0) {
+        hj[e].w = reinterpret_cast<const uint16_t *>(arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B);
+      } else {
+        ring_of[e] = (int)(bi % 2) * half + used++;
+        hj[e].w = reinterpret_cast<const uint16_t *>(staging + (size_t)ring_of[e] * c->B);
+      }
+    }
+  }
+  const int rows = prefill_tile_rows();
+  int nt = 0;
+  auto add_tiles = [&](const std::vector<int> &group, int ncols, int &first, int &count) {
+    first = nt;
+    for (int e : group)
+      for (int m0 = 0; m0 < pl[e].n; m0 += rows)
+        for (int n0 = 0; n0 < ncols; n0 += rows) ht[nt++] = GemmTile{e, m0, n0, 0};
+    count = nt - first;
+  };
+  const size_t ngroups = batches.size() + 1;
+  std::vector<int> up_first(ngroups), up_n(ngroups), dn_first(ngroups), dn_n(ngroups);
+  std::vector<double> group_rows(ngroups, 0.0);
+  add_tiles(resident, c->dff, up_first[0], up_n[0]);
+  add_tiles(resident, c->d, dn_first[0], dn_n[0]);
+  for (int e : resident) group_rows[0] += pl[e].n;
+  for (size_t bi = 0; bi < batches.size(); ++bi) {
+    add_tiles(batches[bi], c->dff, up_first[bi + 1], up_n[bi + 1]);
+    add_tiles(batches[bi], c->d, dn_first[bi + 1], dn_n[bi + 1]);
+    for (int e : batches[bi]) group_rows[bi + 1] += pl[e].n;
+  }
+  if (nt > p.tile_cap) {
+    c->sticky = MOE_ERR_HIP;
+    return fail(MOE_ERR_HIP, "prefill tile schedule overflow (%d > %d)", nt, p.tile_cap);
+  }
+  HIP_TRY(c, hipMemcpyAsync(jobs, hj, sizeof(GemmJob) * kMaxE, hipMemcpyHostToDevice, c->cs));
+  if (nt > 0) HIP_TRY(c, hipMemcpyAsync(tiles, ht, sizeof(GemmTile) * nt, hipMemcpyHostToDevice, c->cs));
+
+  const double up_flop_per_row = 4.0 * c->d * c->dff, down_flop_per_row = 2.0 * c->d * c->dff;
+  auto run_group = [&](size_t gi) -> int {
+    hipEvent_t t0, t1;
+    HIP_TRY(c, span_begin(c, c->cs, &t0));
+    HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, c->cs));
+    HIP_TRY(c, span_end(c, c->cs, SPAN_GEMM_UP, t0, group_rows[gi] * up_flop_per_row));
+    HIP_TRY(c, span_begin(c, c->cs, &t1));
+    HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, c->cs));
+    HIP_TRY(c, span_end(c, c->cs, SPAN_GEMM_DOWN, t1, group_rows[gi] * down_flop_per_row));
+    return MOE_OK;
+  };
+  hipEvent_t evA = c->pf_ev[0], evF = c->pf_ev[1];
+  if (!resident.empty()) {
+    int rc = run_group(0);
+    if (rc != MOE_OK) return rc;
+  }
+  HIP_TRY(c, hipEventRecord(evA, c->cs));
+  hipStream_t q = c->xs;
+  bool waited_A = false;
+  for (size_t bi = 0; bi < batches.size(); ++bi) {
+    hipEvent_t evC = c->pf_ev[2 + 2 * (bi % kMaxE)], evG = c->pf_ev[3 + 2 * (bi % kMaxE)];
+    bool waited_ring = false;
+    for (int e : batches[bi]) {
+      uint8_t *dst;
+      if (pl[e].slot_after >= 0) {
+        if (!waited_A) {
+          HIP_TRY(c, hipStreamWaitEvent(q, evA, 0));
+          waited_A = true;
+        }
+        dst = arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B;
+      } else {
+        if (!waited_ring && bi >= 2) {
+          HIP_TRY(c, hipStreamWaitEvent(q, c->pf_ev[3 + 2 * ((bi - 2) % kMaxE)], 0));
+          waited_ring = true;
+        }
+        dst = staging + (size_t)ring_of[e] * c->B;
+      }
+      HIP_TRY(c, hipMemcpyAsync(dst, host + ((size_t)layer * E + e) * c->B, c->B, hipMemcpyHostToDevice, q));
+    }
+    HIP_TRY(c, hipEventRecord(evC, q));
+    HIP_TRY(c, hipStreamWaitEvent(c->cs, evC, 0));
+    int rc = run_group(bi + 1);
+    if (rc != MOE_OK) return rc;
+    HIP_TRY(c, hipEventRecord(evG, c->cs));
+  }
+  if (!unrouted_new.empty()) {
+    if (!waited_A) HIP_TRY(c, hipStreamWaitEvent(q, evA, 0));
+    for (int e : unrouted_new)
+      HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B,
+                                host + ((size_t)layer * E + e) * c->B, c->B, hipMemcpyHostToDevice, q));
+  }
+  HIP_TRY(c, hipEventRecord(evF, q));
+  HIP_TRY(c, hipStreamWaitEvent(c->cs, evF, 0));
+  HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, c->cs));
+  HIP_TRY(c, span_end(c, c->cs, SPAN_PREFILL, tp));
+  // later decode calls on this layer need no extra wait: the compute stream
+  // has already waited for every copy issued here
+  return MOE_OK;
+}
+
+int prefill_routing(moe_cache *c, int32_t *ids, float *g, size_t cap, size_t *n) {
+  const size_t P = (size_t)c->last_prefill_T * c->K;
+  const size_t m = P < cap ? P : cap;
+  if (ids && m) HIP_TRY(c, hipMemcpy(ids, c->prefill_ws + c->play.ids, m * 4, hipMemcpyDeviceToHost));
+  if (g && m) HIP_TRY(c, hipMemcpy(g, c->prefill_ws + c->play.g, m * 4, hipMemcpyDeviceToHost));
+  *n = P;
+  return MOE_OK;
+}
+
+}  // namespace moe
 
 extern "C" {
 
@@ -554,8 +881,45 @@ int moe_cache_last_routing(moe_cache_t *c, int32_t *ids, float *g, size_t cap, s
   return MOE_OK;
 }
 
+int moe_cache_set_timing(moe_cache_t *c, int enable) {
+  if (!c) return fail(MOE_ERR_ARG, "NULL handle");
+  c->timing = enable != 0;
+  return MOE_OK;
+}
+
+int moe_cache_read_timing(moe_cache_t *c, moe_timing *out) {
+  if (!c || !out) return fail(MOE_ERR_ARG, "NULL argument");
+  std::memset(out, 0, sizeof *out);
+  if (!c->bound) return MOE_OK;
+  (void)hipStreamSynchronize(c->cs);
+  if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
+  double *ms[SPAN_KINDS] = {&out->router_ms, &out->fetch_ms,   &out->ffn_up_ms,  &out->ffn_down_ms,
+                            &out->prefill_ms, &out->gemm_up_ms, &out->gemm_down_ms};
+  uint64_t *n[SPAN_KINDS] = {&out->router_n,  &out->fetch_n,   &out->ffn_up_n,  &out->ffn_down_n,
+                             &out->prefill_n, &out->gemm_up_n, &out->gemm_down_n};
+  int rc = MOE_OK;
+  for (const auto &sp : c->spans) {
+    float t = 0.0f;
+    hipError_t e = hipEventElapsedTime(&t, sp.a, sp.b);
+    if (e != hipSuccess && rc == MOE_OK)
+      rc = fail(MOE_ERR_HIP, "hipEventElapsedTime failed: %s", hipGetErrorString(e));
+    *ms[sp.kind] += t;
+    *n[sp.kind] += 1;
+    if (sp.kind == SPAN_GEMM_UP) out->gemm_up_flop += sp.flop;
+    if (sp.kind == SPAN_GEMM_DOWN) out->gemm_down_flop += sp.flop;
+    c->ev_pool.push_back(sp.a);
+    c->ev_pool.push_back(sp.b);
+  }
+  c->spans.clear();
+  return rc;
+}
+
 void moe_cache_destroy(moe_cache_t *c) {
   if (!c) return;
+  for (const auto &sp : c->spans) {
+    c->ev_pool.push_back(sp.a);
+    c->ev_pool.push_back(sp.b);
+  }
   if (c->bound) {
     (void)hipStreamSynchronize(c->cs);
     if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
@@ -565,6 +929,11 @@ void moe_cache_destroy(moe_cache_t *c) {
       if (e) (void)hipEventDestroy(e);
     if (c->ev_router) (void)hipEventDestroy(c->ev_router);
     if (c->mirror) (void)hipHostFree(c->mirror);
+    if (c->h_plan) (void)hipHostFree(c->h_plan);
+    if (c->h_sched) (void)hipHostFree(c->h_sched);
+    for (hipEvent_t e : c->pf_ev)
+      if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
     (void)hipGetLastError();
   }
   delete c;

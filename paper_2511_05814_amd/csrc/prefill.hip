@@ -1,25 +1,496 @@
-// Batched prefill through one layer (placeholder until the grouped-GEMM path lands).
+// Batched prefill of T tokens through one layer.
+//
+// The paper's measurements cover generated tokens only (Sec. 5.1); this path
+// runs a prompt's tokens through the same MoE layer at once, with the same
+// per-token arithmetic, and lets the cache see the whole batch's routing:
+//
+//   1. gate    Z = H W_g^T in fp64 (exact products, fp64 sums), top-K per
+//              token, renormalised softmax weights, x = h / rms(h) in bf16
+//   2. plan    histogram of the T*K (token, rank) pairs by expert, exclusive
+//              scan, scatter into expert-sorted order; the cache table takes
+//              the batch at once: counts += per-expert routings, the clock
+//              ticks once per pair, then the S highest-ranked experts stay
+//              resident (LFU: count; LRU: last use; ties: resident first,
+//              lower id); kept experts keep their slots, newcomers take the
+//              freed slots in ascending order
+//   3. experts the host schedules: grouped GEMMs (MFMA bf16, fp32 accumulate)
+//              on experts resident at the start, while the copy stream streams
+//              every other routed expert (into its new slot, or a staging ring)
+//              followed by the grouped GEMMs on those
+//   4. unpermute  h_t += sum_r g_tr Y[pos(t, r)] in rank order (no atomics)
+//
+// The grouped GEMMs are dense contractions (rows = tokens routed to one
+// expert), so they run on the matrix cores: a 64 x 64 output tile per
+// workgroup, four waves each owning 32 x 32, v_mfma_f32_16x16x32_bf16 steps.
 #include "common.hpp"
 #include "moe_offload.h"
 
-struct moe_cache;
+#include <cmath>
 
 namespace moe {
 
-size_t prefill_workspace_bytes(int K, int d, int d_ff, int E, int T) {
-  (void)K; (void)d; (void)d_ff; (void)E; (void)T;
-  return 0;
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGateTok = 16;     // tokens per gate workgroup
+constexpr int kGateChunk = 128;  // columns staged per step
+constexpr int kTile = 64;        // GEMM output tile (rows and columns)
+constexpr int kKStep = 32;       // GEMM reduction step (one MFMA depth)
+constexpr int kLdsK = kKStep + 8;  // padded LDS row (bf16 elements)
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
 }
 
-int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
-  (void)c; (void)layer; (void)H; (void)T;
-  return MOE_ERR_STATE;
+__device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }
+
+// ---------------------------------------------------------------------------
+// 1. gate logits, top-K, combine weights, normalised bf16 rows
+__global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
+  __shared__ float hs[kGateTok][kGateChunk];
+  __shared__ float ws[kMaxE][kGateChunk + 1];
+  __shared__ double zs[kGateTok][kMaxE];
+  __shared__ double rs[kGateTok];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int t0 = blockIdx.x * kGateTok;
+  const int E = a.E, d = a.d;
+  const int tok = tid / 16, eb = tid % 16;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  double sq = 0.0;
+  for (int c0 = 0; c0 < d; c0 += kGateChunk) {
+    const int cw = min(kGateChunk, d - c0);
+    // 16 x 128 hidden values: thread -> row tid/16, 8 consecutive columns
+    {
+      const int r = tid / 16, c = (tid % 16) * 8;
+      const int t = t0 + r;
+      for (int i = 0; i < 8; ++i) {
+        float v = 0.0f;
+        if (t < a.T && c + i < cw) v = a.H[(size_t)t * d + c0 + c + i];
+        hs[r][c + i] = v;
+        sq = fma((double)v, (double)v, sq);
+      }
+    }
+    // E x 128 gate weights widened to fp32 (exact)
+    for (int i = tid; i < E * kGateChunk; i += 256) {
+      const int e = i / kGateChunk, c = i % kGateChunk;
+      float w = 0.0f;
+      if (c < cw) {
+        const size_t idx = (size_t)e * d + c0 + c;
+        w = a.dtype == 1 ? __uint_as_float((uint32_t)static_cast<const uint16_t *>(a.gate)[idx] << 16)
+                         : static_cast<const float *>(a.gate)[idx];
+      }
+      ws[e][c] = w;
+    }
+    __syncthreads();
+    for (int c = 0; c < cw; ++c) {
+      const double hv = hs[tok][c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int e = eb + 16 * j;
+        if (e < E) acc[j] = fma((double)ws[e][c], hv, acc[j]);
+      }
+    }
+    __syncthreads();
+  }
+  // row sums of squares: the 16 threads of a row are 16 consecutive lanes
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) sq += __shfl_xor(sq, o, kWave);
+  if (eb == 0) rs[tok] = sq;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = eb + 16 * j;
+    if (e < E) zs[tok][e] = acc[j];
+  }
+  __syncthreads();
+
+  // top-K per token: wave w handles tokens 4w .. 4w+3
+  for (int q = 0; q < kGateTok / 4; ++q) {
+    const int r = wave * (kGateTok / 4) + q;
+    const int t = t0 + r;
+    if (t >= a.T) break;
+    const double z = lane < E ? zs[r][lane] : 0.0;
+    // rank order: larger z first, lower id on ties
+    bool avail = lane < E;
+    int mine = -1;
+    for (int k = 0; k < a.K; ++k) {
+      double bz = avail ? z : -INFINITY;
+      int bl = avail ? lane : 1000 + lane;
+      int bv = avail ? 1 : 0;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const double oz = __shfl_xor(bz, o, kWave);
+        const int ol = __shfl_xor(bl, o, kWave);
+        const int ov = __shfl_xor(bv, o, kWave);
+        if ((ov && !bv) || (ov == bv && (oz > bz || (oz == bz && ol < bl)))) {
+          bz = oz;
+          bl = ol;
+          bv = ov;
+        }
+      }
+      if (lane == k) mine = bl;
+      if (lane == bl) avail = false;
+    }
+    const double rr = sqrt(rs[r] / (double)d + 1e-5);
+    const double zr = (lane < a.K) ? zs[r][mine] : 0.0;
+    const double z0 = __shfl(zr, 0, kWave);
+    const double ex = (lane < a.K) ? exp((zr - z0) / rr) : 0.0;
+    double den = ex;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o, kWave);
+    if (lane < a.K) {
+      a.ids[(size_t)t * a.K + lane] = mine;
+      a.g[(size_t)t * a.K + lane] = (float)(ex / den);
+    }
+    const float inv = (float)(1.0 / rr);
+    if (lane == 0) a.inv_r[t] = inv;
+    for (int c = lane * 4; c < d; c += kWave * 4) {
+      const float4 v = *reinterpret_cast<const float4 *>(a.H + (size_t)t * d + c);
+      uint2 o;
+      o.x = (uint32_t)f32_to_bf16_rne(v.x * inv) | ((uint32_t)f32_to_bf16_rne(v.y * inv) << 16);
+      o.y = (uint32_t)f32_to_bf16_rne(v.z * inv) | ((uint32_t)f32_to_bf16_rne(v.w * inv) << 16);
+      *reinterpret_cast<uint2 *>(a.xn + (size_t)t * d + c) = o;
+    }
+  }
 }
 
-int prefill_routing(moe_cache *c, int32_t *ids, float *g, size_t cap, size_t *n) {
-  (void)c; (void)ids; (void)g; (void)cap;
-  *n = 0;
-  return MOE_OK;
+// ---------------------------------------------------------------------------
+// 2. sort by expert and update the layer's table for the whole batch
+__global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
+  __shared__ int cnt[kMaxE], cur[kMaxE], lastp[kMaxE], offs[kMaxE];
+  __shared__ int bad;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int E = a.E, P = a.T * a.K;
+  if (tid < kMaxE) {
+    cnt[tid] = 0;
+    cur[tid] = 0;
+    lastp[tid] = 0;
+  }
+  if (tid == 0) bad = 0;
+  __syncthreads();
+  for (int p = tid; p < P; p += 1024) {
+    const int e = a.ids[p];
+    if (e < 0 || e >= E) {
+      bad = 1;
+      continue;
+    }
+    atomicAdd(&cnt[e], 1);
+    atomicMax(&lastp[e], p + 1);
+  }
+  __syncthreads();
+  if (bad) {
+    if (tid == 0) *a.err = ERR_BAD_LIST;
+    return;
+  }
+  if (wave == 0) {
+    const int c = lane < E ? cnt[lane] : 0;
+    int incl = c;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int v = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += v;
+    }
+    if (lane < E) offs[lane] = incl - c;
+  }
+  __syncthreads();
+  for (int p = tid; p < P; p += 1024) {
+    const int e = a.ids[p];
+    const int pos = offs[e] + atomicAdd(&cur[e], 1);
+    a.perm_tok[pos] = p / a.K;
+    a.pos_of[p] = pos;
+  }
+  if (wave != 0) return;
+
+  // table update: lane e = expert e
+  LayerTable *T = a.table;
+  const uint64_t tbase = (a.trace && a.trace_cap) ? *a.trace_count : 0;
+  const bool in_range = lane < E;
+  const int slot0 = in_range ? T->expert_slot[lane] : -1;
+  uint32_t count = in_range ? T->count[lane] : 0u;
+  int64_t last = in_range ? T->last[lane] : 0;
+  int pf = in_range ? T->pf[lane] : 0;
+  const int64_t clock0 = T->clock;
+  const int64_t token0 = T->lookups;
+  const int n = in_range ? cnt[lane] : 0;
+  const bool res_start = slot0 >= 0;
+  count += (uint32_t)n;
+  if (in_range && lastp[lane] > 0) last = clock0 + lastp[lane];
+
+  // R*: the S highest-ranked experts
+  bool chosen = false;
+  for (int s = 0; s < a.S; ++s) {
+    bool cand = in_range && !chosen;
+    uint64_t k1 = a.policy == 1 ? (uint64_t)count : (uint64_t)(last + (1ll << 40));
+    int k2 = res_start ? 1 : 0;
+    int bl = lane, bv = cand ? 1 : 0;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint64_t o1 = __shfl_xor(k1, o, kWave);
+      const int o2 = __shfl_xor(k2, o, kWave);
+      const int ol = __shfl_xor(bl, o, kWave);
+      const int ov = __shfl_xor(bv, o, kWave);
+      bool better;
+      if (ov != bv)
+        better = ov > bv;
+      else
+        better = o1 > k1 || (o1 == k1 && (o2 > k2 || (o2 == k2 && ol < bl)));
+      if (better) {
+        k1 = o1;
+        k2 = o2;
+        bl = ol;
+        bv = ov;
+      }
+    }
+    if (lane == bl) chosen = true;
+  }
+  const bool newcomer = chosen && !res_start;
+  const bool evicted = res_start && !chosen;
+  // freed slots (ascending) are handed to newcomers (ascending id)
+  unsigned long long freed = evicted ? (1ull << slot0) : 0ull;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) freed |= __shfl_xor(freed, o, kWave);
+  const unsigned long long newmask = __ballot(newcomer);
+  int slot1 = evicted ? -1 : slot0;
+  int victim = -1;
+  const int n_new = __popcll(newmask);
+  unsigned long long fm = freed, nm = newmask;
+  for (int i = 0; i < n_new; ++i) {
+    const int s = __ffsll((long long)fm) - 1;
+    const int e = __ffsll((long long)nm) - 1;
+    fm &= fm - 1;
+    nm &= nm - 1;
+    const unsigned long long owner = __ballot(slot0 == s);
+    if (lane == e) {
+      slot1 = s;
+      victim = owner ? __ffsll((long long)owner) - 1 : -1;
+    }
+  }
+  const bool fetched = in_range && ((n > 0 && !res_start) || newcomer);
+  int useful = 0, wasted = 0;
+  if (pf) {
+    if (n > 0)
+      useful = 1;
+    else
+      wasted = 1;
+  }
+  const int hits = res_start ? n : 0;
+  const int misses = res_start ? 0 : n;
+  int sh = hits, sm = misses, su = useful, sw = wasted, sf = fetched ? 1 : 0;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    sh += __shfl_xor(sh, o, kWave);
+    sm += __shfl_xor(sm, o, kWave);
+    su += __shfl_xor(su, o, kWave);
+    sw += __shfl_xor(sw, o, kWave);
+    sf += __shfl_xor(sf, o, kWave);
+  }
+  if (in_range) {
+    T->expert_slot[lane] = slot1;
+    T->count[lane] = count;
+    T->last[lane] = last;
+    T->pf[lane] = 0;
+    if (newcomer) T->slot_expert[slot1] = lane;
+    PrefillPlan pl;
+    pl.n = n;
+    pl.off = offs[lane];
+    pl.slot_start = slot0;
+    pl.slot_after = slot1;
+    pl.newcomer = newcomer ? 1 : 0;
+    pl.pad[0] = pl.pad[1] = pl.pad[2] = 0;
+    a.plan[lane] = pl;
+    if (a.trace && a.trace_cap) {
+      TraceRec r;
+      r.kind = REC_PREFILL;
+      r.token = (int32_t)token0;
+      r.layer = a.layer;
+      r.rank = n;
+      r.expert = lane;
+      r.flags = (res_start ? 1 : 0) | (chosen ? 2 : 0) | (fetched ? 4 : 0);
+      r.slot = slot1;
+      r.victim = newcomer ? victim : -1;
+      a.trace[(tbase + lane) % a.trace_cap] = r;
+    }
+  }
+  if (lane == 0) {
+    T->clock = clock0 + (int64_t)P;
+    T->lookups = token0 + a.T;
+    if (a.trace && a.trace_cap) *a.trace_count = tbase + E;
+    LayerStats *st = a.stats;
+    st->v[ST_HITS] += sh;
+    st->v[ST_MISSES] += sm;
+    st->v[ST_EVICT] += n_new;
+    st->v[ST_PF_USEFUL] += su;
+    st->v[ST_PF_WASTED] += sw;
+    st->v[ST_LOOKUPS] += a.T;
+    st->v[ST_BYTES] += (uint64_t)sf * a.expert_bytes;
+  }
 }
+
+// ---------------------------------------------------------------------------
+// 3. grouped GEMMs.  A rows come from the sorted pair order; B = expert
+// weights stored out x in (K contiguous), so both operands are K-major.
+
+// Load a 64 x 32 bf16 tile into LDS (row stride kLdsK); one 16-byte piece per
+// thread.  rowptr(i) gives the address of row i's element k0, or nullptr.
+template <typename RowFn>
+__device__ __forceinline__ void stage_tile(uint16_t (*dst)[kLdsK], RowFn rowptr, int k0, int K) {
+  const int i = threadIdx.x / 4, q = threadIdx.x % 4;
+  const uint16_t *p = rowptr(i);
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (p && k0 + q * 8 < K) v = *reinterpret_cast<const uint4 *>(p + q * 8);
+  *reinterpret_cast<uint4 *>(&dst[i][q * 8]) = v;
+}
+
+__device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row, int lane) {
+  const uint4 v = *reinterpret_cast<const uint4 *>(&src[row][(lane / 16) * 8]);
+  bf16x8 r;
+  __builtin_memcpy(&r, &v, sizeof v);
+  return r;
+}
+
+// act[row, n] = SiLU(x_row . W1[n]) * (x_row . W3[n]) for one 64 x 64 tile
+__global__ __launch_bounds__(256) void prefill_up_kernel(const GemmTile *tiles, const GemmJob *jobs,
+                                                         const uint16_t *xn, const int32_t *perm_tok,
+                                                         uint16_t *act, int d, int d_ff) {
+  __shared__ uint16_t As[kTile][kLdsK], B1[kTile][kLdsK], B3[kTile][kLdsK];
+  const GemmTile t = tiles[blockIdx.x];
+  const GemmJob j = jobs[t.job];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int wm = wave / 2, wn = wave % 2;
+  const uint16_t *w1 = j.w;
+  const uint16_t *w3 = j.w + (size_t)d_ff * d;
+  floatx4 c1[2][2], c3[2][2];
+  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b)
+      for (int i = 0; i < 4; ++i) c1[a][b][i] = c3[a][b][i] = 0.0f;
+  for (int k0 = 0; k0 < d; k0 += kKStep) {
+    stage_tile(As, [&](int i) -> const uint16_t * {
+      const int m = t.m0 + i;
+      if (m >= j.nrows) return nullptr;
+      return xn + (size_t)perm_tok[j.row0 + m] * d + k0;
+    }, k0, d);
+    stage_tile(B1, [&](int i) -> const uint16_t * {
+      const int n = t.n0 + i;
+      return n < d_ff ? w1 + (size_t)n * d + k0 : nullptr;
+    }, k0, d);
+    stage_tile(B3, [&](int i) -> const uint16_t * {
+      const int n = t.n0 + i;
+      return n < d_ff ? w3 + (size_t)n * d + k0 : nullptr;
+    }, k0, d);
+    __syncthreads();
+    bf16x8 af[2], b1f[2], b3f[2];
+    for (int a = 0; a < 2; ++a) af[a] = lds_frag(As, wm * 32 + a * 16 + lane % 16, lane);
+    for (int b = 0; b < 2; ++b) {
+      b1f[b] = lds_frag(B1, wn * 32 + b * 16 + lane % 16, lane);
+      b3f[b] = lds_frag(B3, wn * 32 + b * 16 + lane % 16, lane);
+    }
+    for (int a = 0; a < 2; ++a)
+      for (int b = 0; b < 2; ++b) {
+        c1[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], b1f[b], c1[a][b], 0, 0, 0);
+        c3[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], b3f[b], c3[a][b], 0, 0, 0);
+      }
+    __syncthreads();
+  }
+  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b)
+      for (int i = 0; i < 4; ++i) {
+        const int m = t.m0 + wm * 32 + a * 16 + (lane / 16) * 4 + i;
+        const int n = t.n0 + wn * 32 + b * 16 + lane % 16;
+        if (m < j.nrows && n < d_ff)
+          act[(size_t)(j.row0 + m) * d_ff + n] = f32_to_bf16_rne(silu(c1[a][b][i]) * c3[a][b][i]);
+      }
+}
+
+// Y[row, n] = act_row . W2[n] for one 64 x 64 tile
+__global__ __launch_bounds__(256) void prefill_down_kernel(const GemmTile *tiles, const GemmJob *jobs,
+                                                           const uint16_t *act, float *Y, int d, int d_ff) {
+  __shared__ uint16_t As[kTile][kLdsK], Bs[kTile][kLdsK];
+  const GemmTile t = tiles[blockIdx.x];
+  const GemmJob j = jobs[t.job];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int wm = wave / 2, wn = wave % 2;
+  const uint16_t *w2 = j.w + 2 * (size_t)d_ff * d;
+  floatx4 c[2][2];
+  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b)
+      for (int i = 0; i < 4; ++i) c[a][b][i] = 0.0f;
+  for (int k0 = 0; k0 < d_ff; k0 += kKStep) {
+    stage_tile(As, [&](int i) -> const uint16_t * {
+      const int m = t.m0 + i;
+      return m < j.nrows ? act + (size_t)(j.row0 + m) * d_ff + k0 : nullptr;
+    }, k0, d_ff);
+    stage_tile(Bs, [&](int i) -> const uint16_t * {
+      const int n = t.n0 + i;
+      return n < d ? w2 + (size_t)n * d_ff + k0 : nullptr;
+    }, k0, d_ff);
+    __syncthreads();
+    bf16x8 af[2], bf[2];
+    for (int a = 0; a < 2; ++a) af[a] = lds_frag(As, wm * 32 + a * 16 + lane % 16, lane);
+    for (int b = 0; b < 2; ++b) bf[b] = lds_frag(Bs, wn * 32 + b * 16 + lane % 16, lane);
+    for (int a = 0; a < 2; ++a)
+      for (int b = 0; b < 2; ++b)
+        c[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bf[b], c[a][b], 0, 0, 0);
+    __syncthreads();
+  }
+  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b)
+      for (int i = 0; i < 4; ++i) {
+        const int m = t.m0 + wm * 32 + a * 16 + (lane / 16) * 4 + i;
+        const int n = t.n0 + wn * 32 + b * 16 + lane % 16;
+        if (m < j.nrows && n < d) Y[(size_t)(j.row0 + m) * d + n] = c[a][b][i];
+      }
+}
+
+// ---------------------------------------------------------------------------
+// 4. h_t += sum_r g_tr Y[pos(t, r)], ranks in order
+__global__ __launch_bounds__(256) void prefill_unpermute_kernel(float *H, const float *Y, const float *g,
+                                                                const int32_t *pos_of, int T, int d, int K) {
+  const int t = blockIdx.x;
+  if (t >= T) return;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float y = 0.0f;
+    for (int r = 0; r < K; ++r) y = fmaf(g[(size_t)t * K + r], Y[(size_t)pos_of[(size_t)t * K + r] * d + c], y);
+    H[(size_t)t * d + c] += y;
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// launchers used by the host engine
+hipError_t launch_prefill_gate(const PrefillArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(prefill_gate_kernel, dim3((a.T + kGateTok - 1) / kGateTok), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_plan(const PlanArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(prefill_plan_kernel, dim3(1), dim3(1024), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL(prefill_up_kernel, dim3(ntiles), dim3(256), 0, s, tiles, jobs, xn, perm_tok, act, d, d_ff);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
+                               float *Y, int d, int d_ff, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL(prefill_down_kernel, dim3(ntiles), dim3(256), 0, s, tiles, jobs, act, Y, d, d_ff);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
+                                    int d, int K, hipStream_t s) {
+  hipLaunchKernelGGL(prefill_unpermute_kernel, dim3(T), dim3(256), 0, s, H, Y, g, pos_of, T, d, K);
+  return hipGetLastError();
+}
+
+int prefill_tile_rows() { return kTile; }
 
 }  // namespace moe

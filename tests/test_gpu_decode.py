@@ -12,47 +12,12 @@ from oracle import stack
 from oracle.cache import LayerCache
 from paper_2511_05814_amd import binding as b
 from paper_2511_05814_amd import workload as wl
+from tests._gpu_rig import Rig, _say, _tol
 from tests._parity import check_decode
 
 pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
-
-
-def _say(*a):
-    print("[gpu-test]", *a, flush=True)
-
-
-def _tol(cfg):
-    return 1e-5 if cfg.dtype == "f32" else 2e-2
-
-
-class Rig:
-    """Host store + gates + oracle model for one configuration."""
-
-    def __init__(self, cfg):
-        from paper_2511_05814_amd import offload
-        self.cfg = cfg
-        self.store = offload.HostStore(cfg)
-        self.gates = offload.DeviceGates(cfg)
-        self.model = stack.Model(self.gates.host, lambda l, e: self.store.expert(l, e),
-                                 cfg.d_model, cfg.d_ff, cfg.dtype)
-
-    def cache(self, slots, policy, **kw):
-        from paper_2511_05814_amd import offload
-        return offload.OffloadedMoE(self.cfg, self.store, self.gates, slots, policy, **kw)
-
-    def run(self, moe, tokens, flags=0, h0=None):
-        cfg = self.cfg
-        if h0 is None:
-            h0 = wl.hidden_states(cfg, tokens)
-        H = torch.from_numpy(np.ascontiguousarray(h0[:tokens])).to("cuda")
-        snaps = torch.empty((tokens, cfg.layers + 1, cfg.d_model), device="cuda")
-        moe.decode(H, flags=flags, snapshots=snaps)
-        moe.sync()
-        recs, dropped = moe.trace_records()
-        assert dropped == 0
-        return snaps.cpu().numpy().astype(np.float64), recs, H.cpu().numpy()
 
 
 @pytest.fixture(scope="module")

@@ -1,0 +1,111 @@
+"""GPU parity of the batched prefill (moe_prefill_layer) against the oracle.
+
+Per layer: the routing of every row must equal the oracle's fp64 routing
+wherever certified, the per-expert prefill records and the final tables must
+match the oracle's batch rule exactly, and sampled rows' outputs must match
+the fp64 SwiGLU within 2e-2 relative L2 (bf16 weights; the grouped GEMMs take
+bf16 inputs).  Decode then continues from the prefilled caches and is checked
+teacher-forced like any decode run.
+"""
+import numpy as np
+import pytest
+
+from oracle import moe as omoe
+from oracle import stack
+from oracle.cache import make_caches
+from paper_2511_05814_amd import binding as b
+from paper_2511_05814_amd import workload as wl
+from tests._gpu_rig import Rig, _say
+from tests._parity import check_decode, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def prefill_and_check(rig, moe, policy, slots, T, sample_rows, tol=2e-2):
+    cfg = rig.cfg
+    K, L = cfg.top_k, cfg.layers
+    h = wl.hidden_states(cfg, T + cfg.tokens)
+    H = torch.from_numpy(np.ascontiguousarray(h[:T])).to("cuda")
+    caches = make_caches(L, cfg.experts, slots, policy)
+    worst = 0.0
+    unc = 0
+    torch.cuda.synchronize()
+    for l in range(L):
+        hin = H.cpu().numpy().astype(np.float64)
+        with torch.cuda.stream(moe.compute):
+            b.moe_prefill_layer(moe.handle, l, H.data_ptr(), T)
+        moe.sync()
+        gids, gg, n = b.moe_cache_last_routing(moe.handle, T * K)
+        assert n == T * K
+        gids = np.array(gids).reshape(T, K)
+        hout = H.cpu().numpy().astype(np.float64)
+        _, ids, g, cert, _ = stack.prefill_layer(rig.model, l, hin, K, None, with_ffn=False)
+        unc += int((~cert).sum())
+        assert np.array_equal(ids[cert], gids[cert]), f"layer {l}: routing differs"
+        merged = np.where(cert[:, None], ids, gids)
+        np.testing.assert_allclose(np.array(gg).reshape(T, K)[cert], g[cert], rtol=2e-6, atol=1e-7)
+        want = caches[l].prefill(merged)
+        recs, _ = moe.trace_records()
+        got = [r for r in recs if r[0] == 2 and r[2] == l]
+        assert got == [w.astuple() for w in want], f"layer {l}: prefill records differ"
+        for t in sample_rows:
+            r = omoe.rms(hin[t])
+            y = omoe.moe_output(lambda e: rig.model.expert(l, e), merged[t], g[t], hin[t] / r)
+            worst = max(worst, rel_l2(hout[t] - hin[t], y))
+        se, es, cnt, last, clock = moe.state(l)
+        assert (se, es, cnt, last, clock) == caches[l].state()
+    assert worst <= tol, worst
+    return h, caches, worst, unc
+
+
+@pytest.mark.parametrize("policy", ["lfu", "lru"])
+def test_prefill_fine_grained_two_layers(policy):
+    cfg = wl.CONFIGS["fine-grained"].with_(layers=2, tokens=10, prefill_tokens=300)
+    _say("prefill fine-grained", policy, cfg)
+    rig = Rig(cfg)
+    moe = rig.cache(16, policy, prefetch_max=2, max_prefill_tokens=300)
+    h, caches, worst, unc = prefill_and_check(rig, moe, policy, 16, 300, [0, 1, 63, 64, 150, 299])
+    _say("prefill worst y", worst, "uncertified", unc)
+    # decode continues from the prefilled caches
+    hs = []
+    H = torch.from_numpy(np.ascontiguousarray(h[300:])).to("cuda")
+    snaps = torch.empty((cfg.tokens, cfg.layers + 1, cfg.d_model), device="cuda")
+    moe.decode(H, flags=b.MOE_PREFETCH_NEXT, snapshots=snaps)
+    moe.sync()
+    recs, _ = moe.trace_records()
+    dec = [r for r in recs if r[0] != 2]
+    check_decode(cfg, rig.model, snaps.cpu().numpy().astype(np.float64), dec, 16, policy,
+                 prefetch=True, pmax=2, y_tokens=[0, 9], tol=2e-2, caches=caches)
+    st = moe.stats()
+    for l in range(cfg.layers):
+        assert st[l]["lookups"] == 300 + cfg.tokens
+    moe.close()
+    rig.store.close()
+
+
+def test_prefill_ragged_shapes():
+    # d, d_ff not multiples of the 64 x 64 GEMM tile or the 32-deep k step;
+    # T not a multiple of anything; 5 experts, top-3, 3 slots
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=2, experts=5, top_k=3, d_model=136, d_ff=200,
+                                         dtype="bf16", tokens=4, prefill_tokens=37)
+    _say("prefill ragged", cfg)
+    rig = Rig(cfg)
+    moe = rig.cache(3, "lfu", prefetch_max=1, max_prefill_tokens=64)
+    prefill_and_check(rig, moe, "lfu", 3, 37, list(range(37)))
+    moe.close()
+    rig.store.close()
+
+
+def test_prefill_rejects_bad_token_counts():
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=1, dtype="bf16", d_model=64, d_ff=64)
+    rig = Rig(cfg)
+    moe = rig.cache(4, "lfu", max_prefill_tokens=16)
+    H = torch.zeros((32, 64), device="cuda")
+    for T in (0, 17, -1):
+        with pytest.raises(b.MoeError) as e:
+            b.moe_prefill_layer(moe.handle, 0, H.data_ptr(), T)
+        assert e.value.code == b.MOE_ERR_ARG
+    moe.close()
+    rig.store.close()
