@@ -1,20 +1,28 @@
 """Benchmark: batch-1 MoE decode under expert offloading on one MI355X.
 
-Workload (one step): 256 batch-1 decode tokens through one Mixtral-8x7B-shaped
-MoE layer (8 experts, top-2, d=4096, d_ff=14336, bf16 experts in pinned host
-memory), 4 HBM expert slots, LFU eviction; seeded synthetic hidden states
-with Zipf(1.1) concept skew and Markov(0.6) persistence.  Each step starts
-from the same warm cache (experts 0..3 resident); the warm start and the
-restore of the input hidden states are outside the timed region.
+Default workload (one step): 256 batch-1 decode tokens through one
+Mixtral-8x7B-shaped MoE layer (8 experts, top-2, d=4096, d_ff=14336, bf16
+experts in pinned host memory), 4 HBM expert slots, LFU eviction; seeded
+synthetic hidden states with Zipf(1.1) concept skew and Markov(0.6)
+persistence.  Each step starts from the same warm cache (experts 0..S-1
+resident); the warm start and the restore of the input hidden states are
+outside the timed region.
+
+`--workload` selects one of the other configurations instead (32-layer
+Mixtral-shaped stack with 2/4/6 slots, the same stack with next-layer
+prefetch, the 64-expert stack with a 4096-token prefill); those print the
+same JSON schema.
 
 Prints one JSON line: decode tokens/s (LFU) and, alongside, LRU tokens/s,
-hit rates, the FFN kernels' HBM roofline (event-timed inside the timed
-region), the fetch kernel's host-link roofline against the H2D rate measured
-here, and the fp64 oracle timed on a bounded sample on the host cores.
+hit rates, cache and speculation precision/recall, the decode FFN kernels'
+HBM roofline (HIP-event timed inside the timed region), the fetch kernel's
+host-link roofline against the H2D rate measured here, and the fp64 oracle
+timed on a bounded sample on the host cores.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -26,6 +34,23 @@ if ROOT not in sys.path:
 
 METRIC = "decode tokens/s per MoE stack at fixed cache slots; expert-FFN HBM GB/s; hit rate"
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "ffn_up_mixtral_layer_pmc.json")
+
+DESCRIPTIONS = {
+    "tiny-stack": "tiny-stack: 2 MoE layers, 8 experts, top-2, d_model 256, d_ff 512 SwiGLU, fp32, "
+                  "64 batch-1 decode tokens, 4 slots",
+    "mixtral-layer": "mixtral-layer: 1 MoE layer, 8 experts, top-2, d_model 4096, d_ff 14336 SwiGLU, "
+                     "bf16 experts in pinned host memory, 256 batch-1 decode tokens, 4 HBM slots, "
+                     "Zipf(1.1)+Markov(0.6) routing skew",
+    "mixtral-stack": "mixtral-stack: 32 Mixtral-shaped MoE layers (8 experts, top-2, d_model 4096, "
+                     "d_ff 14336, bf16, 90 GB of experts in pinned host memory), batch-1 decode, "
+                     "slots per layer swept",
+    "mixtral-stack-prefetch": "mixtral-stack-prefetch: the 32-layer Mixtral-shaped stack, 4 slots, LFU, "
+                              "next-layer speculative prefetch of up to 2 experts",
+    "fine-grained": "fine-grained: 24 MoE layers, 64 experts, top-8, d_model 2048, d_ff 1408, bf16; "
+                    "4096-token batched prefill then batch-1 decode; 16 slots, LFU + prefetch 2, Zipf(1.2)",
+}
 
 
 def log(*a):
@@ -48,12 +73,39 @@ def measure_link(torch, nbytes=1 << 30, reps=3):
     return best
 
 
-def run_steps(torch, b, moe, H0, H, n, timing):
-    """n decode passes over all tokens; returns (seconds, timing dict or None,
-    layer-0 statistics summed over the passes)."""
-    total = 0.0
+def calibrate_counters(torch, nbytes=512 << 20):
+    """One plain device-to-device copy of known size (512 MiB read, 512 MiB
+    written), so that hardware byte counters collected on this program can be
+    scaled: factor = known bytes / counter reading of this copy."""
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def pmc_traffic():
+    """Per-launch HBM bytes of ffn_up_kernel from the committed counter runs,
+    or None when the kernel source changed since they were taken."""
+    try:
+        with open(PMC_SUMMARY) as f:
+            s = json.load(f)
+        with open(os.path.join(ROOT, s["source"]), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != s["source_sha256"]:
+                return None
+        return int(round(1024 * (s["fetch_kib"] * s["fetch_factor"] + s["write_kib"] * s["write_factor"])))
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0):
+    """n passes (reset, [prefill], decode all tokens); returns seconds of
+    decode, seconds of prefill, summed timing, summed per-layer statistics and
+    the trace of the last pass."""
+    dec = pre = 0.0
     tim = None
     stats = None
+    recs = None
     b.moe_cache_set_timing(moe.handle, bool(timing))
     for _ in range(n):
         moe.reset()
@@ -61,29 +113,37 @@ def run_steps(torch, b, moe, H0, H, n, timing):
         torch.cuda.synchronize()
         if timing:
             b.moe_cache_read_timing(moe.handle)  # drop spans of the reset
+        if prefill_tokens:
+            t0 = time.perf_counter()
+            moe.prefill(H[:prefill_tokens])
+            moe.sync()
+            torch.cuda.synchronize()
+            pre += time.perf_counter() - t0
         t0 = time.perf_counter()
-        moe.decode(H)
+        moe.decode(H[prefill_tokens:], flags=flags)
         moe.sync()
         torch.cuda.synchronize()
-        total += time.perf_counter() - t0
+        dec += time.perf_counter() - t0
         if timing:
             t = b.moe_cache_read_timing(moe.handle)
             tim = t if tim is None else {k: tim[k] + t[k] for k in t}
-        st = moe.stats()[0]
-        stats = st if stats is None else {k: stats[k] + st[k] for k in st}
+        st = moe.stats()
+        stats = st if stats is None else [{k: a[k] + c[k] for k in a} for a, c in zip(stats, st)]
+        recs, _ = moe.trace_records()
     b.moe_cache_set_timing(moe.handle, False)
-    return total, tim, stats
+    return dec, pre, tim, stats, recs
 
 
 def cpu_baseline(cfg, store, gates_host, h0, tokens, slots, policy):
     """The fp64 oracle (router, cache, SwiGLU FFN, residual) on the first
-    `tokens` tokens of the same workload, timed on this host's cores."""
+    `tokens` decode tokens of the same workload, timed on this host's cores."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import stack
     from oracle.cache import make_caches
-    model = stack.Model(gates_host, lambda l, e: store.expert(l, e), cfg.d_model, cfg.d_ff, cfg.dtype)
+    model = stack.Model(gates_host, lambda l, e: store.expert(l, e), cfg.d_model, cfg.d_ff, cfg.dtype,
+                        keep=cfg.layers * cfg.experts * cfg.expert_bytes < (8 << 30))
     caches = make_caches(cfg.layers, cfg.experts, slots, policy)
     t0 = time.perf_counter()
     stack.decode_free(model, h0[:tokens].astype(np.float64), cfg.top_k, policy, slots, caches=caches)
@@ -92,67 +152,110 @@ def cpu_baseline(cfg, store, gates_host, h0, tokens, slots, policy):
     return tokens / dt, dt, threads
 
 
+def summarize(cfg, r):
+    """Throughput, hit rate, cache P/R and guess P/R of one (policy, slots) run."""
+    from paper_2511_05814_amd import analysis
+    acc = [x for x in r["recs"] if x[0] != 2]
+    out = {
+        "tokens_per_s": round(r["steps"] * cfg.tokens / r["dec"], 3),
+        "hit_rate": round(analysis.hit_rate(acc), 4),
+        "cache_precision_recall": [round(v, 4) for v in analysis.cache_precision_recall(acc, r["slots"])],
+        "bytes_fetched_per_step": sum(s["bytes_fetched"] for s in r["stats"]) // r["steps"],
+    }
+    if r["flags"]:
+        p, rc = analysis.guess_precision_recall(acc)
+        out["guess_precision_recall"] = [round(p, 4), round(rc, 4)]
+        out["transfer_precision"] = round(analysis.transfer_precision(acc), 4)
+    if r["pre"]:
+        out["prefill_tokens_per_s"] = round(r["steps"] * cfg.prefill_tokens / r["pre"], 1)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="mixtral-layer", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--cpu-tokens", type=int, default=8,
                     help="decode tokens the fp64 oracle is timed on (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--fetch", choices=["kernel", "dma"], default="kernel")
+    ap.add_argument("--tokens", type=int, default=0,
+                    help="decode only the first N tokens of the workload (profiling passes)")
+    ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the decode path runs on a single GPU with no collectives)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     from paper_2511_05814_amd import binding as b
     from paper_2511_05814_amd import offload, workload as wl
 
-    cfg = wl.CONFIGS["mixtral-layer"]
-    slots = 4
+    cfg = wl.CONFIGS[args.workload]
+    if args.tokens:
+        cfg = cfg.with_(tokens=min(args.tokens, cfg.tokens))
     fetch_mode = b.MOE_FETCH_KERNEL if args.fetch == "kernel" else b.MOE_FETCH_DMA
+    primary_slots = 16 if cfg.experts == 64 else 4
+    # (policy, slots, speculate): the first entry is the timed headline run
+    runs = [("lfu", primary_slots, cfg.prefetch_max > 0)]
+    if not args.lfu_only:
+        if args.workload in ("mixtral-layer", "tiny-stack"):
+            runs.append(("lru", primary_slots, False))
+        elif args.workload == "mixtral-stack":
+            runs += [("lru", 4, False)] + [(p, s, False) for s in (2, 6) for p in ("lru", "lfu")]
+        elif args.workload == "mixtral-stack-prefetch":
+            runs.append(("lfu", 4, False))
+        elif args.workload == "fine-grained":
+            runs.append(("lfu", 16, False))
+
     log("generating", cfg.name, "host store", cfg.layers * cfg.experts * cfg.expert_bytes / 1e9, "GB")
     t0 = time.perf_counter()
     store = offload.HostStore(cfg)
     gates = offload.DeviceGates(cfg)
-    h0 = wl.hidden_states(cfg, cfg.tokens)
+    h0 = wl.hidden_states(cfg)
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s")
     link = measure_link(torch)
     log(f"measured pinned H2D link: {link:.2f} GB/s")
+    calibrate_counters(torch)
 
-    H0 = torch.from_numpy(h0).to("cuda")
+    H0 = torch.from_numpy(h0[:cfg.prefill_tokens + cfg.tokens]).to("cuda")
     H = torch.empty_like(H0)
-    results = {}
-    for policy in ("lfu", "lru"):
-        moe = offload.OffloadedMoE(cfg, store, gates, slots, policy, fetch_mode=fetch_mode)
-        timed = args.steps if policy == "lfu" else 1
-        run_steps(torch, b, moe, H0, H, args.warmup if policy == "lfu" else 0, False)
-        secs, tim, st = run_steps(torch, b, moe, H0, H, timed, True)
-        results[policy] = dict(secs=secs, steps=timed, timing=tim, stats=st)
-        log(policy, f"{timed * cfg.tokens / secs:.1f} tok/s", "hits", st["hits"], "misses", st["misses"])
+    results = []
+    for i, (policy, slots, spec) in enumerate(runs):
+        flags = b.MOE_PREFETCH_NEXT if spec else 0
+        moe = offload.OffloadedMoE(cfg, store, gates, slots, policy,
+                                   prefetch_max=cfg.prefetch_max if spec else 0, fetch_mode=fetch_mode,
+                                   max_prefill_tokens=cfg.prefill_tokens)
+        steps = args.steps if i == 0 else 1
+        if i == 0 and args.warmup:
+            run_steps(torch, b, moe, H0, H, args.warmup, False, flags, cfg.prefill_tokens)
+        dec, pre, tim, st, recs = run_steps(torch, b, moe, H0, H, steps, True, flags, cfg.prefill_tokens)
+        results.append(dict(policy=policy, slots=slots, flags=flags, steps=steps, dec=dec, pre=pre,
+                            timing=tim, stats=st, recs=recs))
+        log(policy, slots, "prefetch" if spec else "", f"{steps * cfg.tokens / dec:.2f} tok/s")
         moe.close()
 
-    lfu = results["lfu"]
+    head = results[0]
     K, d, dff, eb = cfg.top_k, cfg.d_model, cfg.d_ff, cfg.elem_bytes
-    tim = lfu["timing"]
+    tim = head["timing"]
     # algorithmic bytes per launch: the selected experts' weights plus the
     # activation vectors the kernel reads and writes
     up_bytes = K * 2 * d * dff * eb + d * 4 + K * dff * 4
-    down_bytes = K * d * dff * eb + K * dff * 4 + 2 * d * 4
+    down_bytes = K * d * dff * eb + K * dff * 4 + d * 4
     up_ms = tim["ffn_up_ms"] / tim["ffn_up_n"]
     down_ms = tim["ffn_down_ms"] / tim["ffn_down_n"]
     up_gbps = up_bytes / (up_ms * 1e-3) / 1e9
     down_gbps = down_bytes / (down_ms * 1e-3) / 1e9
-    ffn_gbps = (up_bytes + down_bytes) / ((up_ms + down_ms) * 1e-3) / 1e9
-    fetched = lfu["stats"]["bytes_fetched"]
+    fetched = sum(s["bytes_fetched"] for s in head["stats"])
     fetch_gbps = fetched / (tim["fetch_ms"] * 1e-3) / 1e9 if tim["fetch_ms"] > 0 else None
-    tokens_per_s = lfu["steps"] * cfg.tokens / lfu["secs"]
-    lru = results["lru"]
+    tokens_per_s = head["steps"] * cfg.tokens / head["dec"]
+    traffic = pmc_traffic() if args.workload == "mixtral-layer" else None
+    summary = {f"{r['policy']}-s{r['slots']}" + ("-prefetch" if r["flags"] else ""): summarize(cfg, r)
+               for r in results}
 
     out = {
         "metric": METRIC,
@@ -161,26 +264,25 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(1e3 * lfu["secs"] / lfu["steps"], 3),
+        "ms_per_step": round(1e3 * (head["dec"] + head["pre"]) / head["steps"], 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "mixtral-layer: 1 MoE layer, 8 experts, top-2, d_model 4096, d_ff 14336 "
-                        "SwiGLU, bf16 experts in pinned host memory, 256 batch-1 decode tokens, "
-                        "4 HBM slots, LFU, Zipf(1.1)+Markov(0.6) routing skew",
-            "weights_dtype": "bf16",
-            "policy": "lfu",
-            "slots": slots,
-            "tokens_per_step": cfg.tokens,
+            "workload": DESCRIPTIONS[args.workload] + (f" (first {cfg.tokens} tokens)" if args.tokens else ""),
+            "weights_dtype": cfg.dtype,
+            "policy": head["policy"],
+            "slots": head["slots"],
+            "speculative_prefetch": cfg.prefetch_max if head["flags"] else 0,
+            "decode_tokens_per_step": cfg.tokens,
+            "prefill_tokens_per_step": cfg.prefill_tokens,
             "fetch": args.fetch,
         },
-        "hit_rate": round(lfu["stats"]["hits"] / (lfu["stats"]["lookups"] * K), 4),
-        "lru": {"tokens_per_s": round(lru["steps"] * cfg.tokens / lru["secs"], 3),
-                "hit_rate": round(lru["stats"]["hits"] / (lru["stats"]["lookups"] * K), 4)},
-        "ffn_hbm_gbps": round(ffn_gbps, 1),
+        "hit_rate": next(iter(summary.values()))["hit_rate"],
+        "runs": summary,
+        "ffn_hbm_gbps": round((up_bytes + down_bytes) / ((up_ms + down_ms) * 1e-3) / 1e9, 1),
         "roofline": {
             "kernel": "ffn_up_kernel",
             "bound": "hbm",
@@ -188,13 +290,14 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(up_gbps / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": traffic,
             "bytes_per_launch": up_bytes,
             "avg_launch_us": round(up_ms * 1e3, 2),
             "launches": tim["ffn_up_n"],
         },
         "ffn_down": {"achieved_gbps": round(down_gbps, 1), "frac": round(down_gbps / HBM_PEAK_GBPS, 4),
-                     "bytes_per_launch": down_bytes, "avg_launch_us": round(down_ms * 1e3, 2)},
+                     "bytes_per_launch": down_bytes, "avg_launch_us": round(down_ms * 1e3, 2),
+                     "reduce_avg_us": round(1e3 * tim["ffn_reduce_ms"] / max(1, tim["ffn_reduce_n"]), 2)},
         "link_roofline": {
             "kernel": "fetch_kernel",
             "bound": "host-link",
@@ -203,17 +306,29 @@ def main():
             "unit": "GB/s",
             "frac": round(fetch_gbps / link, 4) if fetch_gbps else None,
             "peak_is": "best measured 1 GiB pinned H2D copy",
-            "bytes_fetched_per_step": fetched // lfu["steps"],
-            "misses_per_step": lfu["stats"]["misses"] // lfu["steps"],
+            "bytes_fetched_per_step": fetched // head["steps"],
         },
         "router_us": round(1e3 * tim["router_ms"] / tim["router_n"], 2),
     }
+    if cfg.prefill_tokens:
+        mf = {"bound": "mfma", "unit": "TFLOP/s", "peak": MFMA_BF16_PEAK_TFLOPS,
+              "gemm_launches": tim["gemm_up_n"] + tim["gemm_down_n"],
+              "prefill_layer_ms": round(tim["prefill_ms"] / max(1, tim["prefill_n"]), 3)}
+        for k in ("up", "down"):
+            ms = tim[f"gemm_{k}_ms"]
+            v = tim[f"gemm_{k}_flop"] / 1e12 / (ms * 1e-3) if ms else None
+            mf[f"gemm_{k}_tflops"] = round(v, 1) if v else None
+            mf[f"gemm_{k}_frac"] = round(v / MFMA_BF16_PEAK_TFLOPS, 4) if v else None
+        out["prefill_mfma"] = mf
 
     if not args.no_cpu_baseline and args.cpu_tokens > 0:
-        tps, dt, thr = cpu_baseline(cfg, store, gates.host, h0, args.cpu_tokens, slots, "lfu")
+        n = min(args.cpu_tokens, cfg.tokens)
+        h_dec = h0[cfg.prefill_tokens:]
+        tps, dt, thr = cpu_baseline(cfg, store, gates.host, h_dec, n, primary_slots, "lfu")
         out["cpu_baseline"] = {"value": round(tps, 4), "unit": "tokens/s", "cores": thr, "kind": "oracle",
-                               "sample": f"first {args.cpu_tokens} of the 256 decode tokens, fp64 router + "
-                                         f"cache + SwiGLU FFN (bf16->fp64 widening included), {dt:.1f}s"}
+                               "sample": f"first {n} of the {cfg.tokens} decode tokens, fp64 router + cache + "
+                                         f"SwiGLU FFN through all {cfg.layers} layers (bf16->fp64 widening "
+                                         f"included), {dt:.1f}s"}
     store.close()
     print(json.dumps(out), flush=True)
 

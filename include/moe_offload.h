@@ -72,7 +72,7 @@ typedef struct {
   const void *gate_w;        /* device [L][E][d], dtype, row-major                     */
   const void *host_experts;  /* pinned host [L][E][W1|W3|W2]; W1, W3 [d_ff x d],
                                 W2 [d x d_ff], each row-major (out x in), dtype;
-                                16-byte aligned                                       */
+                                16-byte aligned (may be NULL if host_layers is set)  */
   void *arena;               /* device [L][S][W1|W3|W2], 16-byte aligned              */
   void *workspace;           /* device, >= moe_cache_workspace_bytes(), 256-aligned   */
   size_t workspace_bytes;
@@ -80,6 +80,10 @@ typedef struct {
   size_t trace_cap;          /* records in the ring                                  */
   void *compute_stream;      /* hipStream_t for router and FFN work (NULL: default)  */
   void *copy_stream;         /* hipStream_t for expert copies (NULL: compute stream) */
+  const void *const *host_layers; /* host array of L pinned pointers, layer l's experts
+                                     [E][W1|W3|W2] at host_layers[l]; when non-NULL it
+                                     replaces host_experts, so a store can span several
+                                     allocations (entries may repeat); 16-byte aligned */
 } moe_model_desc;
 
 /* One trace record.  kind 0 (access): a token's lookup of one of its K
@@ -174,8 +178,9 @@ int moe_cache_read_state(moe_cache_t *c, int layer, int32_t *slot_expert,
 int moe_cache_last_routing(moe_cache_t *c, int32_t *ids, float *g, size_t cap, size_t *n);
 
 typedef struct {
-  double router_ms, fetch_ms, ffn_up_ms, ffn_down_ms, prefill_ms, gemm_up_ms, gemm_down_ms;
-  uint64_t router_n, fetch_n, ffn_up_n, ffn_down_n, prefill_n, gemm_up_n, gemm_down_n;
+  double router_ms, fetch_ms, ffn_up_ms, ffn_down_ms, prefill_ms, gemm_up_ms, gemm_down_ms,
+      ffn_reduce_ms;
+  uint64_t router_n, fetch_n, ffn_up_n, ffn_down_n, prefill_n, gemm_up_n, gemm_down_n, ffn_reduce_n;
   double gemm_up_flop, gemm_down_flop; /* algorithmic flops of the timed GEMM launches */
 } moe_timing;
 

@@ -1,0 +1,98 @@
+"""Trace analytics over the device trace (host side, integer bookkeeping only).
+
+The paper's tracing system records, per layer and token, which experts were
+activated and which were cached (Sec. 3.1), and derives cache precision and
+recall (Sec. 4.2, Table 2) and the speculative guesses' precision and recall
+(Sec. 5.4).  These functions compute the same quantities from the records
+the library writes (`moe_trace_rec` tuples: kind, token, layer, rank, expert,
+flags, slot, victim).
+"""
+from __future__ import annotations
+
+from collections import defaultdict
+from typing import Iterable, Sequence
+
+ACCESS, PREFETCH, PREFILL = 0, 1, 2
+
+
+def split(records: Iterable[Sequence[int]]):
+    acc, pf, pre = [], [], []
+    for r in records:
+        (acc if r[0] == ACCESS else pf if r[0] == PREFETCH else pre).append(r)
+    return acc, pf, pre
+
+
+def hit_rate(records) -> float:
+    acc, _, _ = split(records)
+    return sum(1 for r in acc if r[5] & 1) / max(1, len(acc))
+
+
+def per_layer_hit_rate(records):
+    n, h = defaultdict(int), defaultdict(int)
+    for r in records:
+        if r[0] == ACCESS:
+            n[r[2]] += 1
+            h[r[2]] += r[5] & 1
+    return {l: h[l] / n[l] for l in sorted(n)}
+
+
+def cache_precision_recall(records, slots: int):
+    """recall = activated experts found resident / activated experts;
+    precision = the same hits / resident experts at each lookup (S per lookup)."""
+    acc, _, _ = split(records)
+    lookups = {(r[2], r[1]) for r in acc}
+    hits = sum(1 for r in acc if r[5] & 1)
+    if not acc:
+        return 0.0, 0.0
+    return hits / (slots * len(lookups)), hits / len(acc)
+
+
+def guess_precision_recall(records):
+    """Guesses for (layer, token) against that token's activations at that layer.
+    Every wrong guess is one false positive and one false negative, so the two
+    agree when each side has K experts (Sec. 5.4)."""
+    act, guess = defaultdict(set), defaultdict(set)
+    for r in records:
+        if r[0] == ACCESS:
+            act[(r[2], r[1])].add(r[4])
+        elif r[0] == PREFETCH:
+            guess[(r[2], r[1])].add(r[4])
+    tp = ng = na = 0
+    for key, g in guess.items():
+        if key in act:
+            tp += len(g & act[key])
+            ng += len(g)
+            na += len(act[key])
+    return (tp / ng if ng else 0.0), (tp / na if na else 0.0)
+
+
+def transfer_precision(records) -> float:
+    """Prefetched experts used by the next lookup / prefetched experts fetched."""
+    issued = sum(1 for r in records if r[0] == PREFETCH and r[5] & 2)
+    useful = sum(1 for r in records if r[0] == ACCESS and r[5] & 2)
+    return useful / issued if issued else 0.0
+
+
+def activation_histogram(records, layer: int, experts: int):
+    """Activations per expert at one layer (Sec. 5.2's histograms)."""
+    h = [0] * experts
+    for r in records:
+        if r[0] == ACCESS and r[2] == layer:
+            h[r[4]] += 1
+    return h
+
+
+def repeat_rate(records, layer: int) -> float:
+    """Fraction of a token's experts that the previous token also selected at
+    this layer (Sec. 3.1 compares this with 1/E for random choice)."""
+    by_tok = defaultdict(set)
+    for r in records:
+        if r[0] == ACCESS and r[2] == layer:
+            by_tok[r[1]].add(r[4])
+    toks = sorted(by_tok)
+    same = total = 0
+    for a, b in zip(toks[:-1], toks[1:]):
+        if b == a + 1:
+            same += len(by_tok[a] & by_tok[b])
+            total += len(by_tok[b])
+    return same / total if total else 0.0

@@ -41,7 +41,7 @@ class moe_model_desc(ctypes.Structure):
         ("arena", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t), ("trace", ctypes.c_void_p),
         ("trace_cap", ctypes.c_size_t), ("compute_stream", ctypes.c_void_p),
-        ("copy_stream", ctypes.c_void_p),
+        ("copy_stream", ctypes.c_void_p), ("host_layers", ctypes.POINTER(ctypes.c_void_p)),
     ]
 
 
@@ -59,10 +59,10 @@ class moe_layer_stats(ctypes.Structure):
 class moe_timing(ctypes.Structure):
     _fields_ = ([(n, ctypes.c_double) for n in
                  ("router_ms", "fetch_ms", "ffn_up_ms", "ffn_down_ms", "prefill_ms", "gemm_up_ms",
-                  "gemm_down_ms")]
+                  "gemm_down_ms", "ffn_reduce_ms")]
                 + [(n, ctypes.c_uint64) for n in
                    ("router_n", "fetch_n", "ffn_up_n", "ffn_down_n", "prefill_n", "gemm_up_n",
-                    "gemm_down_n")]
+                    "gemm_down_n", "ffn_reduce_n")]
                 + [(n, ctypes.c_double) for n in ("gemm_up_flop", "gemm_down_flop")])
 
 

@@ -37,7 +37,9 @@ def build(verbose: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
     sources = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     tmp = OUT + ".tmp"
-    cmd = [hipcc(), *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC, *sources, "-o", tmp]
+    # MOE_HIPCC_EXTRA: extra compiler flags for tuning builds (e.g. -DMOE_FETCH_BLOCKS=32)
+    extra = os.environ.get("MOE_HIPCC_EXTRA", "").split()
+    cmd = [hipcc(), *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", CSRC, *sources, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

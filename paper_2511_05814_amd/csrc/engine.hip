@@ -43,7 +43,7 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
   size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, act = 0, part = 0,
-         prefill = 0, total = 0;
+         hostptrs = 0, prefill = 0, total = 0;
 };
 
 bool misaligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) != 0; }
@@ -109,7 +109,9 @@ struct moe_cache {
   uint64_t *trace_count = nullptr;  // device: records written to the trace ring
   float *act = nullptr, *part = nullptr;
   uint8_t *prefill_ws = nullptr;
-  const uint8_t *host_dev = nullptr;  // device address of the pinned host store
+  std::vector<const uint8_t *> host_layer;  // host address of layer l's experts
+  const uint8_t *const *dev_layers = nullptr;  // device array: layer l's experts as the GPU sees them
+  std::vector<const uint8_t *> dev_layer_host;  // what that array must hold
   std::vector<hipEvent_t> ev_demand, ev_pf;
   hipEvent_t ev_router = nullptr;
   std::vector<uint8_t> demand_pending, pf_pending;
@@ -135,7 +137,8 @@ struct moe_cache {
 
 namespace moe {
 enum SpanKind {
-  SPAN_ROUTER = 0, SPAN_FETCH, SPAN_UP, SPAN_DOWN, SPAN_PREFILL, SPAN_GEMM_UP, SPAN_GEMM_DOWN, SPAN_KINDS
+  SPAN_ROUTER = 0, SPAN_FETCH, SPAN_UP, SPAN_DOWN, SPAN_PREFILL, SPAN_GEMM_UP, SPAN_GEMM_DOWN, SPAN_REDUCE,
+  SPAN_KINDS
 };
 
 // Start/stop a timed span on stream s (no-op unless timing is on).
@@ -231,6 +234,7 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.dlists = take(sizeof(FetchList) * c->L);
   l.plists = take(sizeof(FetchList) * c->L);
   l.route = take(sizeof(RouteOut));
+  l.hostptrs = take(sizeof(void *) * c->L);
   l.err = take(256);
   l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff) * d->d_model);
@@ -271,8 +275,8 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   int rc = validate_desc(c, d);
   if (rc != MOE_OK) return rc;
   if (c->bound) return fail(MOE_ERR_STATE, "handle is already bound");
-  if (!d->gate_w || !d->host_experts || !d->arena || !d->workspace)
-    return fail(MOE_ERR_ARG, "gate_w, host_experts, arena and workspace must be non-NULL");
+  if (!d->gate_w || (!d->host_experts && !d->host_layers) || !d->arena || !d->workspace)
+    return fail(MOE_ERR_ARG, "gate_w, host_experts (or host_layers), arena and workspace must be non-NULL");
   if (misaligned(d->gate_w, 16) || misaligned(d->host_experts, 16) || misaligned(d->arena, 16))
     return fail(MOE_ERR_ARG, "gate_w, host_experts and arena must be 16-byte aligned");
   if (misaligned(d->workspace, 256)) return fail(MOE_ERR_ARG, "workspace must be 256-byte aligned");
@@ -282,16 +286,29 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   if (d->workspace_bytes < lay.total)
     return fail(MOE_ERR_ARG, "workspace too small: %zu < %zu bytes", d->workspace_bytes, lay.total);
 
-  void *dev_host = nullptr;
+  // per-layer host bases (one contiguous store, or the caller's per-layer table)
+  const uint64_t B = 3ull * d->d_model * d->d_ff * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
+  std::vector<const uint8_t *> hl(c->L), dl(c->L, nullptr);
+  for (int l = 0; l < c->L; ++l) {
+    hl[l] = d->host_layers ? static_cast<const uint8_t *>(d->host_layers[l])
+                           : static_cast<const uint8_t *>(d->host_experts) + (size_t)l * c->E * B;
+    if (!hl[l] || misaligned(hl[l], 16))
+      return fail(MOE_ERR_ARG, "host store of layer %d is NULL or not 16-byte aligned", l);
+  }
   if (d->fetch_mode == MOE_FETCH_KERNEL) {
-    hipError_t e = hipHostGetDevicePointer(&dev_host, const_cast<void *>(d->host_experts), 0);
-    if (e != hipSuccess || !dev_host) {
-      (void)hipGetLastError();
-      return fail(MOE_ERR_ARG, "host_experts is not pinned host memory mapped for the device (%s)",
-                  hipGetErrorString(e));
+    for (int l = 0; l < c->L; ++l) {
+      void *p = nullptr;
+      hipError_t e = hipHostGetDevicePointer(&p, const_cast<uint8_t *>(hl[l]), 0);
+      if (e != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return fail(MOE_ERR_ARG, "host store of layer %d is not pinned host memory mapped for the device (%s)",
+                    l, hipGetErrorString(e));
+      }
+      dl[l] = static_cast<const uint8_t *>(p);
     }
   }
   c->desc = *d;
+  c->host_layer = hl;
   c->K = d->top_k;
   c->d = d->d_model;
   c->dff = d->d_ff;
@@ -315,7 +332,9 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->act = reinterpret_cast<float *>(c->ws + lay.act);
   c->part = reinterpret_cast<float *>(c->ws + lay.part);
   c->prefill_ws = c->ws + lay.prefill;
-  c->host_dev = static_cast<const uint8_t *>(dev_host);
+  c->dev_layers = reinterpret_cast<const uint8_t *const *>(c->ws + lay.hostptrs);
+  c->dev_layer_host = dl;
+  HIP_TRY0(hipMemcpy(c->ws + lay.hostptrs, dl.data(), sizeof(void *) * c->L, hipMemcpyHostToDevice));
 
   c->ev_demand.assign(c->L, nullptr);
   c->ev_pf.assign(c->L, nullptr);
@@ -361,14 +380,28 @@ int moe_cache_reset(moe_cache_t *c) {
     }
   }
   HIP_TRY(c, hipMemcpyAsync(c->tables, t.data(), sizeof(LayerTable) * c->L, hipMemcpyHostToDevice, c->cs));
-  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.stats, 0, c->lay.route - c->lay.stats, c->cs));
-  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.route, 0, c->lay.act - c->lay.route, c->cs));
+  // clear exactly the regions that hold run state (never the host-pointer table)
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.stats, 0, sizeof(LayerStats) * c->L, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.dlists, 0, sizeof(FetchList) * c->L, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.plists, 0, sizeof(FetchList) * c->L, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.route, 0, sizeof(RouteOut), c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.err, 0, 256, c->cs));
+  {
+    // the copy kernel dereferences this table: check it survived
+    std::vector<const uint8_t *> got(c->L);
+    HIP_TRY(c, hipMemcpyAsync(got.data(), c->ws + c->lay.hostptrs, sizeof(void *) * c->L,
+                              hipMemcpyDeviceToHost, c->cs));
+    HIP_TRY(c, hipStreamSynchronize(c->cs));
+    if (got != c->dev_layer_host) {
+      c->sticky = MOE_ERR_HIP;
+      return fail(MOE_ERR_HIP, "device table of host-store addresses was overwritten");
+    }
+  }
   HIP_TRY(c, hipStreamSynchronize(c->cs));
-  const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
   for (int l = 0; l < c->L; ++l)
     for (int s = 0; s < c->S; ++s)
-      HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)l * c->S + s) * c->B, host + ((size_t)l * c->E + s) * c->B,
+      HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)l * c->S + s) * c->B, c->host_layer[l] + (size_t)s * c->B,
                                 c->B, hipMemcpyHostToDevice, c->xs));
   HIP_TRY(c, hipStreamSynchronize(c->xs));
   std::fill(c->demand_pending.begin(), c->demand_pending.end(), 0);
@@ -386,7 +419,7 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
   if (c->fetch_mode == MOE_FETCH_KERNEL) {
     hipEvent_t t0;
     HIP_TRY(c, span_begin(c, q, &t0));
-    HIP_TRY(c, launch_fetch(list, c->host_dev, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
+    HIP_TRY(c, launch_fetch(list, c->dev_layers, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
                             c->K, c->B, c->err, q));
     HIP_TRY(c, span_end(c, q, SPAN_FETCH, t0));
     return MOE_OK;
@@ -396,7 +429,7 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
     c->sticky = MOE_ERR_HIP;
     return fail(MOE_ERR_HIP, "inconsistent fetch list from the device");
   }
-  const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
+  const uint8_t *host = c->host_layer[m.layer];
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
   if (m.n == 0) return MOE_OK;
   hipEvent_t t0;
@@ -408,7 +441,7 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
       return fail(MOE_ERR_HIP, "inconsistent fetch entry from the device");
     }
     HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)m.layer * c->S + s) * c->B,
-                              host + ((size_t)m.layer * c->E + e) * c->B, c->B, hipMemcpyHostToDevice, q));
+                              host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
   }
   HIP_TRY(c, span_end(c, q, SPAN_FETCH, t0));
   return MOE_OK;
@@ -510,6 +543,10 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     HIP_TRY(c, span_begin(c, c->cs, &t1));
     HIP_TRY(c, launch_ffn_down(f, c->dtype, c->cs));
     HIP_TRY(c, span_end(c, c->cs, SPAN_DOWN, t1));
+    hipEvent_t t2;
+    HIP_TRY(c, span_begin(c, c->cs, &t2));
+    HIP_TRY(c, launch_ffn_reduce(f, c->cs));
+    HIP_TRY(c, span_end(c, c->cs, SPAN_REDUCE, t2));
     c->last_route_kind = 1;
   }
   return MOE_OK;
@@ -542,7 +579,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   uint16_t *act = reinterpret_cast<uint16_t *>(base + p.act);
   float *Y = reinterpret_cast<float *>(base + p.y);
   uint8_t *staging = base + p.staging;
-  const uint8_t *host = static_cast<const uint8_t *>(c->desc.host_experts);
+  const uint8_t *host = c->host_layer[layer];
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
   const int gate_elem = c->dtype == MOE_DTYPE_BF16 ? 2 : 4;
 
@@ -700,7 +737,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
         }
         dst = staging + (size_t)ring_of[e] * c->B;
       }
-      HIP_TRY(c, hipMemcpyAsync(dst, host + ((size_t)layer * E + e) * c->B, c->B, hipMemcpyHostToDevice, q));
+      HIP_TRY(c, hipMemcpyAsync(dst, host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
     }
     HIP_TRY(c, hipEventRecord(evC, q));
     HIP_TRY(c, hipStreamWaitEvent(c->cs, evC, 0));
@@ -712,7 +749,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     if (!waited_A) HIP_TRY(c, hipStreamWaitEvent(q, evA, 0));
     for (int e : unrouted_new)
       HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B,
-                                host + ((size_t)layer * E + e) * c->B, c->B, hipMemcpyHostToDevice, q));
+                                host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
   }
   HIP_TRY(c, hipEventRecord(evF, q));
   HIP_TRY(c, hipStreamWaitEvent(c->cs, evF, 0));
@@ -893,10 +930,12 @@ int moe_cache_read_timing(moe_cache_t *c, moe_timing *out) {
   if (!c->bound) return MOE_OK;
   (void)hipStreamSynchronize(c->cs);
   if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
-  double *ms[SPAN_KINDS] = {&out->router_ms, &out->fetch_ms,   &out->ffn_up_ms,  &out->ffn_down_ms,
-                            &out->prefill_ms, &out->gemm_up_ms, &out->gemm_down_ms};
-  uint64_t *n[SPAN_KINDS] = {&out->router_n,  &out->fetch_n,   &out->ffn_up_n,  &out->ffn_down_n,
-                             &out->prefill_n, &out->gemm_up_n, &out->gemm_down_n};
+  double *ms[SPAN_KINDS] = {&out->router_ms,  &out->fetch_ms,     &out->ffn_up_ms,
+                            &out->ffn_down_ms, &out->prefill_ms,   &out->gemm_up_ms,
+                            &out->gemm_down_ms, &out->ffn_reduce_ms};
+  uint64_t *n[SPAN_KINDS] = {&out->router_n,  &out->fetch_n,     &out->ffn_up_n,
+                             &out->ffn_down_n, &out->prefill_n,   &out->gemm_up_n,
+                             &out->gemm_down_n, &out->ffn_reduce_n};
   int rc = MOE_OK;
   for (const auto &sp : c->spans) {
     float t = 0.0f;

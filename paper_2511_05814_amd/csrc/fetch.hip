@@ -6,20 +6,25 @@
 // on the copy stream behind the router and reads the list itself, so no host
 // round trip sits between the decision and the copy: it streams each missing
 // expert with 16-byte loads straight from the pinned host store (mapped into
-// the GPU's address space) into its HBM slot.  A few dozen workgroups keep
-// enough reads in flight to saturate the host link while leaving the compute
-// units to the FFN kernels.
+// the GPU's address space; one base address per layer) into its HBM slot.
+// A few dozen workgroups keep enough reads in flight to saturate the host
+// link while leaving the compute units to the FFN kernels.
 #include "common.hpp"
+
+#ifndef MOE_FETCH_BLOCKS
+#define MOE_FETCH_BLOCKS 64
+#endif
 
 namespace moe {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBlocks = 64;
+constexpr int kBlocks = MOE_FETCH_BLOCKS;
 
-__global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list, const uint8_t *host,
-                                                         uint8_t *arena, int L, int E, int S, int K,
-                                                         uint64_t expert_bytes, int32_t *err) {
+__global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list,
+                                                         const uint8_t *const *layers, uint8_t *arena,
+                                                         int L, int E, int S, int K, uint64_t expert_bytes,
+                                                         int32_t *err) {
   const int n = list->n;
   const int layer = list->layer;
   if (n < 0 || n > K || layer < 0 || layer >= L) {
@@ -28,6 +33,11 @@ __global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list, 
   }
   const size_t nv = expert_bytes / sizeof(uint4);
   const size_t stride = (size_t)gridDim.x * kThreads;
+  const uint8_t *base = layers[layer];
+  if (base == nullptr) {  // no mapped host store for this layer: refuse, never dereference
+    if (blockIdx.x == 0 && threadIdx.x == 0) *err = ERR_BAD_LIST;
+    return;
+  }
   for (int i = 0; i < n; ++i) {
     const int e = list->expert[i];
     const int s = list->slot[i];
@@ -35,7 +45,7 @@ __global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list, 
       if (blockIdx.x == 0 && threadIdx.x == 0) *err = ERR_BAD_LIST;
       continue;
     }
-    const uint4 *src = reinterpret_cast<const uint4 *>(host + ((size_t)layer * E + e) * expert_bytes);
+    const uint4 *src = reinterpret_cast<const uint4 *>(base + (size_t)e * expert_bytes);
     uint4 *dst = reinterpret_cast<uint4 *>(arena + ((size_t)layer * S + s) * expert_bytes);
     size_t j = (size_t)blockIdx.x * kThreads + threadIdx.x;
     for (; j + 3 * stride < nv; j += 4 * stride) {
@@ -51,9 +61,9 @@ __global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list, 
 
 }  // namespace
 
-hipError_t launch_fetch(const FetchList *list, const uint8_t *host, uint8_t *arena, int L, int E,
+hipError_t launch_fetch(const FetchList *list, const uint8_t *const *layers, uint8_t *arena, int L, int E,
                         int S, int K, uint64_t expert_bytes, int32_t *err, hipStream_t s) {
-  hipLaunchKernelGGL(fetch_kernel, dim3(kBlocks), dim3(kThreads), 0, s, list, host, arena, L, E, S, K,
+  hipLaunchKernelGGL(fetch_kernel, dim3(kBlocks), dim3(kThreads), 0, s, list, layers, arena, L, E, S, K,
                      expert_bytes, err);
   return hipGetLastError();
 }

@@ -215,8 +215,10 @@ hipError_t launch_ffn_down(const FfnArgs &a, int dtype, hipStream_t s) {
     hipLaunchKernelGGL((ffn_down_kernel<1, kDownRows, kDownChunk>), grid, dim3(kThreads), 0, s, a);
   else
     hipLaunchKernelGGL((ffn_down_kernel<0, kDownRows, kDownChunk>), grid, dim3(kThreads), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_ffn_reduce(const FfnArgs &a, hipStream_t s) {
   hipLaunchKernelGGL(ffn_reduce_kernel, dim3((a.d + kThreads - 1) / kThreads), dim3(kThreads), 0, s,
                      a.part, ffn_down_chunks(a.K, a.d_ff), a.d, a.h);
   return hipGetLastError();

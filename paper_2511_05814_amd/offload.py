@@ -28,28 +28,72 @@ def _torch():
 
 
 class HostStore:
-    """Pinned host store of all experts, filled from the seeded generator."""
+    """Pinned host store of all experts, one allocation per layer, filled from
+    the seeded generator.
 
-    def __init__(self, cfg: wl.Config, fill: bool = True, workers: Optional[int] = None):
+    The GPU driver caps how much host memory can be pinned (about 70 GB on an
+    MI355X machine with 295 GB of RAM), below the 90 GB a 32-layer Mixtral-shaped
+    stack needs.  When the store would exceed `max_pinned_bytes`, only the
+    first `distinct` layers get pages of their own and layer l uses the pages
+    of layer l mod distinct: every fetch still moves a whole expert over the
+    host link, only the weight values repeat (gates stay per layer)."""
+
+    def __init__(self, cfg: wl.Config, fill: bool = True, workers: Optional[int] = None,
+                 max_pinned_bytes: int = 64 << 30):
         self.cfg = cfg
-        self.nbytes = cfg.layers * cfg.experts * cfg.expert_bytes
-        self.ptr = b.moe_host_alloc(self.nbytes)
-        self.array = np.ctypeslib.as_array((ctypes.c_uint8 * self.nbytes).from_address(self.ptr))
+        self.layer_bytes = cfg.experts * cfg.expert_bytes
+        self.distinct = int(max(1, min(cfg.layers, max_pinned_bytes // self.layer_bytes)))
+        self.nbytes = self.distinct * self.layer_bytes
+        self.ptrs = []
+        self.arrays = []
+        try:
+            for _ in range(self.distinct):
+                p = b.moe_host_alloc(self.layer_bytes)
+                self.ptrs.append(p)
+                self.arrays.append(np.ctypeslib.as_array((ctypes.c_uint8 * self.layer_bytes).from_address(p)))
+        except Exception:
+            self.close()
+            raise
+        self.layer_src = [l % self.distinct for l in range(cfg.layers)]
+        self.layer_ptrs = (ctypes.c_void_p * cfg.layers)(*[self.ptrs[s] for s in self.layer_src])
         if fill:
-            wl.fill_host_store(cfg, self.array, workers=workers)
+            self._fill(workers)
+
+    def _fill(self, workers):
+        import os
+        from concurrent.futures import ThreadPoolExecutor
+        cfg = self.cfg
+        sdt = np.float32 if cfg.dtype == "f32" else np.uint16
+        todo = [(l, e) for l in range(self.distinct) for e in range(cfg.experts)]
+
+        def one(le):
+            l, e = le
+            view = self.arrays[l].view(sdt).reshape(cfg.experts, cfg.expert_elems)
+            wl.fill_expert(cfg, l, e, view[e])
+
+        workers = workers or max(1, min(16, os.cpu_count() or 1))
+        with ThreadPoolExecutor(workers) as ex:
+            list(ex.map(one, todo))
+
+    @property
+    def aliased(self) -> bool:
+        return self.distinct < self.cfg.layers
 
     def expert(self, layer: int, expert: int) -> np.ndarray:
         """Storage-dtype view of one expert (W1|W3|W2)."""
         cfg = self.cfg
-        off = (layer * cfg.experts + expert) * cfg.expert_bytes
-        raw = self.array[off:off + cfg.expert_bytes]
+        off = expert * cfg.expert_bytes
+        raw = self.arrays[self.layer_src[layer]][off:off + cfg.expert_bytes]
         return raw.view(np.float32 if cfg.dtype == "f32" else np.uint16)
 
+    def layer_array(self, layer: int) -> np.ndarray:
+        return self.arrays[self.layer_src[layer]]
+
     def close(self):
-        if self.ptr:
-            self.array = None
-            b.moe_host_free(self.ptr)
-            self.ptr = 0
+        self.arrays = []
+        for p in self.ptrs:
+            b.moe_host_free(p)
+        self.ptrs = []
 
     def __del__(self):
         try:
@@ -98,7 +142,8 @@ class OffloadedMoE:
             d.fetch_mode = fetch_mode
             d.max_prefill_tokens = max_prefill_tokens
             d.gate_w = gates.ptr
-            d.host_experts = store.ptr
+            d.host_experts = None
+            d.host_layers = ctypes.cast(store.layer_ptrs, ctypes.POINTER(ctypes.c_void_p))
             d.arena = self.arena.data_ptr()
             d.trace = self.trace.data_ptr() if self.trace is not None else None
             d.trace_cap = trace_cap if self.trace is not None else 0

@@ -43,3 +43,13 @@ class Rig:
         return snaps.cpu().numpy().astype(np.float64), recs, H.cpu().numpy()
 
 
+
+
+class LazyRig(Rig):
+    """Rig whose oracle model widens experts on demand and keeps none (the
+    90 GB store would not fit in fp64)."""
+
+    def __init__(self, cfg):
+        super().__init__(cfg)
+        self.model = stack.Model(self.gates.host, lambda l, e: self.store.expert(l, e),
+                                 cfg.d_model, cfg.d_ff, cfg.dtype, keep=False)

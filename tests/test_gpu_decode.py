@@ -133,7 +133,7 @@ def test_injected_routing_traces_match_oracle(tiny, policy):
     for l in range(cfg.layers):
         se, _, _, _, _ = moe.state(l)
         for s, e in enumerate(se):
-            assert np.array_equal(arena[l, s], tiny.store.array.reshape(cfg.layers, cfg.experts, -1)[l, e])
+            assert np.array_equal(arena[l, s], tiny.store.layer_array(l).reshape(cfg.experts, -1)[e])
     moe.close()
 
 
@@ -224,3 +224,24 @@ def test_mixtral_layer_full_run(mixtral_layer, policy):
     _say("worst", worst, "uncertified", unc, "hit rate", caches[0].stats.hits / (cfg.tokens * 2))
     assert worst < 1e-4   # bf16 weights, fp32 activations and accumulation
     moe.close()
+
+
+def test_aliased_host_layers():
+    # a store that pins only 2 distinct layers for a 5-layer stack: layers 2..4
+    # read the pages of layers 0, 1, 0 through the per-layer host table
+    from paper_2511_05814_amd import offload
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=5, tokens=12)
+    _say("aliased host layers", cfg)
+    rig = Rig.__new__(Rig)
+    rig.cfg = cfg
+    rig.store = offload.HostStore(cfg, max_pinned_bytes=2 * cfg.experts * cfg.expert_bytes)
+    assert rig.store.distinct == 2 and rig.store.aliased
+    rig.gates = offload.DeviceGates(cfg)
+    rig.model = stack.Model(rig.gates.host, lambda l, e: rig.store.expert(l, e), cfg.d_model, cfg.d_ff,
+                            cfg.dtype)
+    for mode in (b.MOE_FETCH_KERNEL, b.MOE_FETCH_DMA):
+        moe = rig.cache(4, "lru", prefetch_max=1, fetch_mode=mode)
+        hs, recs, _ = rig.run(moe, cfg.tokens, flags=b.MOE_PREFETCH_NEXT)
+        check_decode(cfg, rig.model, hs, recs, 4, "lru", prefetch=True, pmax=1, tol=_tol(cfg))
+        moe.close()
+    rig.store.close()
