@@ -106,6 +106,7 @@ def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0):
     tim = None
     stats = None
     recs = None
+    prefill_bytes = 0
     b.moe_cache_set_timing(moe.handle, bool(timing))
     for _ in range(n):
         moe.reset()
@@ -119,6 +120,7 @@ def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0):
             moe.sync()
             torch.cuda.synchronize()
             pre += time.perf_counter() - t0
+            prefill_bytes += sum(s["bytes_fetched"] for s in moe.stats())
         t0 = time.perf_counter()
         moe.decode(H[prefill_tokens:], flags=flags)
         moe.sync()
@@ -131,7 +133,7 @@ def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0):
         stats = st if stats is None else [{k: a[k] + c[k] for k in a} for a, c in zip(stats, st)]
         recs, _ = moe.trace_records()
     b.moe_cache_set_timing(moe.handle, False)
-    return dec, pre, tim, stats, recs
+    return dec, pre, tim, stats, recs, prefill_bytes
 
 
 def cpu_baseline(cfg, store, gates_host, h0, tokens, slots, policy):
@@ -160,7 +162,8 @@ def summarize(cfg, r):
         "tokens_per_s": round(r["steps"] * cfg.tokens / r["dec"], 3),
         "hit_rate": round(analysis.hit_rate(acc), 4),
         "cache_precision_recall": [round(v, 4) for v in analysis.cache_precision_recall(acc, r["slots"])],
-        "bytes_fetched_per_step": sum(s["bytes_fetched"] for s in r["stats"]) // r["steps"],
+        "decode_bytes_fetched_per_step":
+            (sum(s["bytes_fetched"] for s in r["stats"]) - r["prefill_bytes"]) // r["steps"],
     }
     if r["flags"]:
         p, rc = analysis.guess_precision_recall(acc)
@@ -233,8 +236,10 @@ def main():
         steps = args.steps if i == 0 else 1
         if i == 0 and args.warmup:
             run_steps(torch, b, moe, H0, H, args.warmup, False, flags, cfg.prefill_tokens)
-        dec, pre, tim, st, recs = run_steps(torch, b, moe, H0, H, steps, True, flags, cfg.prefill_tokens)
+        dec, pre, tim, st, recs, pbytes = run_steps(torch, b, moe, H0, H, steps, True, flags,
+                                                    cfg.prefill_tokens)
         results.append(dict(policy=policy, slots=slots, flags=flags, steps=steps, dec=dec, pre=pre,
+                            prefill_bytes=pbytes,
                             timing=tim, stats=st, recs=recs))
         log(policy, slots, "prefetch" if spec else "", f"{steps * cfg.tokens / dec:.2f} tok/s")
         moe.close()
@@ -250,7 +255,7 @@ def main():
     down_ms = tim["ffn_down_ms"] / tim["ffn_down_n"]
     up_gbps = up_bytes / (up_ms * 1e-3) / 1e9
     down_gbps = down_bytes / (down_ms * 1e-3) / 1e9
-    fetched = sum(s["bytes_fetched"] for s in head["stats"])
+    fetched = sum(s["bytes_fetched"] for s in head["stats"]) - head["prefill_bytes"]  # decode only
     fetch_gbps = fetched / (tim["fetch_ms"] * 1e-3) / 1e9 if tim["fetch_ms"] > 0 else None
     tokens_per_s = head["steps"] * cfg.tokens / head["dec"]
     traffic = pmc_traffic() if args.workload == "mixtral-layer" else None
@@ -306,7 +311,7 @@ def main():
             "unit": "GB/s",
             "frac": round(fetch_gbps / link, 4) if fetch_gbps else None,
             "peak_is": "best measured 1 GiB pinned H2D copy",
-            "bytes_fetched_per_step": fetched // head["steps"],
+            "decode_bytes_fetched_per_step": fetched // head["steps"],
         },
         "router_us": round(1e3 * tim["router_ms"] / tim["router_n"], 2),
     }
