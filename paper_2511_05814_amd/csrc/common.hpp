@@ -144,8 +144,8 @@ hipError_t launch_fetch(const FetchList *list, const uint8_t *const *layers, uin
                         int S, int K, uint64_t expert_bytes, int32_t *err, hipStream_t s);
 hipError_t launch_ffn_up(const FfnArgs &a, int dtype, hipStream_t s);
 hipError_t launch_ffn_down(const FfnArgs &a, int dtype, hipStream_t s);
-hipError_t launch_ffn_reduce(const FfnArgs &a, hipStream_t s);
-int ffn_down_chunks(int K, int d_ff);
+hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, hipStream_t s);
+int ffn_down_chunks(int K, int d_ff, int dtype);
 hipError_t launch_prefill_gate(const PrefillArgs &a, hipStream_t s);
 hipError_t launch_prefill_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,

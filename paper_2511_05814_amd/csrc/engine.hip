@@ -237,7 +237,7 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.hostptrs = take(sizeof(void *) * c->L);
   l.err = take(256);
   l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
-  l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff) * d->d_model);
+  l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff, d->dtype) * d->d_model);
   const uint64_t B = 3ull * d->d_model * d->d_ff * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
   l.prefill = take(prefill_layout(d->top_k, d->d_model, d->d_ff, c->E, c->S, d->max_prefill_tokens, B).total);
   l.total = off;
@@ -545,7 +545,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     HIP_TRY(c, span_end(c, c->cs, SPAN_DOWN, t1));
     hipEvent_t t2;
     HIP_TRY(c, span_begin(c, c->cs, &t2));
-    HIP_TRY(c, launch_ffn_reduce(f, c->cs));
+    HIP_TRY(c, launch_ffn_reduce(f, c->dtype, c->cs));
     HIP_TRY(c, span_end(c, c->cs, SPAN_REDUCE, t2));
     c->last_route_kind = 1;
   }
