@@ -3,6 +3,7 @@
 // workspace; the host engine carves the workspace into these regions.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -138,23 +139,33 @@ struct PlanArgs {
   int T, K, E, S, layer, policy;
 };
 
+// Where a kernel goes: its stream and, when kernel timing is on, two events
+// the dispatch itself stamps at the kernel's start and end.
+struct Launch {
+  hipStream_t s = nullptr;
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+#define MOE_LAUNCH(kernel, grid, block, shmem, L, ...) \
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, (L).s, (L).start, (L).stop, 0, __VA_ARGS__)
+
 // launchers (one per translation unit that owns the kernel)
-hipError_t launch_router(const RouterArgs &a, hipStream_t s);
+hipError_t launch_router(const RouterArgs &a, const Launch &l);
 hipError_t launch_fetch(const FetchList *list, const uint8_t *const *layers, uint8_t *arena, int L, int E,
-                        int S, int K, uint64_t expert_bytes, int32_t *err, hipStream_t s);
-hipError_t launch_ffn_up(const FfnArgs &a, int dtype, hipStream_t s);
-hipError_t launch_ffn_down(const FfnArgs &a, int dtype, hipStream_t s);
-hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, hipStream_t s);
+                        int S, int K, uint64_t expert_bytes, int32_t *err, const Launch &l);
+hipError_t launch_ffn_up(const FfnArgs &a, int dtype, const Launch &l);
+hipError_t launch_ffn_down(const FfnArgs &a, int dtype, const Launch &l);
+hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, const Launch &l);
 int ffn_down_chunks(int K, int d_ff, int dtype);
-hipError_t launch_prefill_gate(const PrefillArgs &a, hipStream_t s);
-hipError_t launch_prefill_plan(const PlanArgs &a, hipStream_t s);
+hipError_t launch_prefill_gate(const PrefillArgs &a, const Launch &l);
+hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l);
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, hipStream_t s);
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l);
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, hipStream_t s);
+                               float *Y, int d, int d_ff, const Launch &l);
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
-                                    int d, int K, hipStream_t s);
-int prefill_tile_rows();
+                                    int d, int K, const Launch &l);
+int prefill_tile_rows();  // GEMM output tile: rows (tokens) ...
+int prefill_tile_cols();  // ... and columns
 
 // ---------------------------------------------------------------------------
 // device helpers

@@ -170,6 +170,28 @@ hipError_t span_end(moe_cache *c, hipStream_t s, int kind, hipEvent_t begin, dou
   c->spans.push_back({kind, begin, e, flop});
   return hipEventRecord(e, s);
 }
+
+// A kernel launch on stream s; with timing on it carries two pooled events
+// that the dispatch itself stamps at the kernel's start and end.
+hipError_t kernel_span(moe_cache *c, hipStream_t s, Launch *l) {
+  l->s = s;
+  l->start = l->stop = nullptr;
+  if (!c->timing) return hipSuccess;
+  for (hipEvent_t *e : {&l->start, &l->stop}) {
+    if (!c->ev_pool.empty()) {
+      *e = c->ev_pool.back();
+      c->ev_pool.pop_back();
+    } else {
+      hipError_t r = hipEventCreate(e);
+      if (r != hipSuccess) return r;
+    }
+  }
+  return hipSuccess;
+}
+
+void kernel_span_done(moe_cache *c, int kind, const Launch &l, double flop = 0.0) {
+  if (l.start) c->spans.push_back({kind, l.start, l.stop, flop});
+}
 }  // namespace moe
 
 namespace moe {
@@ -417,11 +439,11 @@ int moe_cache_reset(moe_cache_t *c) {
 // Issue the copies for one fetch list that the router just wrote.
 static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_t q) {
   if (c->fetch_mode == MOE_FETCH_KERNEL) {
-    hipEvent_t t0;
-    HIP_TRY(c, span_begin(c, q, &t0));
+    Launch l;
+    HIP_TRY(c, kernel_span(c, q, &l));
     HIP_TRY(c, launch_fetch(list, c->dev_layers, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
-                            c->K, c->B, c->err, q));
-    HIP_TRY(c, span_end(c, q, SPAN_FETCH, t0));
+                            c->K, c->B, c->err, l));
+    kernel_span_done(c, SPAN_FETCH, l);
     return MOE_OK;
   }
   const FetchList &m = c->mirror[mirror_idx];
@@ -480,10 +502,10 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.demand = demand;
   a.spec_layer = spec_layer;
   a.pmax = pmax;
-  hipEvent_t t0;
-  HIP_TRY(c, span_begin(c, c->cs, &t0));
-  HIP_TRY(c, launch_router(a, c->cs));
-  HIP_TRY(c, span_end(c, c->cs, SPAN_ROUTER, t0));
+  Launch lr;
+  HIP_TRY(c, kernel_span(c, c->cs, &lr));
+  HIP_TRY(c, launch_router(a, lr));
+  kernel_span_done(c, SPAN_ROUTER, lr);
 
   hipStream_t q = c->xs;
   if (c->fetch_mode == MOE_FETCH_KERNEL) {
@@ -536,17 +558,16 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     f.d = c->d;
     f.d_ff = c->dff;
     f.phase = 0;
-    hipEvent_t t0, t1;
-    HIP_TRY(c, span_begin(c, c->cs, &t0));
-    HIP_TRY(c, launch_ffn_up(f, c->dtype, c->cs));
-    HIP_TRY(c, span_end(c, c->cs, SPAN_UP, t0));
-    HIP_TRY(c, span_begin(c, c->cs, &t1));
-    HIP_TRY(c, launch_ffn_down(f, c->dtype, c->cs));
-    HIP_TRY(c, span_end(c, c->cs, SPAN_DOWN, t1));
-    hipEvent_t t2;
-    HIP_TRY(c, span_begin(c, c->cs, &t2));
-    HIP_TRY(c, launch_ffn_reduce(f, c->dtype, c->cs));
-    HIP_TRY(c, span_end(c, c->cs, SPAN_REDUCE, t2));
+    Launch lu, ld, lx;
+    HIP_TRY(c, kernel_span(c, c->cs, &lu));
+    HIP_TRY(c, launch_ffn_up(f, c->dtype, lu));
+    kernel_span_done(c, SPAN_UP, lu);
+    HIP_TRY(c, kernel_span(c, c->cs, &ld));
+    HIP_TRY(c, launch_ffn_down(f, c->dtype, ld));
+    kernel_span_done(c, SPAN_DOWN, ld);
+    HIP_TRY(c, kernel_span(c, c->cs, &lx));
+    HIP_TRY(c, launch_ffn_reduce(f, c->dtype, lx));
+    kernel_span_done(c, SPAN_REDUCE, lx);
     c->last_route_kind = 1;
   }
   return MOE_OK;
@@ -597,7 +618,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   ga.E = c->E;
   ga.K = c->K;
   ga.dtype = c->dtype;
-  HIP_TRY(c, launch_prefill_gate(ga, c->cs));
+  HIP_TRY(c, launch_prefill_gate(ga, Launch{c->cs}));
   PlanArgs pa{};
   pa.ids = ids;
   pa.perm_tok = perm;
@@ -616,7 +637,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   pa.S = c->S;
   pa.layer = layer;
   pa.policy = c->policy;
-  HIP_TRY(c, launch_prefill_plan(pa, c->cs));
+  HIP_TRY(c, launch_prefill_plan(pa, Launch{c->cs}));
   HIP_TRY(c, hipMemcpyAsync(c->h_plan, plan, sizeof(PrefillPlan) * c->E, hipMemcpyDeviceToHost, c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   {
@@ -673,13 +694,13 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       }
     }
   }
-  const int rows = prefill_tile_rows();
+  const int rows = prefill_tile_rows(), cols = prefill_tile_cols();
   int nt = 0;
   auto add_tiles = [&](const std::vector<int> &group, int ncols, int &first, int &count) {
     first = nt;
     for (int e : group)
       for (int m0 = 0; m0 < pl[e].n; m0 += rows)
-        for (int n0 = 0; n0 < ncols; n0 += rows) ht[nt++] = GemmTile{e, m0, n0, 0};
+        for (int n0 = 0; n0 < ncols; n0 += cols) ht[nt++] = GemmTile{e, m0, n0, 0};
     count = nt - first;
   };
   const size_t ngroups = batches.size() + 1;
@@ -702,13 +723,14 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
 
   const double up_flop_per_row = 4.0 * c->d * c->dff, down_flop_per_row = 2.0 * c->d * c->dff;
   auto run_group = [&](size_t gi) -> int {
-    hipEvent_t t0, t1;
-    HIP_TRY(c, span_begin(c, c->cs, &t0));
-    HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, c->cs));
-    HIP_TRY(c, span_end(c, c->cs, SPAN_GEMM_UP, t0, group_rows[gi] * up_flop_per_row));
-    HIP_TRY(c, span_begin(c, c->cs, &t1));
-    HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, c->cs));
-    HIP_TRY(c, span_end(c, c->cs, SPAN_GEMM_DOWN, t1, group_rows[gi] * down_flop_per_row));
+    if (up_n[gi] <= 0) return MOE_OK;
+    Launch lu, ld;
+    HIP_TRY(c, kernel_span(c, c->cs, &lu));
+    HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, lu));
+    kernel_span_done(c, SPAN_GEMM_UP, lu, group_rows[gi] * up_flop_per_row);
+    HIP_TRY(c, kernel_span(c, c->cs, &ld));
+    HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, ld));
+    kernel_span_done(c, SPAN_GEMM_DOWN, ld, group_rows[gi] * down_flop_per_row);
     return MOE_OK;
   };
   hipEvent_t evA = c->pf_ev[0], evF = c->pf_ev[1];
@@ -753,7 +775,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   }
   HIP_TRY(c, hipEventRecord(evF, q));
   HIP_TRY(c, hipStreamWaitEvent(c->cs, evF, 0));
-  HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, c->cs));
+  HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, Launch{c->cs}));
   HIP_TRY(c, span_end(c, c->cs, SPAN_PREFILL, tp));
   // later decode calls on this layer need no extra wait: the compute stream
   // has already waited for every copy issued here

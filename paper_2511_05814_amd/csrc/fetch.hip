@@ -62,9 +62,9 @@ __global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list,
 }  // namespace
 
 hipError_t launch_fetch(const FetchList *list, const uint8_t *const *layers, uint8_t *arena, int L, int E,
-                        int S, int K, uint64_t expert_bytes, int32_t *err, hipStream_t s) {
-  hipLaunchKernelGGL(fetch_kernel, dim3(kBlocks), dim3(kThreads), 0, s, list, layers, arena, L, E, S, K,
-                     expert_bytes, err);
+                        int S, int K, uint64_t expert_bytes, int32_t *err, const Launch &l) {
+  MOE_LAUNCH(fetch_kernel, dim3(kBlocks), dim3(kThreads), 0, l, list, layers, arena, L, E, S, K, expert_bytes,
+             err);
   return hipGetLastError();
 }
 

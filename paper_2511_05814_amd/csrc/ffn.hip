@@ -271,35 +271,34 @@ DownShape down_shape(int d_ff, int dtype) {
 }
 
 template <int DT>
-hipError_t launch_up_t(const FfnArgs &a, hipStream_t s) {
+hipError_t launch_up_t(const FfnArgs &a, const Launch &l) {
   constexpr int COLS = kWave * Elem<DT>::kVec;
   const int steps = (a.d + COLS - 1) / COLS;
   const dim3 grid(a.K * ((a.d_ff + kWavesPerBlock * kUpRows - 1) / (kWavesPerBlock * kUpRows)));
   if (steps <= 1)
-    hipLaunchKernelGGL((ffn_up_kernel<DT, 1, kUpRows>), grid, dim3(kThreads), 0, s, a);
+    MOE_LAUNCH((ffn_up_kernel<DT, 1, kUpRows>), grid, dim3(kThreads), 0, l, a);
   else if (steps <= 2)
-    hipLaunchKernelGGL((ffn_up_kernel<DT, 2, kUpRows>), grid, dim3(kThreads), 0, s, a);
+    MOE_LAUNCH((ffn_up_kernel<DT, 2, kUpRows>), grid, dim3(kThreads), 0, l, a);
   else if (steps <= 4)
-    hipLaunchKernelGGL((ffn_up_kernel<DT, 4, kUpRows>), grid, dim3(kThreads), 0, s, a);
+    MOE_LAUNCH((ffn_up_kernel<DT, 4, kUpRows>), grid, dim3(kThreads), 0, l, a);
   else if (steps <= 8)
-    hipLaunchKernelGGL((ffn_up_kernel<DT, 8, kUpRows>), grid, dim3(kThreads), 0, s, a);
+    MOE_LAUNCH((ffn_up_kernel<DT, 8, kUpRows>), grid, dim3(kThreads), 0, l, a);
   else {
     const dim3 g2(a.K * ((a.d_ff + kWavesPerBlock * kUpLdsRows - 1) / (kWavesPerBlock * kUpLdsRows)));
-    hipLaunchKernelGGL((ffn_up_lds_kernel<DT, kUpLdsRows>), g2, dim3(kThreads), (size_t)a.d * sizeof(float), s,
-                       a);
+    MOE_LAUNCH((ffn_up_lds_kernel<DT, kUpLdsRows>), g2, dim3(kThreads), (uint32_t)(a.d * sizeof(float)), l, a);
   }
   return hipGetLastError();
 }
 
 template <int DT>
-hipError_t launch_down_t(const FfnArgs &a, hipStream_t s) {
+hipError_t launch_down_t(const FfnArgs &a, const Launch &l) {
   const DownShape sh = down_shape(a.d_ff, DT);
   const int rows = kWavesPerBlock * sh.rows;
   const dim3 grid(((a.d + rows - 1) / rows) * ffn_down_chunks(a.K, a.d_ff, DT));
   if (sh.steps == 4)
-    hipLaunchKernelGGL((ffn_down_kernel<DT, 4, 2>), grid, dim3(kThreads), 0, s, a);
+    MOE_LAUNCH((ffn_down_kernel<DT, 4, 2>), grid, dim3(kThreads), 0, l, a);
   else
-    hipLaunchKernelGGL((ffn_down_kernel<DT, 2, 4>), grid, dim3(kThreads), 0, s, a);
+    MOE_LAUNCH((ffn_down_kernel<DT, 2, 4>), grid, dim3(kThreads), 0, l, a);
   return hipGetLastError();
 }
 
@@ -310,17 +309,17 @@ int ffn_down_chunks(int K, int d_ff, int dtype) {
   return K * ((d_ff + ch - 1) / ch);
 }
 
-hipError_t launch_ffn_up(const FfnArgs &a, int dtype, hipStream_t s) {
-  return dtype == 1 ? launch_up_t<1>(a, s) : launch_up_t<0>(a, s);
+hipError_t launch_ffn_up(const FfnArgs &a, int dtype, const Launch &l) {
+  return dtype == 1 ? launch_up_t<1>(a, l) : launch_up_t<0>(a, l);
 }
 
-hipError_t launch_ffn_down(const FfnArgs &a, int dtype, hipStream_t s) {
-  return dtype == 1 ? launch_down_t<1>(a, s) : launch_down_t<0>(a, s);
+hipError_t launch_ffn_down(const FfnArgs &a, int dtype, const Launch &l) {
+  return dtype == 1 ? launch_down_t<1>(a, l) : launch_down_t<0>(a, l);
 }
 
-hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, hipStream_t s) {
-  hipLaunchKernelGGL(ffn_reduce_kernel, dim3((a.d + kThreads - 1) / kThreads), dim3(kThreads), 0, s, a.part,
-                     ffn_down_chunks(a.K, a.d_ff, dtype), a.d, a.h);
+hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, const Launch &l) {
+  MOE_LAUNCH(ffn_reduce_kernel, dim3((a.d + kThreads - 1) / kThreads), dim3(kThreads), 0, l,
+             (const float *)a.part, ffn_down_chunks(a.K, a.d_ff, dtype), a.d, a.h);
   return hipGetLastError();
 }
 

@@ -445,6 +445,122 @@ __global__ __launch_bounds__(256) void prefill_down_kernel(const GemmTile *tiles
 }
 
 // ---------------------------------------------------------------------------
+// Grouped GEMM, 128 x 128 output tile per workgroup (four waves of 64 x 64,
+// 4 x 4 blocks of v_mfma_f32_16x16x32_bf16 each).  The next 32-deep K slice
+// is loaded from global memory into registers while the current one is
+// multiplied out of LDS; LDS is double-buffered so one barrier per step
+// suffices.  Every output still accumulates its K slices in ascending order
+// with the same instruction as the 64 x 64 kernels, so results are identical.
+constexpr int kBM = 128, kBN = 128;
+
+struct TileRows {
+  const uint16_t *p[2];  // this thread's two rows of the 128-row tile (or nullptr)
+};
+
+template <bool UP>
+__global__ __launch_bounds__(256) void prefill_gemm_v2_kernel(const GemmTile *tiles, const GemmJob *jobs,
+                                                              const uint16_t *a_src, const int32_t *perm_tok,
+                                                              void *out, int d, int d_ff) {
+  constexpr int NB = UP ? 2 : 1;  // B matrices: W1 and W3, or W2
+  __shared__ uint16_t As[2][kBM][kLdsK];
+  __shared__ uint16_t Bs[2][NB][kBN][kLdsK];
+  const GemmTile t = tiles[blockIdx.x];
+  const GemmJob j = jobs[t.job];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int wm = wave / 2, wn = wave % 2;
+  const int K = UP ? d : d_ff;   // reduction length
+  const int N = UP ? d_ff : d;   // output columns
+  const int ldo = N;
+  // staging: thread -> rows (tid / 4) and (tid / 4 + 64), 16-byte quarter tid % 4
+  const int r0 = tid / 4, q = tid % 4;
+  TileRows ar, br[NB];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int m = t.m0 + r0 + 64 * h;
+    if (m < j.nrows)
+      ar.p[h] = UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff;
+    else
+      ar.p[h] = nullptr;
+    const int n = t.n0 + r0 + 64 * h;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const uint16_t *w = j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d);
+      br[b].p[h] = n < N ? w + (size_t)n * K : nullptr;
+    }
+  }
+  uint4 ra[2], rb[NB][2];
+  auto gload = [&](int k0) {
+    const int k = k0 + q * 8;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      ra[h] = (ar.p[h] && k < K) ? *reinterpret_cast<const uint4 *>(ar.p[h] + k) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        rb[b][h] = (br[b].p[h] && k < K) ? *reinterpret_cast<const uint4 *>(br[b].p[h] + k)
+                                         : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][q * 8]) = ra[h];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][q * 8]) = rb[b][h];
+    }
+  };
+  floatx4 c[NB][4][4];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < 4; ++y)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) c[b][x][y][i] = 0.0f;
+
+  const int nk = (K + kKStep - 1) / kKStep;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int s = 0; s < nk; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nk) gload((s + 1) * kKStep);
+    bf16x8 af[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) af[x] = lds_frag(As[buf], wm * 64 + x * 16 + lane % 16, lane);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      bf16x8 bf[4];
+#pragma unroll
+      for (int y = 0; y < 4; ++y) bf[y] = lds_frag(Bs[buf][b], wn * 64 + y * 16 + lane % 16, lane);
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y)
+          c[b][x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
+    }
+    if (s + 1 < nk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = t.m0 + wm * 64 + x * 16 + (lane / 16) * 4 + i;
+        const int n = t.n0 + wn * 64 + y * 16 + lane % 16;
+        if (m < j.nrows && n < N) {
+          const size_t o = (size_t)(j.row0 + m) * ldo + n;
+          if (UP)
+            static_cast<uint16_t *>(out)[o] = f32_to_bf16_rne(silu(c[0][x][y][i]) * c[NB - 1][x][y][i]);
+          else
+            static_cast<float *>(out)[o] = c[0][x][y][i];
+        }
+      }
+}
+
+// ---------------------------------------------------------------------------
 // 4. h_t += sum_r g_tr Y[pos(t, r)], ranks in order
 __global__ __launch_bounds__(256) void prefill_unpermute_kernel(float *H, const float *Y, const float *g,
                                                                 const int32_t *pos_of, int T, int d, int K) {
@@ -461,36 +577,39 @@ __global__ __launch_bounds__(256) void prefill_unpermute_kernel(float *H, const 
 
 // ---------------------------------------------------------------------------
 // launchers used by the host engine
-hipError_t launch_prefill_gate(const PrefillArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(prefill_gate_kernel, dim3((a.T + kGateTok - 1) / kGateTok), dim3(256), 0, s, a);
+hipError_t launch_prefill_gate(const PrefillArgs &a, const Launch &l) {
+  MOE_LAUNCH(prefill_gate_kernel, dim3((a.T + kGateTok - 1) / kGateTok), dim3(256), 0, l, a);
   return hipGetLastError();
 }
 
-hipError_t launch_prefill_plan(const PlanArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(prefill_plan_kernel, dim3(1), dim3(1024), 0, s, a);
+hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l) {
+  MOE_LAUNCH(prefill_plan_kernel, dim3(1), dim3(1024), 0, l, a);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, hipStream_t s) {
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(prefill_up_kernel, dim3(ntiles), dim3(256), 0, s, tiles, jobs, xn, perm_tok, act, d, d_ff);
+  MOE_LAUNCH(prefill_gemm_v2_kernel<true>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, perm_tok,
+             (void *)act, d, d_ff);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, hipStream_t s) {
+                               float *Y, int d, int d_ff, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(prefill_down_kernel, dim3(ntiles), dim3(256), 0, s, tiles, jobs, act, Y, d, d_ff);
+  MOE_LAUNCH(prefill_gemm_v2_kernel<false>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
+             (const int32_t *)nullptr, (void *)Y, d, d_ff);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
-                                    int d, int K, hipStream_t s) {
-  hipLaunchKernelGGL(prefill_unpermute_kernel, dim3(T), dim3(256), 0, s, H, Y, g, pos_of, T, d, K);
+                                    int d, int K, const Launch &l) {
+  MOE_LAUNCH(prefill_unpermute_kernel, dim3(T), dim3(256), 0, l, H, Y, g, pos_of, T, d, K);
   return hipGetLastError();
 }
 
-int prefill_tile_rows() { return kTile; }
+int prefill_tile_rows() { return kBM; }
+int prefill_tile_cols() { return kBN; }
 
 }  // namespace moe

@@ -397,8 +397,8 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
 
 }  // namespace
 
-hipError_t launch_router(const RouterArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(router_kernel, dim3(1), dim3(kThreads), 0, s, a);
+hipError_t launch_router(const RouterArgs &a, const Launch &l) {
+  MOE_LAUNCH(router_kernel, dim3(1), dim3(kThreads), 0, l, a);
   return hipGetLastError();
 }
 
