@@ -33,10 +33,9 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef double double4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kGateTok = 16;     // tokens per gate workgroup
-constexpr int kGateChunk = 128;  // columns staged per step
-constexpr int kTile = 64;        // GEMM output tile (rows and columns)
 constexpr int kKStep = 32;       // GEMM reduction step (one MFMA depth)
 constexpr int kLdsK = kKStep + 8;  // padded LDS row (bf16 elements)
 
@@ -50,62 +49,138 @@ __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v));
 
 // ---------------------------------------------------------------------------
 // 1. gate logits, top-K, combine weights, normalised bf16 rows
+//
+// Z = H W_g^T is a dense T x E x d contraction kept in fp64 (every bf16 x fp32
+// product is exact there), so it runs on the fp64 matrix cores:
+// v_mfma_f64_16x16x4_f64, A = 16 tokens x 4 columns, B = 4 columns x 16
+// experts; lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16] and gets
+// back D[l / 16 + 4 v][l % 16], v = 0..3.
+//
+// A workgroup holds 16 tokens and all experts.  The columns are cut into
+// 16-wide blocks dealt round-robin to the four waves, so each wave reads a
+// distinct quarter of H.  In a block, lane (i, kq) = (lane % 16, lane / 16)
+// loads columns 4kq .. 4kq+3 of token row i and of expert row 16g + i for
+// each expert group g, and MFMA step s uses column 4kq + s of both, so A and
+// B always pair the same column.  The waves' partial sums meet in LDS and
+// are added in wave order.
+constexpr int kGateWaves = 4;
+constexpr int kGateAhead = 2;  // blocks in flight per wave
+
+struct GateBlock {
+  float4 h;              // 4 columns of this lane's token row
+  uint2 w[kMaxE / 16];   // 4 bf16 columns of this lane's row in each expert group
+  float4 wf[kMaxE / 16]; // fp32 gate weights instead (dtype 0)
+};
+
+template <int DT>
+__device__ __forceinline__ void gate_load(GateBlock &b, const float *hrow, const uint8_t *wbase, int ng, int k,
+                                          int d, int E, int i) {
+  b.h = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (hrow && k < d) b.h = *reinterpret_cast<const float4 *>(hrow + k);
+#pragma unroll
+  for (int g = 0; g < kMaxE / 16; ++g) {
+    const int e = 16 * g + i;
+    if (DT == 1) {
+      b.w[g] = make_uint2(0, 0);
+      if (g < ng && e < E && k < d)
+        b.w[g] = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(wbase) + (size_t)e * d + k);
+    } else {
+      b.wf[g] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (g < ng && e < E && k < d)
+        b.wf[g] = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(wbase) + (size_t)e * d + k);
+    }
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ void gate_mfma(const GateBlock &b, int ng, double4_t *acc, double &sq) {
+  const double h4[4] = {b.h.x, b.h.y, b.h.z, b.h.w};
+#pragma unroll
+  for (int s = 0; s < 4; ++s) sq = fma(h4[s], h4[s], sq);
+#pragma unroll
+  for (int g = 0; g < kMaxE / 16; ++g) {
+    if (g >= ng) break;
+    double w4[4];
+    if (DT == 1) {
+      w4[0] = __uint_as_float(b.w[g].x << 16);
+      w4[1] = __uint_as_float(b.w[g].x & 0xFFFF0000u);
+      w4[2] = __uint_as_float(b.w[g].y << 16);
+      w4[3] = __uint_as_float(b.w[g].y & 0xFFFF0000u);
+    } else {
+      w4[0] = b.wf[g].x;
+      w4[1] = b.wf[g].y;
+      w4[2] = b.wf[g].z;
+      w4[3] = b.wf[g].w;
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc[g] = __builtin_amdgcn_mfma_f64_16x16x4f64(h4[s], w4[s], acc[g], 0, 0, 0);
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ void gate_partial(const PrefillArgs &a, int t0, int wave, int lane,
+                                             double (*zp)[kGateTok][kMaxE], double (*rp)[kGateTok]) {
+  const int d = a.d, E = a.E;
+  const int i = lane % 16, kq = lane / 16;
+  const int ng = (E + 15) / 16;
+  const float *hrow = t0 + i < a.T ? a.H + (size_t)(t0 + i) * d : nullptr;
+  const uint8_t *wbase = static_cast<const uint8_t *>(a.gate);
+  double4_t acc[kMaxE / 16];
+#pragma unroll
+  for (int g = 0; g < kMaxE / 16; ++g) acc[g] = double4_t{0.0, 0.0, 0.0, 0.0};
+  double sq = 0.0;
+  const int stride = 16 * kGateWaves;
+  GateBlock buf[kGateAhead];
+#pragma unroll
+  for (int j = 0; j < kGateAhead; ++j) gate_load<DT>(buf[j], hrow, wbase, ng, (wave + j * kGateWaves) * 16 + 4 * kq, d, E, i);
+  for (int k0 = wave * 16; k0 < d; k0 += stride * kGateAhead) {
+#pragma unroll
+    for (int j = 0; j < kGateAhead; ++j) {
+      const GateBlock cur = buf[j];
+      gate_load<DT>(buf[j], hrow, wbase, ng, k0 + (j + kGateAhead) * stride + 4 * kq, d, E, i);
+      gate_mfma<DT>(cur, ng, acc, sq);
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < kMaxE / 16; ++g)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      if (16 * g + i < E) zp[wave][kq + 4 * v][16 * g + i] = acc[g][v];
+  sq += __shfl_xor(sq, 16, kWave);
+  sq += __shfl_xor(sq, 32, kWave);
+  if (kq == 0) rp[wave][i] = sq;
+}
+
 __global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
-  __shared__ float hs[kGateTok][kGateChunk];
-  __shared__ float ws[kMaxE][kGateChunk + 1];
-  __shared__ double zs[kGateTok][kMaxE];
-  __shared__ double rs[kGateTok];
+  __shared__ double zp[kGateWaves][kGateTok][kMaxE];
+  __shared__ double rp[kGateWaves][kGateTok];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int t0 = blockIdx.x * kGateTok;
   const int E = a.E, d = a.d;
-  const int tok = tid / 16, eb = tid % 16;
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
-  double sq = 0.0;
-  for (int c0 = 0; c0 < d; c0 += kGateChunk) {
-    const int cw = min(kGateChunk, d - c0);
-    // 16 x 128 hidden values: thread -> row tid/16, 8 consecutive columns
-    {
-      const int r = tid / 16, c = (tid % 16) * 8;
-      const int t = t0 + r;
-      for (int i = 0; i < 8; ++i) {
-        float v = 0.0f;
-        if (t < a.T && c + i < cw) v = a.H[(size_t)t * d + c0 + c + i];
-        hs[r][c + i] = v;
-        sq = fma((double)v, (double)v, sq);
-      }
-    }
-    // E x 128 gate weights widened to fp32 (exact)
-    for (int i = tid; i < E * kGateChunk; i += 256) {
-      const int e = i / kGateChunk, c = i % kGateChunk;
-      float w = 0.0f;
-      if (c < cw) {
-        const size_t idx = (size_t)e * d + c0 + c;
-        w = a.dtype == 1 ? __uint_as_float((uint32_t)static_cast<const uint16_t *>(a.gate)[idx] << 16)
-                         : static_cast<const float *>(a.gate)[idx];
-      }
-      ws[e][c] = w;
-    }
-    __syncthreads();
-    for (int c = 0; c < cw; ++c) {
-      const double hv = hs[tok][c];
+  if (a.dtype == 1)
+    gate_partial<1>(a, t0, wave, lane, zp, rp);
+  else
+    gate_partial<0>(a, t0, wave, lane, zp, rp);
+  __syncthreads();
+  // zs = zp[0] + zp[1] + zp[2] + zp[3] in that order, kept in zp[0]
+  for (int x = tid; x < kGateTok * kMaxE; x += 256) {
+    const int r = x / kMaxE, e = x % kMaxE;
+    if (e < E) {
+      double z = zp[0][r][e];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = eb + 16 * j;
-        if (e < E) acc[j] = fma((double)ws[e][c], hv, acc[j]);
-      }
+      for (int w = 1; w < kGateWaves; ++w) z += zp[w][r][e];
+      zp[0][r][e] = z;
     }
-    __syncthreads();
   }
-  // row sums of squares: the 16 threads of a row are 16 consecutive lanes
+  if (tid < kGateTok) {
+    double r = rp[0][tid];
 #pragma unroll
-  for (int o = 8; o > 0; o >>= 1) sq += __shfl_xor(sq, o, kWave);
-  if (eb == 0) rs[tok] = sq;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = eb + 16 * j;
-    if (e < E) zs[tok][e] = acc[j];
+    for (int w = 1; w < kGateWaves; ++w) r += rp[w][tid];
+    rp[0][tid] = r;
   }
   __syncthreads();
+  double (*zs)[kMaxE] = zp[0];
+  double *rs = rp[0];
 
   // top-K per token: wave w handles tokens 4w .. 4w+3
   for (int q = 0; q < kGateTok / 4; ++q) {
@@ -333,17 +408,8 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
 // 3. grouped GEMMs.  A rows come from the sorted pair order; B = expert
 // weights stored out x in (K contiguous), so both operands are K-major.
 
-// Load a 64 x 32 bf16 tile into LDS (row stride kLdsK); one 16-byte piece per
-// thread.  rowptr(i) gives the address of row i's element k0, or nullptr.
-template <typename RowFn>
-__device__ __forceinline__ void stage_tile(uint16_t (*dst)[kLdsK], RowFn rowptr, int k0, int K) {
-  const int i = threadIdx.x / 4, q = threadIdx.x % 4;
-  const uint16_t *p = rowptr(i);
-  uint4 v = make_uint4(0, 0, 0, 0);
-  if (p && k0 + q * 8 < K) v = *reinterpret_cast<const uint4 *>(p + q * 8);
-  *reinterpret_cast<uint4 *>(&dst[i][q * 8]) = v;
-}
-
+// One MFMA 16x16x32 operand fragment from a K-major LDS tile: lane i holds
+// row (i % 16), elements (i / 16) * 8 .. + 8 of the 32-deep slice.
 __device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row, int lane) {
   const uint4 v = *reinterpret_cast<const uint4 *>(&src[row][(lane / 16) * 8]);
   bf16x8 r;
@@ -351,106 +417,11 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row
   return r;
 }
 
-// act[row, n] = SiLU(x_row . W1[n]) * (x_row . W3[n]) for one 64 x 64 tile
-__global__ __launch_bounds__(256) void prefill_up_kernel(const GemmTile *tiles, const GemmJob *jobs,
-                                                         const uint16_t *xn, const int32_t *perm_tok,
-                                                         uint16_t *act, int d, int d_ff) {
-  __shared__ uint16_t As[kTile][kLdsK], B1[kTile][kLdsK], B3[kTile][kLdsK];
-  const GemmTile t = tiles[blockIdx.x];
-  const GemmJob j = jobs[t.job];
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int wm = wave / 2, wn = wave % 2;
-  const uint16_t *w1 = j.w;
-  const uint16_t *w3 = j.w + (size_t)d_ff * d;
-  floatx4 c1[2][2], c3[2][2];
-  for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b)
-      for (int i = 0; i < 4; ++i) c1[a][b][i] = c3[a][b][i] = 0.0f;
-  for (int k0 = 0; k0 < d; k0 += kKStep) {
-    stage_tile(As, [&](int i) -> const uint16_t * {
-      const int m = t.m0 + i;
-      if (m >= j.nrows) return nullptr;
-      return xn + (size_t)perm_tok[j.row0 + m] * d + k0;
-    }, k0, d);
-    stage_tile(B1, [&](int i) -> const uint16_t * {
-      const int n = t.n0 + i;
-      return n < d_ff ? w1 + (size_t)n * d + k0 : nullptr;
-    }, k0, d);
-    stage_tile(B3, [&](int i) -> const uint16_t * {
-      const int n = t.n0 + i;
-      return n < d_ff ? w3 + (size_t)n * d + k0 : nullptr;
-    }, k0, d);
-    __syncthreads();
-    bf16x8 af[2], b1f[2], b3f[2];
-    for (int a = 0; a < 2; ++a) af[a] = lds_frag(As, wm * 32 + a * 16 + lane % 16, lane);
-    for (int b = 0; b < 2; ++b) {
-      b1f[b] = lds_frag(B1, wn * 32 + b * 16 + lane % 16, lane);
-      b3f[b] = lds_frag(B3, wn * 32 + b * 16 + lane % 16, lane);
-    }
-    for (int a = 0; a < 2; ++a)
-      for (int b = 0; b < 2; ++b) {
-        c1[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], b1f[b], c1[a][b], 0, 0, 0);
-        c3[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], b3f[b], c3[a][b], 0, 0, 0);
-      }
-    __syncthreads();
-  }
-  for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b)
-      for (int i = 0; i < 4; ++i) {
-        const int m = t.m0 + wm * 32 + a * 16 + (lane / 16) * 4 + i;
-        const int n = t.n0 + wn * 32 + b * 16 + lane % 16;
-        if (m < j.nrows && n < d_ff)
-          act[(size_t)(j.row0 + m) * d_ff + n] = f32_to_bf16_rne(silu(c1[a][b][i]) * c3[a][b][i]);
-      }
-}
-
-// Y[row, n] = act_row . W2[n] for one 64 x 64 tile
-__global__ __launch_bounds__(256) void prefill_down_kernel(const GemmTile *tiles, const GemmJob *jobs,
-                                                           const uint16_t *act, float *Y, int d, int d_ff) {
-  __shared__ uint16_t As[kTile][kLdsK], Bs[kTile][kLdsK];
-  const GemmTile t = tiles[blockIdx.x];
-  const GemmJob j = jobs[t.job];
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int wm = wave / 2, wn = wave % 2;
-  const uint16_t *w2 = j.w + 2 * (size_t)d_ff * d;
-  floatx4 c[2][2];
-  for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b)
-      for (int i = 0; i < 4; ++i) c[a][b][i] = 0.0f;
-  for (int k0 = 0; k0 < d_ff; k0 += kKStep) {
-    stage_tile(As, [&](int i) -> const uint16_t * {
-      const int m = t.m0 + i;
-      return m < j.nrows ? act + (size_t)(j.row0 + m) * d_ff + k0 : nullptr;
-    }, k0, d_ff);
-    stage_tile(Bs, [&](int i) -> const uint16_t * {
-      const int n = t.n0 + i;
-      return n < d ? w2 + (size_t)n * d_ff + k0 : nullptr;
-    }, k0, d_ff);
-    __syncthreads();
-    bf16x8 af[2], bf[2];
-    for (int a = 0; a < 2; ++a) af[a] = lds_frag(As, wm * 32 + a * 16 + lane % 16, lane);
-    for (int b = 0; b < 2; ++b) bf[b] = lds_frag(Bs, wn * 32 + b * 16 + lane % 16, lane);
-    for (int a = 0; a < 2; ++a)
-      for (int b = 0; b < 2; ++b)
-        c[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[a], bf[b], c[a][b], 0, 0, 0);
-    __syncthreads();
-  }
-  for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b)
-      for (int i = 0; i < 4; ++i) {
-        const int m = t.m0 + wm * 32 + a * 16 + (lane / 16) * 4 + i;
-        const int n = t.n0 + wn * 32 + b * 16 + lane % 16;
-        if (m < j.nrows && n < d) Y[(size_t)(j.row0 + m) * d + n] = c[a][b][i];
-      }
-}
-
-// ---------------------------------------------------------------------------
-// Grouped GEMM, 128 x 128 output tile per workgroup (four waves of 64 x 64,
+// 128 x 128 output tile per workgroup (four waves of 64 x 64,
 // 4 x 4 blocks of v_mfma_f32_16x16x32_bf16 each).  The next 32-deep K slice
 // is loaded from global memory into registers while the current one is
 // multiplied out of LDS; LDS is double-buffered so one barrier per step
-// suffices.  Every output still accumulates its K slices in ascending order
-// with the same instruction as the 64 x 64 kernels, so results are identical.
+// suffices.  Every output accumulates its K slices in ascending order.
 constexpr int kBM = 128, kBN = 128;
 
 struct TileRows {
@@ -458,7 +429,7 @@ struct TileRows {
 };
 
 template <bool UP>
-__global__ __launch_bounds__(256) void prefill_gemm_v2_kernel(const GemmTile *tiles, const GemmJob *jobs,
+__global__ __launch_bounds__(256) void prefill_gemm_kernel(const GemmTile *tiles, const GemmJob *jobs,
                                                               const uint16_t *a_src, const int32_t *perm_tok,
                                                               void *out, int d, int d_ff) {
   constexpr int NB = UP ? 2 : 1;  // B matrices: W1 and W3, or W2
@@ -590,7 +561,7 @@ hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l) {
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH(prefill_gemm_v2_kernel<true>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, perm_tok,
+  MOE_LAUNCH(prefill_gemm_kernel<true>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, perm_tok,
              (void *)act, d, d_ff);
   return hipGetLastError();
 }
@@ -598,7 +569,7 @@ hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *j
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
                                float *Y, int d, int d_ff, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH(prefill_gemm_v2_kernel<false>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
+  MOE_LAUNCH(prefill_gemm_kernel<false>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
              (const int32_t *)nullptr, (void *)Y, d, d_ff);
   return hipGetLastError();
 }
