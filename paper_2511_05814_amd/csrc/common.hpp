@@ -194,4 +194,28 @@ __device__ __forceinline__ double wave_sum_d(double v) {
   return v;
 }
 
+// Top-K of E <= 64 logits held in LDS, in rank order: larger z first, lower
+// id on ties, NaN ranked as -inf.  Lane e < E counts the entries that come
+// before its own in that order, which is its rank, and rank r < K writes its
+// id to out[r].  Returns out[lane] on lanes < K and -1 elsewhere.  Called by
+// one whole wave; `out` is LDS owned by that wave.
+__device__ __forceinline__ double rank_key(double z) { return z != z ? -__builtin_inf() : z; }
+
+__device__ inline int wave_topk_lds(const double *z, int E, int K, int lane, int *out) {
+  if (lane < E) {
+    const double mine = rank_key(z[lane]);
+    int rank = 0;
+#pragma unroll 8
+    for (int o = 0; o < E; ++o) {
+      const double zo = rank_key(z[o]);
+      rank += (zo > mine || (zo == mine && o < lane)) ? 1 : 0;
+    }
+    if (rank < K) out[rank] = lane;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  return lane < K ? out[lane] : -1;
+}
+
 }  // namespace moe

@@ -154,6 +154,7 @@ __device__ __forceinline__ void gate_partial(const PrefillArgs &a, int t0, int w
 __global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
   __shared__ double zp[kGateWaves][kGateTok][kMaxE];
   __shared__ double rp[kGateWaves][kGateTok];
+  __shared__ int s_top[kGateWaves][kMaxK];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int t0 = blockIdx.x * kGateTok;
   const int E = a.E, d = a.d;
@@ -187,28 +188,7 @@ __global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
     const int r = wave * (kGateTok / 4) + q;
     const int t = t0 + r;
     if (t >= a.T) break;
-    const double z = lane < E ? zs[r][lane] : 0.0;
-    // rank order: larger z first, lower id on ties
-    bool avail = lane < E;
-    int mine = -1;
-    for (int k = 0; k < a.K; ++k) {
-      double bz = avail ? z : -INFINITY;
-      int bl = avail ? lane : 1000 + lane;
-      int bv = avail ? 1 : 0;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const double oz = __shfl_xor(bz, o, kWave);
-        const int ol = __shfl_xor(bl, o, kWave);
-        const int ov = __shfl_xor(bv, o, kWave);
-        if ((ov && !bv) || (ov == bv && (oz > bz || (oz == bz && ol < bl)))) {
-          bz = oz;
-          bl = ol;
-          bv = ov;
-        }
-      }
-      if (lane == k) mine = bl;
-      if (lane == bl) avail = false;
-    }
+    const int mine = wave_topk_lds(zs[r], E, a.K, lane, s_top[wave]);
     const double rr = sqrt(rs[r] / (double)d + 1e-5);
     const double zr = (lane < a.K) ? zs[r][mine] : 0.0;
     const double z0 = __shfl(zr, 0, kWave);

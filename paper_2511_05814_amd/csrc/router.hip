@@ -25,67 +25,75 @@ namespace {
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
 
-__device__ double gate_row_dot(const void *gate, int dtype, size_t row_off, const float *h, int d,
-                               int lane) {
-  double acc = 0.0;
-  if (dtype == 1) {  // bf16
-    const uint16_t *w = static_cast<const uint16_t *>(gate) + row_off;
-    for (int c = lane * 8; c < d; c += kWave * 8) {
-      const uint4 v = *reinterpret_cast<const uint4 *>(w + c);
-      float f[8];
-      bf16x8_to_f32(v, f);
-      const float4 h0 = *reinterpret_cast<const float4 *>(h + c);
-      const float4 h1 = *reinterpret_cast<const float4 *>(h + c + 4);
-      acc = fma((double)f[0], (double)h0.x, acc);
-      acc = fma((double)f[1], (double)h0.y, acc);
-      acc = fma((double)f[2], (double)h0.z, acc);
-      acc = fma((double)f[3], (double)h0.w, acc);
-      acc = fma((double)f[4], (double)h1.x, acc);
-      acc = fma((double)f[5], (double)h1.y, acc);
-      acc = fma((double)f[6], (double)h1.z, acc);
-      acc = fma((double)f[7], (double)h1.w, acc);
-    }
-  } else {  // fp32
-    const float *w = static_cast<const float *>(gate) + row_off;
-    for (int c = lane * 4; c < d; c += kWave * 4) {
-      const float4 v = *reinterpret_cast<const float4 *>(w + c);
-      const float4 hv = *reinterpret_cast<const float4 *>(h + c);
-      acc = fma((double)v.x, (double)hv.x, acc);
-      acc = fma((double)v.y, (double)hv.y, acc);
-      acc = fma((double)v.z, (double)hv.z, acc);
-      acc = fma((double)v.w, (double)hv.w, acc);
-    }
-  }
-  return wave_sum_d(acc);
-}
+// Gate logits z[row] for up to two layers: rows 0..E-1 belong to a.layer (when
+// routing here), rows E..2E-1 to a.spec_layer (when speculating); only the
+// needed rows are visited.  Wave w owns needed rows r0 + w, r0 + w + kWaves,
+// ...; lane i covers columns EPL*i + EPL*64*c of a row (chunk c), accumulating
+// in fp64 in column order, and the wave sums the lanes at the end of each row.
+// h comes from LDS.  The weight loads of kBatch (row, chunk) items are issued
+// together, from addresses clamped into the gate array so that no load sits
+// behind a branch (a load under a condition is waited for on the spot), and
+// only then used.
+constexpr int kBatch = 16;
+constexpr int kMaxD = 16384;
 
-// Top-K over lanes < E holding z (rank order: larger z first, lower id on
-// ties; NaN ranks as -inf).  Lane r < K receives the id of rank r.
-__device__ int wave_topk(double z, int E, int K, int lane) {
-  const double NEG = -INFINITY;
-  bool avail = lane < E;
-  const double key = (z != z) ? NEG : z;
-  int mine = -1;
-  for (int r = 0; r < K; ++r) {
-    double bz = avail ? key : NEG;
-    int bl = avail ? lane : 1000 + lane;
-    int bv = avail ? 1 : 0;
+template <int DT>
+__device__ void gate_logits(const RouterArgs &a, const float *hs, int r0, int r1, int wave, int lane,
+                            double *zs) {
+  constexpr int EPL = DT == 1 ? 8 : 4;  // elements per 16-byte load
+  constexpr int ESZ = DT == 1 ? 2 : 4;
+  const int E = a.E, d = a.d;
+  const int cpr = (d + kWave * EPL - 1) / (kWave * EPL);
+  const int M = r0 + wave < r1 ? (r1 - r0 - wave + kWaves - 1) / kWaves : 0;
+  const int n = M * cpr;
+  const uint8_t *gate = static_cast<const uint8_t *>(a.gate);
+  double acc = 0.0;
+  for (int j0 = 0; j0 < n; j0 += kBatch) {
+    uint4 v[kBatch];
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const double oz = __shfl_xor(bz, o, kWave);
-      const int ol = __shfl_xor(bl, o, kWave);
-      const int ov = __shfl_xor(bv, o, kWave);
-      const bool take = (ov && !bv) || (ov == bv && (oz > bz || (oz == bz && ol < bl)));
-      if (take) {
-        bz = oz;
-        bl = ol;
-        bv = ov;
+    for (int u = 0; u < kBatch; ++u) {
+      const int j = min(j0 + u, n - 1);
+      const int row = r0 + wave + kWaves * (j / cpr);
+      const int gl = row < E ? a.layer : a.spec_layer;
+      const int e = row < E ? row : row - E;
+      const int col = min((j % cpr) * kWave * EPL + lane * EPL, d - EPL);
+      v[u] = *reinterpret_cast<const uint4 *>(gate + (((size_t)gl * E + e) * d + col) * ESZ);
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int j = j0 + u;
+      if (j < n) {
+        const int c = j % cpr;
+        const int col = c * kWave * EPL + lane * EPL;
+        if (col < d) {
+          const float4 h0 = *reinterpret_cast<const float4 *>(hs + col);
+          if (DT == 1) {
+            const float4 h1 = *reinterpret_cast<const float4 *>(hs + col + 4);
+            float f[8];
+            bf16x8_to_f32(v[u], f);
+            acc = fma((double)f[0], (double)h0.x, acc);
+            acc = fma((double)f[1], (double)h0.y, acc);
+            acc = fma((double)f[2], (double)h0.z, acc);
+            acc = fma((double)f[3], (double)h0.w, acc);
+            acc = fma((double)f[4], (double)h1.x, acc);
+            acc = fma((double)f[5], (double)h1.y, acc);
+            acc = fma((double)f[6], (double)h1.z, acc);
+            acc = fma((double)f[7], (double)h1.w, acc);
+          } else {
+            acc = fma((double)__uint_as_float(v[u].x), (double)h0.x, acc);
+            acc = fma((double)__uint_as_float(v[u].y), (double)h0.y, acc);
+            acc = fma((double)__uint_as_float(v[u].z), (double)h0.z, acc);
+            acc = fma((double)__uint_as_float(v[u].w), (double)h0.w, acc);
+          }
+        }
+        if (c == cpr - 1) {
+          const double z = wave_sum_d(acc);
+          if (lane == 0) zs[r0 + wave + kWaves * (j / cpr)] = z;
+          acc = 0.0;
+        }
       }
     }
-    if (lane == r) mine = bl;
-    if (lane == bl) avail = false;
   }
-  return mine;
 }
 
 // Lane of the resident, unpinned expert with the smallest policy key
@@ -218,18 +226,19 @@ __device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t
   }
   if (lane == 0) {
     T->clock = clock;
-    T->lookups += 1;
+    T->lookups = token + 1;
     fl->n = n_miss;
     fl->layer = a.layer;
     a.route->k = K;
-    st->v[ST_HITS] += hits;
-    st->v[ST_MISSES] += n_miss;
-    st->v[ST_EVICT] += n_miss;
-    st->v[ST_PF_USEFUL] += useful;
-    st->v[ST_PF_WASTED] += wasted;
-    st->v[ST_LOOKUPS] += 1;
-    st->v[ST_BYTES] += (uint64_t)n_miss * a.expert_bytes;
   }
+  // counters: one lane each, so the read-modify-writes overlap
+  const uint64_t add = lane == ST_HITS ? (uint64_t)hits
+                     : lane == ST_MISSES || lane == ST_EVICT ? (uint64_t)n_miss
+                     : lane == ST_PF_USEFUL ? (uint64_t)useful
+                     : lane == ST_PF_WASTED ? (uint64_t)wasted
+                     : lane == ST_LOOKUPS ? 1ull
+                     : lane == ST_BYTES ? (uint64_t)n_miss * a.expert_bytes : 0ull;
+  if (add) st->v[lane] += add;
 }
 
 // Wave 1: insert up to pmax of the K guesses (lane r holds rank r's guess)
@@ -300,15 +309,18 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
     T->clock = clock;
     fl->n = issued;
     fl->layer = L2;
-    st->v[ST_PF_GUESS] += K;
-    st->v[ST_PF_ISSUED] += issued;
-    st->v[ST_PF_WASTED] += wasted;
-    st->v[ST_BYTES] += (uint64_t)issued * a.expert_bytes;
   }
+  const uint64_t add = lane == ST_PF_GUESS ? (uint64_t)K
+                     : lane == ST_PF_ISSUED ? (uint64_t)issued
+                     : lane == ST_PF_WASTED ? (uint64_t)wasted
+                     : lane == ST_BYTES ? (uint64_t)issued * a.expert_bytes : 0ull;
+  if (add) st->v[lane] += add;
 }
 
 __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
+  __shared__ __align__(16) float hs[kMaxD];
   __shared__ double zs[2 * kMaxE];
+  __shared__ int s_top[2][kMaxK];
   __shared__ double red[kWaves];
   __shared__ double s_rms;
   __shared__ uint64_t s_tbase;
@@ -318,27 +330,29 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   const bool route_here = a.demand && a.inj_ids == nullptr;
   const bool spec = a.spec_layer >= 0;
 
-  for (int row = wave; row < 2 * E; row += kWaves) {
-    const bool first = row < E;
-    if (first && !route_here) continue;
-    if (!first && !spec) continue;
-    const int gl = first ? a.layer : a.spec_layer;
-    const int e = first ? row : row - E;
-    const double z = gate_row_dot(a.gate, a.dtype, ((size_t)gl * E + e) * (size_t)d, a.h, d, lane);
-    if (lane == 0) zs[row] = z;
-  }
   if (tid == 0) {
     s_tbase = a.trace ? *a.trace_count : 0;
     s_demand_ok = 0;
   }
-  if (route_here) {
+  if (route_here || spec) {
+    // h into LDS (h is NULL when no gate row is needed); sum of squares on the way
     double ss = 0.0;
-    for (int i = tid; i < d; i += kThreads) {
-      const double v = a.h[i];
-      ss = fma(v, v, ss);
+    for (int i = tid * 4; i < d; i += kThreads * 4) {
+      const float4 v = *reinterpret_cast<const float4 *>(a.h + i);
+      *reinterpret_cast<float4 *>(hs + i) = v;
+      ss = fma((double)v.x, (double)v.x, ss);
+      ss = fma((double)v.y, (double)v.y, ss);
+      ss = fma((double)v.z, (double)v.z, ss);
+      ss = fma((double)v.w, (double)v.w, ss);
     }
     ss = wave_sum_d(ss);
     if (lane == 0) red[wave] = ss;
+    __syncthreads();
+    const int r0 = route_here ? 0 : E, r1 = spec ? 2 * E : E;
+    if (a.dtype == 1)
+      gate_logits<1>(a, hs, r0, r1, wave, lane, zs);
+    else
+      gate_logits<0>(a, hs, r0, r1, wave, lane, zs);
   }
   __syncthreads();
   if (route_here && tid == 0) {
@@ -351,7 +365,7 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   if (wave == 0 && a.demand) {
     int idreg;
     if (route_here) {
-      idreg = wave_topk(lane < E ? zs[lane] : 0.0, E, a.K, lane);
+      idreg = wave_topk_lds(zs, E, a.K, lane, s_top[0]);
       // renormalised softmax over the selected logits z / rms (rank 0 is the max)
       double zr = (lane < a.K) ? zs[idreg < 0 ? 0 : idreg] : 0.0;
       const double r = s_rms;
@@ -387,7 +401,7 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     }
   }
   if (wave == 1 && spec) {
-    const int greg = wave_topk(lane < E ? zs[E + lane] : 0.0, E, a.K, lane);
+    const int greg = wave_topk_lds(zs + E, E, a.K, lane, s_top[1]);
     prefetch_insert(a, greg, lane, s_tbase + (a.demand ? (uint64_t)a.K : 0));
   }
   __syncthreads();
