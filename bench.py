@@ -183,7 +183,8 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=8,
                     help="decode tokens the fp64 oracle is timed on (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--fetch", choices=["kernel", "dma"], default="kernel")
+    ap.add_argument("--fetch", choices=["split", "kernel", "dma"], default="split",
+                    help="split: demand misses by the copy kernel, speculative prefetches by the DMA engines")
     ap.add_argument("--tokens", type=int, default=0,
                     help="decode only the first N tokens of the workload (profiling passes)")
     ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
@@ -201,7 +202,7 @@ def main():
     cfg = wl.CONFIGS[args.workload]
     if args.tokens:
         cfg = cfg.with_(tokens=min(args.tokens, cfg.tokens))
-    fetch_mode = b.MOE_FETCH_KERNEL if args.fetch == "kernel" else b.MOE_FETCH_DMA
+    fetch_mode = {"kernel": b.MOE_FETCH_KERNEL, "dma": b.MOE_FETCH_DMA, "split": b.MOE_FETCH_SPLIT}[args.fetch]
     primary_slots = 16 if cfg.experts == 64 else 4
     # (policy, slots, speculate): the first entry is the timed headline run
     runs = [("lfu", primary_slots, cfg.prefetch_max > 0)]

@@ -52,8 +52,14 @@ enum { MOE_PREFETCH_NEXT = 1 };
 enum {
   MOE_FETCH_KERNEL = 0, /* a copy kernel on the copy stream reads the host store
                            directly; no host round trip per layer            */
-  MOE_FETCH_DMA = 1     /* the host waits for the routing decision, then issues
+  MOE_FETCH_DMA = 1,    /* the host waits for the routing decision, then issues
                            one DMA-engine copy per missed expert              */
+  MOE_FETCH_SPLIT = 2   /* demand misses by the copy kernel (no host round
+                           trip on the critical path); speculative prefetches
+                           by the DMA engines, which read host memory without
+                           slowing the FFN kernels that run meanwhile. The
+                           host reads each prefetch list back on a stream the
+                           library owns, after enqueueing the layer's FFN.   */
 };
 
 /* Limits of this build. */

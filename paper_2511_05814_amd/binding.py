@@ -19,7 +19,7 @@ MOE_POLICY_LRU, MOE_POLICY_LFU = 0, 1
 MOE_DTYPE_F32, MOE_DTYPE_BF16 = 0, 1
 MOE_OK, MOE_ERR_ARG, MOE_ERR_STATE, MOE_ERR_HIP, MOE_ERR_NOMEM = 0, -1, -2, -3, -4
 MOE_PREFETCH_NEXT = 1
-MOE_FETCH_KERNEL, MOE_FETCH_DMA = 0, 1
+MOE_FETCH_KERNEL, MOE_FETCH_DMA, MOE_FETCH_SPLIT = 0, 1, 2
 MOE_MAX_EXPERTS, MOE_MAX_TOPK = 64, 16
 
 POLICIES = {"lru": MOE_POLICY_LRU, "lfu": MOE_POLICY_LFU}

@@ -114,9 +114,10 @@ struct moe_cache {
   std::vector<const uint8_t *> dev_layer_host;  // what that array must hold
   std::vector<hipEvent_t> ev_demand, ev_pf;
   hipEvent_t ev_router = nullptr;
+  hipStream_t ms = nullptr;  // library-owned: prefetch-list read-back (split fetch mode)
   std::vector<uint8_t> demand_pending, pf_pending;
   int sticky = MOE_OK;
-  FetchList *mirror = nullptr;  // pinned host copies of two fetch lists (DMA mode)
+  FetchList *mirror = nullptr;  // pinned host: demand list, prefetch list, error word (DMA / split modes)
   int last_route_kind = 0;      // 0 none, 1 decode, 2 prefill
   int last_prefill_T = 0;
   // batched prefill
@@ -233,7 +234,7 @@ static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
   if (d->dtype != MOE_DTYPE_F32 && d->dtype != MOE_DTYPE_BF16) return fail(MOE_ERR_ARG, "bad dtype");
   if (d->prefetch_max < 0 || d->prefetch_max > d->top_k)
     return fail(MOE_ERR_ARG, "prefetch_max must be in [0, top_k]");
-  if (d->fetch_mode != MOE_FETCH_KERNEL && d->fetch_mode != MOE_FETCH_DMA)
+  if (d->fetch_mode != MOE_FETCH_KERNEL && d->fetch_mode != MOE_FETCH_DMA && d->fetch_mode != MOE_FETCH_SPLIT)
     return fail(MOE_ERR_ARG, "bad fetch_mode");
   if (d->max_prefill_tokens < 0) return fail(MOE_ERR_ARG, "max_prefill_tokens < 0");
   if (d->max_prefill_tokens > 0 && d->dtype != MOE_DTYPE_BF16)
@@ -317,7 +318,7 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
     if (!hl[l] || misaligned(hl[l], 16))
       return fail(MOE_ERR_ARG, "host store of layer %d is NULL or not 16-byte aligned", l);
   }
-  if (d->fetch_mode == MOE_FETCH_KERNEL) {
+  if (d->fetch_mode != MOE_FETCH_DMA) {
     for (int l = 0; l < c->L; ++l) {
       void *p = nullptr;
       hipError_t e = hipHostGetDevicePointer(&p, const_cast<uint8_t *>(hl[l]), 0);
@@ -367,7 +368,9 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
     HIP_TRY0(hipEventCreateWithFlags(&c->ev_pf[l], hipEventDisableTiming));
   }
   HIP_TRY0(hipEventCreateWithFlags(&c->ev_router, hipEventDisableTiming));
-  HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->mirror), 2 * sizeof(FetchList),
+  if (c->fetch_mode == MOE_FETCH_SPLIT && !c->one_stream)
+    HIP_TRY0(hipStreamCreateWithFlags(&c->ms, hipStreamNonBlocking));
+  HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->mirror), 3 * sizeof(FetchList),
                                  hipHostMallocDefault));
   if (c->max_T > 0) {
     c->play = prefill_layout(c->K, c->d, c->dff, c->E, c->S, c->max_T, c->B);
@@ -438,7 +441,8 @@ int moe_cache_reset(moe_cache_t *c) {
 
 // Issue the copies for one fetch list that the router just wrote.
 static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_t q) {
-  if (c->fetch_mode == MOE_FETCH_KERNEL) {
+  const bool by_kernel = c->fetch_mode == MOE_FETCH_KERNEL || (c->fetch_mode == MOE_FETCH_SPLIT && mirror_idx == 0);
+  if (by_kernel) {
     Launch l;
     HIP_TRY(c, kernel_span(c, q, &l));
     HIP_TRY(c, launch_fetch(list, c->dev_layers, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
@@ -508,7 +512,8 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   kernel_span_done(c, SPAN_ROUTER, lr);
 
   hipStream_t q = c->xs;
-  if (c->fetch_mode == MOE_FETCH_KERNEL) {
+  const bool split = c->fetch_mode == MOE_FETCH_SPLIT;
+  if (c->fetch_mode != MOE_FETCH_DMA) {
     if (!c->one_stream) {
       HIP_TRY(c, hipEventRecord(c->ev_router, c->cs));
       HIP_TRY(c, hipStreamWaitEvent(q, c->ev_router, 0));
@@ -530,7 +535,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
       c->demand_pending[layer] = 1;
     }
   }
-  if (spec_layer >= 0) {
+  if (spec_layer >= 0 && !split) {
     int rc = issue_fetch(c, c->pl + spec_layer, 1, q);
     if (rc != MOE_OK) return rc;
     if (!c->one_stream) {
@@ -569,6 +574,24 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     HIP_TRY(c, launch_ffn_reduce(f, c->dtype, lx));
     kernel_span_done(c, SPAN_REDUCE, lx);
     c->last_route_kind = 1;
+  }
+  if (spec_layer >= 0 && split) {
+    // The prefetch list comes back on the library's own stream, so neither the
+    // FFN just enqueued nor the demand copies wait for the host; the DMA copies
+    // then queue on the copy stream behind this layer's demand copies.
+    hipStream_t m = c->ms ? c->ms : c->cs;
+    int32_t *err_mirror = reinterpret_cast<int32_t *>(&c->mirror[2]);
+    if (c->ms) HIP_TRY(c, hipStreamWaitEvent(m, c->ev_router, 0));
+    HIP_TRY(c, hipMemcpyAsync(&c->mirror[1], c->pl + spec_layer, sizeof(FetchList), hipMemcpyDeviceToHost, m));
+    HIP_TRY(c, hipMemcpyAsync(err_mirror, c->err, sizeof(int32_t), hipMemcpyDeviceToHost, m));
+    HIP_TRY(c, hipStreamSynchronize(m));
+    if (*err_mirror != ERR_NONE) return MOE_OK;  // reported at the next synchronising call
+    int rc = issue_fetch(c, c->pl + spec_layer, 1, q);
+    if (rc != MOE_OK) return rc;
+    if (!c->one_stream) {
+      HIP_TRY(c, hipEventRecord(c->ev_pf[spec_layer], q));
+      c->pf_pending[spec_layer] = 1;
+    }
   }
   return MOE_OK;
 }
@@ -989,6 +1012,7 @@ void moe_cache_destroy(moe_cache_t *c) {
     for (hipEvent_t e : c->ev_pf)
       if (e) (void)hipEventDestroy(e);
     if (c->ev_router) (void)hipEventDestroy(c->ev_router);
+    if (c->ms) (void)hipStreamDestroy(c->ms);
     if (c->mirror) (void)hipHostFree(c->mirror);
     if (c->h_plan) (void)hipHostFree(c->h_plan);
     if (c->h_sched) (void)hipHostFree(c->h_sched);

@@ -118,7 +118,7 @@ class OffloadedMoE:
     """One expert cache over a whole stack (one handle of the C ABI)."""
 
     def __init__(self, cfg: wl.Config, store: HostStore, gates: DeviceGates, slots: int,
-                 policy: str, prefetch_max: int = 0, fetch_mode: int = b.MOE_FETCH_KERNEL,
+                 policy: str, prefetch_max: int = 0, fetch_mode: int = b.MOE_FETCH_SPLIT,
                  trace_cap: Optional[int] = None, max_prefill_tokens: int = 0,
                  separate_copy_stream: bool = True):
         torch = _torch()

@@ -67,36 +67,42 @@ def test_streams_and_fetch_modes_give_identical_results(tiny):
     cfg = tiny.cfg
     _say("stream/fetch-mode equivalence")
     outs = []
-    for kw in (dict(), dict(separate_copy_stream=False), dict(fetch_mode=b.MOE_FETCH_DMA)):
+    for kw in (dict(), dict(separate_copy_stream=False), dict(fetch_mode=b.MOE_FETCH_DMA),
+               dict(fetch_mode=b.MOE_FETCH_KERNEL), dict(fetch_mode=b.MOE_FETCH_SPLIT, separate_copy_stream=False)):
         moe = tiny.cache(4, "lfu", prefetch_max=2, **kw)
         hs, recs, H = tiny.run(moe, 32, flags=b.MOE_PREFETCH_NEXT)
         outs.append((H.tobytes(), recs))
         moe.close()
-    assert outs[0] == outs[1] == outs[2]
+    assert all(o == outs[0] for o in outs[1:])
 
 
-def test_delayed_copy_stream_still_correct(tiny):
+@pytest.mark.parametrize("mode", ["kernel", "split"])
+def test_delayed_copy_stream_still_correct(tiny, mode):
     # A long spin on the copy stream ahead of every layer: if any FFN did not
-    # wait for the copies that fill its slots it would read stale weights.
+    # wait for the copies that fill its slots (demand copies, and with
+    # speculation the previous layer's prefetch copies) it would read stale
+    # weights.
     cfg = tiny.cfg
-    _say("delayed copy stream")
-    ref = tiny.cache(4, "lru")
-    _, recs0, H0 = tiny.run(ref, 16)
-    ref.close()
-    moe = tiny.cache(4, "lru")
-    h0 = wl.hidden_states(cfg, 16)
-    H = torch.from_numpy(h0).to("cuda")
-    with torch.cuda.stream(moe.compute):
-        for t in range(16):
-            for l in range(cfg.layers):
-                with torch.cuda.stream(moe.copy):
-                    torch.cuda._sleep(200000)
-                b.moe_decode_layer(moe.handle, l, H[t].data_ptr(), 0)
-    moe.sync()
-    recs, _ = moe.trace_records()
-    assert recs == recs0
-    assert H.cpu().numpy().tobytes() == H0.tobytes()
-    moe.close()
+    fm = b.MOE_FETCH_KERNEL if mode == "kernel" else b.MOE_FETCH_SPLIT
+    for flags, pmax in ((0, 0), (b.MOE_PREFETCH_NEXT, 2)):
+        _say(f"delayed copy stream {mode} flags={flags}")
+        ref = tiny.cache(4, "lru", prefetch_max=pmax, fetch_mode=fm)
+        _, recs0, H0 = tiny.run(ref, 16, flags=flags)
+        ref.close()
+        moe = tiny.cache(4, "lru", prefetch_max=pmax, fetch_mode=fm)
+        h0 = wl.hidden_states(cfg, 16)
+        H = torch.from_numpy(h0).to("cuda")
+        with torch.cuda.stream(moe.compute):
+            for t in range(16):
+                for l in range(cfg.layers):
+                    with torch.cuda.stream(moe.copy):
+                        torch.cuda._sleep(200000)
+                    b.moe_decode_layer(moe.handle, l, H[t].data_ptr(), flags)
+        moe.sync()
+        recs, _ = moe.trace_records()
+        assert recs == recs0
+        assert H.cpu().numpy().tobytes() == H0.tobytes()
+        moe.close()
 
 
 def test_reset_replays_identically(tiny):
@@ -239,7 +245,7 @@ def test_aliased_host_layers():
     rig.gates = offload.DeviceGates(cfg)
     rig.model = stack.Model(rig.gates.host, lambda l, e: rig.store.expert(l, e), cfg.d_model, cfg.d_ff,
                             cfg.dtype)
-    for mode in (b.MOE_FETCH_KERNEL, b.MOE_FETCH_DMA):
+    for mode in (b.MOE_FETCH_KERNEL, b.MOE_FETCH_DMA, b.MOE_FETCH_SPLIT):
         moe = rig.cache(4, "lru", prefetch_max=1, fetch_mode=mode)
         hs, recs, _ = rig.run(moe, cfg.tokens, flags=b.MOE_PREFETCH_NEXT)
         check_decode(cfg, rig.model, hs, recs, 4, "lru", prefetch=True, pmax=1, tol=_tol(cfg))
