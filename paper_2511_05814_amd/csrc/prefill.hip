@@ -19,9 +19,10 @@
 //              followed by the grouped GEMMs on those
 //   4. unpermute  h_t += sum_r g_tr Y[pos(t, r)] in rank order (no atomics)
 //
-// The grouped GEMMs are dense contractions (rows = tokens routed to one
-// expert), so they run on the matrix cores: a 64 x 64 output tile per
-// workgroup, four waves each owning 32 x 32, v_mfma_f32_16x16x32_bf16 steps.
+// The gate GEMM and the grouped GEMMs are dense contractions, so they run on
+// the matrix cores: the gate on the fp64 ones (exact products, fp64 sums),
+// the expert GEMMs (rows = pairs routed to one expert) on bf16 ones with a
+// 128 x 128 output tile per workgroup, four waves of 64 x 64 each.
 #include "common.hpp"
 #include "moe_offload.h"
 
