@@ -14,12 +14,13 @@ from typing import Callable, Dict, Optional
 
 import numpy as np
 
-from . import moe
+from . import moe, quant
 from .cache import LayerCache, make_caches
 
 
 class Model:
-    """fp64 view of stored weights; experts are widened on first use and kept."""
+    """fp64 view of stored weights (fp32, bf16 bit patterns, or group-quantised
+    bytes); experts are widened on first use and kept."""
 
     def __init__(self, gates: np.ndarray, expert_source: Callable[[int, int], np.ndarray],
                  d_model: int, d_ff: int, dtype: str, keep: bool = True):
@@ -32,15 +33,19 @@ class Model:
         self._gates: Dict[int, np.ndarray] = {}
 
     def gate(self, l: int) -> np.ndarray:
+        # the gate of a group-quantised model stays bf16
         if l not in self._gates:
-            self._gates[l] = moe.to_f64(self.gates[l], self.dtype)
+            self._gates[l] = moe.to_f64(self.gates[l], "bf16" if self.dtype == "q2g16" else self.dtype)
         return self._gates[l]
 
     def expert(self, l: int, e: int):
         key = (l, e)
         if key in self._experts:
             return self._experts[key]
-        w = moe.split_expert(moe.to_f64(self._src(l, e), self.dtype), self.d, self.d_ff)
+        if self.dtype == "q2g16":
+            w = quant.split_expert(self._src(l, e), self.d, self.d_ff)
+        else:
+            w = moe.split_expert(moe.to_f64(self._src(l, e), self.dtype), self.d, self.d_ff)
         if self._keep:
             self._experts[key] = w
         return w

@@ -22,6 +22,16 @@ Expert storage layout (host store and HBM slots alike): per expert the three
 matrices W1 [d_ff x d], W3 [d_ff x d] and W2 [d x d_ff], each row-major
 (out x in), stored back to back as W1 | W3 | W2.  The host store is
 [layers][experts][expert bytes]; the gate tensor is [layers][experts][d].
+
+Group-quantised storage ("q2g16", the paper's expert setting of Sec. 5.1:
+2-bit codes, groups of 16, compressed zero points): each matrix [rows x cols]
+becomes three planes, back to back:
+  codes  [rows][cols / 4] uint8, column c at bits 2 (c % 4) of byte c / 4;
+  scales [rows][cols / 16] fp16, one per group of 16 consecutive columns;
+  zeros  [rows][cols / 16] uint8, zero point = code / 64.
+The stored weight is (q - zero) * scale.  The codes come from a plain
+round-to-nearest min/max quantiser of the fp32 draw (HQQ's own optimiser needs
+real weights and is not reproduced); the gate stays bf16.
 """
 from __future__ import annotations
 
@@ -39,6 +49,13 @@ TAG_GATE, TAG_W1, TAG_W3, TAG_W2, TAG_DIR, TAG_CHAIN, TAG_NOISE = range(7)
 WEIGHT_STD = 0.02
 _CHUNK = 1 << 22  # elements generated per call, bounds temporary memory
 
+# group-quantised storage: 16 weights per group, 2-bit codes, fp16 scale,
+# 8-bit zero code (zero point = code / Q_ZERO_STEPS); 2 + 16/16 + 8/16 bits
+# = 3.5 bits per weight, i.e. 7 bytes per 16 weights
+Q_GROUP = 16
+Q_ZERO_STEPS = 64
+Q_BITS_PER_WEIGHT_X16 = 7
+
 
 @dataclasses.dataclass(frozen=True)
 class Config:
@@ -49,7 +66,7 @@ class Config:
     top_k: int
     d_model: int
     d_ff: int
-    dtype: str            # "f32" or "bf16" (storage type of gates and experts)
+    dtype: str            # "f32", "bf16" or "q2g16" (storage type of the experts)
     tokens: int           # batch-1 decode tokens
     slots: tuple          # cache slots per layer to run
     policies: tuple       # ("lru", "lfu") subset
@@ -59,8 +76,9 @@ class Config:
     prefill_tokens: int = 0
 
     @property
-    def elem_bytes(self) -> int:
-        return 4 if self.dtype == "f32" else 2
+    def gate_dtype(self) -> str:
+        """Storage type of the gate: fp32 for the fp32 stack, bf16 otherwise."""
+        return "f32" if self.dtype == "f32" else "bf16"
 
     @property
     def matrix_elems(self) -> int:
@@ -71,8 +89,24 @@ class Config:
         return 3 * self.matrix_elems
 
     @property
+    def matrix_bytes(self) -> int:
+        """Stored bytes of one expert matrix."""
+        if self.dtype == "q2g16":
+            return self.matrix_elems * Q_BITS_PER_WEIGHT_X16 // 16
+        return self.matrix_elems * (4 if self.dtype == "f32" else 2)
+
+    @property
     def expert_bytes(self) -> int:
-        return self.expert_elems * self.elem_bytes
+        return 3 * self.matrix_bytes
+
+    @property
+    def storage_dtype(self):
+        """numpy type an expert is viewed as: fp32 values, bf16 bit patterns or bytes."""
+        return {"f32": np.float32, "bf16": np.uint16, "q2g16": np.uint8}[self.dtype]
+
+    @property
+    def expert_storage_len(self) -> int:
+        return self.expert_bytes // np.dtype(self.storage_dtype).itemsize
 
     @property
     def alpha(self) -> float:
@@ -101,6 +135,13 @@ CONFIGS = {
     # 256 decode tokens; 16 slots, LFU + prefetch
     "fine-grained": Config("fine-grained", 251105, 24, 64, 8, 2048, 1408, "bf16", 256,
                            (16,), ("lfu",), 1.2, 0.6, prefetch_max=2, prefill_tokens=4096),
+    # group-quantised experts (2-bit codes, groups of 16, compressed zeros)
+    "tiny-q2": Config("tiny-q2", 251106, 2, 8, 2, 512, 1024, "q2g16", 64,
+                      (4,), ("lru", "lfu"), 1.1, 0.6),
+    "mixtral-layer-q2": Config("mixtral-layer-q2", 251107, 1, 8, 2, 4096, 14336, "q2g16",
+                               256, (4,), ("lru", "lfu"), 1.1, 0.6),
+    "mixtral-stack-q2": Config("mixtral-stack-q2", 251108, 32, 8, 2, 4096, 14336, "q2g16",
+                               128, (4,), ("lfu",), 1.1, 0.6, prefetch_max=2),
 }
 
 
@@ -116,38 +157,87 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
 
 
 def _storage_dtype(cfg: Config):
-    return np.float32 if cfg.dtype == "f32" else np.uint16
+    return cfg.storage_dtype
 
 
-def _draw_into(rng: np.random.Generator, out: np.ndarray, cfg: Config) -> None:
-    """Fill flat `out` (storage dtype) with N(0, 0.02^2) drawn in fp32."""
+def _draw_into(rng: np.random.Generator, out: np.ndarray, dtype: str) -> None:
+    """Fill flat `out` with N(0, 0.02^2) drawn in fp32, stored as `dtype`
+    ('f32' values or 'bf16' bit patterns)."""
     n = out.size
     std = np.float32(WEIGHT_STD)
     for i in range(0, n, _CHUNK):
         m = min(_CHUNK, n - i)
         v = rng.standard_normal(m, dtype=np.float32)
         v *= std
-        out[i:i + m] = v if cfg.dtype == "f32" else f32_to_bf16_bits(v)
+        out[i:i + m] = v if dtype == "f32" else f32_to_bf16_bits(v)
+
+
+def quantize_q2g16(w: np.ndarray):
+    """Round-to-nearest 2-bit quantisation of fp32 rows in groups of 16
+    consecutive columns: scale = (max - min) / 3 rounded to fp16, zero code =
+    round(-min / scale * 64) clipped to [0, 255], code = round(w / scale +
+    zero) clipped to [0, 3].  Returns (packed codes [rows][cols/4] uint8,
+    scales [rows][cols/16] fp16, zero codes [rows][cols/16] uint8)."""
+    rows, cols = w.shape
+    g = np.asarray(w, np.float32).reshape(rows, cols // Q_GROUP, Q_GROUP)
+    lo, hi = g.min(axis=2), g.max(axis=2)
+    s = (hi - lo) / np.float32(3)
+    s16 = np.where(s > 0, s, np.float32(1)).astype(np.float16)
+    s16 = np.where(s16 > 0, s16, np.float16(2.0 ** -24))  # keep every scale positive
+    sf = s16.astype(np.float32)
+    zc = np.clip(np.rint(-lo / sf * np.float32(Q_ZERO_STEPS)), 0, 255).astype(np.uint8)
+    z = zc.astype(np.float32) / np.float32(Q_ZERO_STEPS)
+    q = np.clip(np.rint(g / sf[..., None] + z[..., None]), 0, 3).astype(np.uint8).reshape(rows, cols // 4, 4)
+    packed = (q[..., 0] | (q[..., 1] << 2) | (q[..., 2] << 4) | (q[..., 3] << 6)).astype(np.uint8)
+    return packed, s16, zc
+
+
+def q2_planes(buf: np.ndarray, rows: int, cols: int):
+    """Views (codes, scales, zeros) of one stored q2g16 matrix in byte buffer `buf`."""
+    n = rows * cols
+    codes = buf[:n // 4].reshape(rows, cols // 4)
+    scales = buf[n // 4:n // 4 + n // 8].view(np.float16).reshape(rows, cols // Q_GROUP)
+    zeros = buf[n // 4 + n // 8:n // 4 + n // 8 + n // 16].reshape(rows, cols // Q_GROUP)
+    return codes, scales, zeros
+
+
+def _draw_quantized(rng: np.random.Generator, out: np.ndarray, rows: int, cols: int) -> None:
+    """Draw a [rows x cols] fp32 matrix (the same stream as the other storage
+    types) and store it group-quantised into byte buffer `out`."""
+    codes, scales, zeros = q2_planes(out, rows, cols)
+    std = np.float32(WEIGHT_STD)
+    step = max(1, _CHUNK // cols)
+    for r in range(0, rows, step):
+        m = min(step, rows - r)
+        v = rng.standard_normal(m * cols, dtype=np.float32)
+        v *= std
+        codes[r:r + m], scales[r:r + m], zeros[r:r + m] = quantize_q2g16(v.reshape(m, cols))
 
 
 def gate_weights(cfg: Config) -> np.ndarray:
-    """Gate tensor [layers][experts][d_model] in the storage dtype."""
-    g = np.empty((cfg.layers, cfg.experts, cfg.d_model), dtype=_storage_dtype(cfg))
+    """Gate tensor [layers][experts][d_model] in the gate's storage dtype."""
+    g = np.empty((cfg.layers, cfg.experts, cfg.d_model),
+                 dtype=np.float32 if cfg.gate_dtype == "f32" else np.uint16)
     for l in range(cfg.layers):
-        _draw_into(_rng(cfg, TAG_GATE, l), g[l].reshape(-1), cfg)
+        _draw_into(_rng(cfg, TAG_GATE, l), g[l].reshape(-1), cfg.gate_dtype)
     return g
 
 
 def fill_expert(cfg: Config, layer: int, expert: int, out: np.ndarray) -> None:
     """Write expert (layer, expert) as W1 | W3 | W2 into flat `out` (storage dtype)."""
-    m = cfg.matrix_elems
-    assert out.size == 3 * m
+    assert out.size == cfg.expert_storage_len
+    shapes = ((cfg.d_ff, cfg.d_model), (cfg.d_ff, cfg.d_model), (cfg.d_model, cfg.d_ff))
+    n = out.size // 3
     for j, tag in enumerate((TAG_W1, TAG_W3, TAG_W2)):
-        _draw_into(_rng(cfg, tag, layer, expert), out[j * m:(j + 1) * m], cfg)
+        part = out[j * n:(j + 1) * n]
+        if cfg.dtype == "q2g16":
+            _draw_quantized(_rng(cfg, tag, layer, expert), part, *shapes[j])
+        else:
+            _draw_into(_rng(cfg, tag, layer, expert), part, cfg.dtype)
 
 
 def expert_weights(cfg: Config, layer: int, expert: int) -> np.ndarray:
-    out = np.empty(cfg.expert_elems, dtype=_storage_dtype(cfg))
+    out = np.empty(cfg.expert_storage_len, dtype=_storage_dtype(cfg))
     fill_expert(cfg, layer, expert, out)
     return out
 
@@ -159,7 +249,7 @@ def fill_host_store(cfg: Config, out: np.ndarray, workers: Optional[int] = None,
     `out` may be a view of pinned host memory; it is written in place.
     `layers` restricts the fill to a subset of layers (offsets are unchanged).
     """
-    view = out.view(_storage_dtype(cfg)).reshape(cfg.layers, cfg.experts, cfg.expert_elems)
+    view = out.view(_storage_dtype(cfg)).reshape(cfg.layers, cfg.experts, cfg.expert_storage_len)
     todo = [(l, e) for l in (layers if layers is not None else range(cfg.layers))
             for e in range(cfg.experts)]
     if workers is None:
