@@ -50,6 +50,13 @@ DESCRIPTIONS = {
                               "next-layer speculative prefetch of up to 2 experts",
     "fine-grained": "fine-grained: 24 MoE layers, 64 experts, top-8, d_model 2048, d_ff 1408, bf16; "
                     "4096-token batched prefill then batch-1 decode; 16 slots, LFU + prefetch 2, Zipf(1.2)",
+    "tiny-q2": "tiny-q2: 2 MoE layers, 8 experts, top-2, d_model 512, d_ff 1024, 2-bit group-16 experts, "
+               "64 batch-1 decode tokens, 4 slots",
+    "mixtral-layer-q2": "mixtral-layer-q2: the Mixtral-shaped layer with experts group-quantised as in the "
+                        "paper's measured model (2-bit codes, groups of 16, fp16 scales, 8-bit zero codes: "
+                        "77 MB per expert), 256 batch-1 decode tokens, 4 HBM slots, Zipf(1.1)+Markov(0.6)",
+    "mixtral-stack-q2": "mixtral-stack-q2: 32 Mixtral-shaped layers, 2-bit group-16 experts (19.7 GB in "
+                        "pinned host memory), 128 batch-1 decode tokens, 4 slots, LFU + next-layer prefetch 2",
 }
 
 
@@ -214,8 +221,10 @@ def main():
     # (policy, slots, speculate): the first entry is the timed headline run
     runs = [("lfu", primary_slots, cfg.prefetch_max > 0)]
     if not args.lfu_only:
-        if args.workload in ("mixtral-layer", "tiny-stack"):
+        if args.workload in ("mixtral-layer", "tiny-stack", "mixtral-layer-q2", "tiny-q2"):
             runs.append(("lru", primary_slots, False))
+        elif args.workload == "mixtral-stack-q2":
+            runs.append(("lfu", 4, False))
         elif args.workload == "mixtral-stack":
             runs += [("lru", 4, False)] + [(p, s, False) for s in (2, 6) for p in ("lru", "lfu")]
         elif args.workload == "mixtral-stack-prefetch":
@@ -253,12 +262,12 @@ def main():
         moe.close()
 
     head = results[0]
-    K, d, dff, eb = cfg.top_k, cfg.d_model, cfg.d_ff, cfg.elem_bytes
+    K, d, dff, mb = cfg.top_k, cfg.d_model, cfg.d_ff, cfg.matrix_bytes
     tim = head["timing"]
     # algorithmic bytes per launch: the selected experts' weights plus the
     # activation vectors the kernel reads and writes
-    up_bytes = K * 2 * d * dff * eb + d * 4 + K * dff * 4
-    down_bytes = K * d * dff * eb + K * dff * 4 + d * 4
+    up_bytes = K * 2 * mb + d * 4 + K * dff * 4
+    down_bytes = K * mb + K * dff * 4 + d * 4
     up_ms = tim["ffn_up_ms"] / tim["ffn_up_n"]
     down_ms = tim["ffn_down_ms"] / tim["ffn_down_n"]
     up_gbps = up_bytes / (up_ms * 1e-3) / 1e9

@@ -44,7 +44,19 @@ extern "C" {
 typedef struct moe_cache moe_cache_t; /* opaque, library-owned */
 
 enum { MOE_POLICY_LRU = 0, MOE_POLICY_LFU = 1 };
-enum { MOE_DTYPE_F32 = 0, MOE_DTYPE_BF16 = 1 };
+enum {
+  MOE_DTYPE_F32 = 0,  /* fp32 gates and experts                                   */
+  MOE_DTYPE_BF16 = 1, /* bf16 gates and experts                                   */
+  MOE_DTYPE_Q2G16 = 2 /* bf16 gates; experts group-quantised as in the paper's
+                         measured model (Sec. 5.1: 2-bit codes, groups of 16,
+                         compressed zero points).  Each matrix [rows x cols] is
+                         three planes back to back: codes [rows][cols/4] bytes
+                         (column c in bits 2*(c%4) of byte c/4), fp16 scales
+                         [rows][cols/16], uint8 zero codes [rows][cols/16]
+                         (zero point = code/64); weight = (q - zero) * scale.
+                         Requires d_model and d_ff multiples of 64 and
+                         d_model <= 8192; decode only (no batched prefill).  */
+};
 enum { MOE_OK = 0, MOE_ERR_ARG = -1, MOE_ERR_STATE = -2, MOE_ERR_HIP = -3, MOE_ERR_NOMEM = -4 };
 /* flags of moe_decode_layer */
 enum { MOE_PREFETCH_NEXT = 1 };

@@ -16,14 +16,14 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_lib", "libmoe_offload.so")
 
 MOE_POLICY_LRU, MOE_POLICY_LFU = 0, 1
-MOE_DTYPE_F32, MOE_DTYPE_BF16 = 0, 1
+MOE_DTYPE_F32, MOE_DTYPE_BF16, MOE_DTYPE_Q2G16 = 0, 1, 2
 MOE_OK, MOE_ERR_ARG, MOE_ERR_STATE, MOE_ERR_HIP, MOE_ERR_NOMEM = 0, -1, -2, -3, -4
 MOE_PREFETCH_NEXT = 1
 MOE_FETCH_KERNEL, MOE_FETCH_DMA, MOE_FETCH_SPLIT = 0, 1, 2
 MOE_MAX_EXPERTS, MOE_MAX_TOPK = 64, 16
 
 POLICIES = {"lru": MOE_POLICY_LRU, "lfu": MOE_POLICY_LFU}
-DTYPES = {"f32": MOE_DTYPE_F32, "bf16": MOE_DTYPE_BF16}
+DTYPES = {"f32": MOE_DTYPE_F32, "bf16": MOE_DTYPE_BF16, "q2g16": MOE_DTYPE_Q2G16}
 
 
 class MoeError(RuntimeError):

@@ -156,6 +156,10 @@ hipError_t launch_ffn_up(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_down(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, const Launch &l);
 int ffn_down_chunks(int K, int d_ff, int dtype);
+// group-quantised experts (dtype 2)
+hipError_t launch_ffnq_up(const FfnArgs &a, const Launch &l);
+hipError_t launch_ffnq_down(const FfnArgs &a, const Launch &l);
+int ffnq_down_chunks(int K, int d_ff);
 hipError_t launch_prefill_gate(const PrefillArgs &a, const Launch &l);
 hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l);
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,

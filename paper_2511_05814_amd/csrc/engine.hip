@@ -223,6 +223,16 @@ static int check_ready(const moe_cache *c) {
   return MOE_OK;
 }
 
+// Stored bytes of one expert (W1 | W3 | W2).
+static uint64_t expert_bytes(const moe_model_desc *d) {
+  const uint64_t n = (uint64_t)d->d_model * d->d_ff;
+  if (d->dtype == MOE_DTYPE_Q2G16) return 3 * (n / 16 * 7);
+  return 3 * n * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
+}
+
+// Element type of the gate: fp32 for fp32 models, bf16 otherwise (router dtype code).
+static int gate_dtype(int dtype) { return dtype == MOE_DTYPE_F32 ? 0 : 1; }
+
 static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
   if (!c || !d) return fail(MOE_ERR_ARG, "NULL handle or description");
   if (d->d_model < 8 || d->d_model % 8 || d->d_model > 16384)
@@ -231,7 +241,10 @@ static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
   if (d->top_k < 1 || d->top_k > MOE_MAX_TOPK || d->top_k > c->E)
     return fail(MOE_ERR_ARG, "top_k must be in [1, min(experts, %d)]", MOE_MAX_TOPK);
   if (c->S < d->top_k) return fail(MOE_ERR_ARG, "slots (%d) < top_k (%d)", c->S, d->top_k);
-  if (d->dtype != MOE_DTYPE_F32 && d->dtype != MOE_DTYPE_BF16) return fail(MOE_ERR_ARG, "bad dtype");
+  if (d->dtype != MOE_DTYPE_F32 && d->dtype != MOE_DTYPE_BF16 && d->dtype != MOE_DTYPE_Q2G16)
+    return fail(MOE_ERR_ARG, "bad dtype");
+  if (d->dtype == MOE_DTYPE_Q2G16 && (d->d_model % 64 || d->d_ff % 64 || d->d_model > 8192))
+    return fail(MOE_ERR_ARG, "group-quantised experts need d_model and d_ff multiples of 64 and d_model <= 8192");
   if (d->prefetch_max < 0 || d->prefetch_max > d->top_k)
     return fail(MOE_ERR_ARG, "prefetch_max must be in [0, top_k]");
   if (d->fetch_mode != MOE_FETCH_KERNEL && d->fetch_mode != MOE_FETCH_DMA && d->fetch_mode != MOE_FETCH_SPLIT)
@@ -261,7 +274,7 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.err = take(256);
   l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff, d->dtype) * d->d_model);
-  const uint64_t B = 3ull * d->d_model * d->d_ff * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
+  const uint64_t B = expert_bytes(d);
   l.prefill = take(prefill_layout(d->top_k, d->d_model, d->d_ff, c->E, c->S, d->max_prefill_tokens, B).total);
   l.total = off;
   return l;
@@ -310,7 +323,7 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
     return fail(MOE_ERR_ARG, "workspace too small: %zu < %zu bytes", d->workspace_bytes, lay.total);
 
   // per-layer host bases (one contiguous store, or the caller's per-layer table)
-  const uint64_t B = 3ull * d->d_model * d->d_ff * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
+  const uint64_t B = expert_bytes(d);
   std::vector<const uint8_t *> hl(c->L), dl(c->L, nullptr);
   for (int l = 0; l < c->L; ++l) {
     hl[l] = d->host_layers ? static_cast<const uint8_t *>(d->host_layers[l])
@@ -339,7 +352,7 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->pmax = d->prefetch_max;
   c->fetch_mode = d->fetch_mode;
   c->max_T = d->max_prefill_tokens;
-  c->B = 3ull * d->d_model * d->d_ff * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
+  c->B = expert_bytes(d);
   c->cs = static_cast<hipStream_t>(d->compute_stream);
   c->xs = d->copy_stream ? static_cast<hipStream_t>(d->copy_stream) : c->cs;
   c->one_stream = (c->xs == c->cs);
@@ -501,7 +514,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.S = c->S;
   a.K = c->K;
   a.d = c->d;
-  a.dtype = c->dtype;
+  a.dtype = gate_dtype(c->dtype);
   a.policy = c->policy;
   a.demand = demand;
   a.spec_layer = spec_layer;

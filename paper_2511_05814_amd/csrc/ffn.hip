@@ -305,15 +305,18 @@ hipError_t launch_down_t(const FfnArgs &a, const Launch &l) {
 }  // namespace
 
 int ffn_down_chunks(int K, int d_ff, int dtype) {
+  if (dtype == 2) return ffnq_down_chunks(K, d_ff);
   const int ch = down_shape(d_ff, dtype).steps * kWave * (dtype == 1 ? 8 : 4);
   return K * ((d_ff + ch - 1) / ch);
 }
 
 hipError_t launch_ffn_up(const FfnArgs &a, int dtype, const Launch &l) {
+  if (dtype == 2) return launch_ffnq_up(a, l);
   return dtype == 1 ? launch_up_t<1>(a, l) : launch_up_t<0>(a, l);
 }
 
 hipError_t launch_ffn_down(const FfnArgs &a, int dtype, const Launch &l) {
+  if (dtype == 2) return launch_ffnq_down(a, l);
   return dtype == 1 ? launch_down_t<1>(a, l) : launch_down_t<0>(a, l);
 }
 

@@ -63,12 +63,12 @@ class HostStore:
         import os
         from concurrent.futures import ThreadPoolExecutor
         cfg = self.cfg
-        sdt = np.float32 if cfg.dtype == "f32" else np.uint16
+        sdt = cfg.storage_dtype
         todo = [(l, e) for l in range(self.distinct) for e in range(cfg.experts)]
 
         def one(le):
             l, e = le
-            view = self.arrays[l].view(sdt).reshape(cfg.experts, cfg.expert_elems)
+            view = self.arrays[l].view(sdt).reshape(cfg.experts, cfg.expert_storage_len)
             wl.fill_expert(cfg, l, e, view[e])
 
         workers = workers or max(1, min(16, os.cpu_count() or 1))
@@ -84,7 +84,7 @@ class HostStore:
         cfg = self.cfg
         off = expert * cfg.expert_bytes
         raw = self.arrays[self.layer_src[layer]][off:off + cfg.expert_bytes]
-        return raw.view(np.float32 if cfg.dtype == "f32" else np.uint16)
+        return raw.view(cfg.storage_dtype)
 
     def layer_array(self, layer: int) -> np.ndarray:
         return self.arrays[self.layer_src[layer]]

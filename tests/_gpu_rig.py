@@ -11,7 +11,9 @@ def _say(*a):
 
 
 def _tol(cfg):
-    return 1e-5 if cfg.dtype == "f32" else 2e-2
+    # fp32 and group-quantised weights are exact fp32 numbers on both sides;
+    # bf16 uses the bound stated for bf16 experts
+    return 2e-2 if cfg.dtype == "bf16" else 1e-5
 
 
 class Rig:

@@ -80,6 +80,16 @@ def test_workspace_query_and_bind_validation_without_gpu():
     b.moe_cache_destroy(0)  # NULL-safe
 
 
+def test_group_quantised_shape_rules():
+    h = b.moe_cache_create(2, 8, 4, b.MOE_POLICY_LFU)
+    try:
+        assert b.moe_cache_workspace_bytes(h, _desc(dtype=b.MOE_DTYPE_Q2G16)) > 0
+        for bad in (dict(d_model=72), dict(d_ff=200), dict(d_model=8256, d_ff=64), dict(max_prefill_tokens=16)):
+            assert b.moe_cache_workspace_bytes(h, _desc(dtype=b.MOE_DTYPE_Q2G16, **bad)) == 0, bad
+    finally:
+        b.moe_cache_destroy(h)
+
+
 def test_slots_below_top_k_rejected():
     h = b.moe_cache_create(1, 8, 2, b.MOE_POLICY_LRU)
     try:
