@@ -16,7 +16,8 @@
 // 64 consecutive columns (four groups) per step: 16 bytes of codes, 8 bytes
 // of scales and 4 bytes of zero codes.  Per group the dot product is taken as
 // scale * (sum_i q_i x_i - zero * sum_i x_i) with the group sums of x formed
-// once, so a weight costs a field extract, a conversion and an FMA.
+// once; four codes are masked out of a word at a time and converted byte by
+// byte, so a weight costs about 2.4 vector instructions.
 //
 // Loads are issued from addresses clamped into the matrix (rows past the end
 // read the last row, columns past the end the last unit) so that none sits
@@ -31,8 +32,9 @@ constexpr int kThreads = 256;
 constexpr int kWpb = kThreads / kWave;
 constexpr int kLaneCols = 64;                 // four groups of 16
 constexpr int kStepCols = kWave * kLaneCols;  // 4096 columns per wave step
-constexpr int kQUpRows = 4;                   // rows of W1 and of W3 per wave
-constexpr int kQDownRows = 16;                // rows of W2 per wave
+constexpr int kQUpRows = 2;                   // rows of W1 and of W3 per wave and step
+constexpr int kUpWaves = 256 * 4 * 3;         // waves of one up launch: 3 per SIMD
+constexpr int kQDownRows = 8;                 // rows of W2 per wave
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
@@ -86,6 +88,18 @@ __device__ __forceinline__ void load_x(const float *p, int c, int n, float scale
   }
 }
 
+// Byte j of a word as a float (v_cvt_f32_ubyte<j>).  Written out because the
+// compiler otherwise extracts each 2-bit field on its own before converting.
+template <int J>
+__device__ __forceinline__ float byte_to_f32(uint32_t m) {
+  float r;
+  if constexpr (J == 0) asm("v_cvt_f32_ubyte0 %0, %1" : "=v"(r) : "v"(m));
+  else if constexpr (J == 1) asm("v_cvt_f32_ubyte1 %0, %1" : "=v"(r) : "v"(m));
+  else if constexpr (J == 2) asm("v_cvt_f32_ubyte2 %0, %1" : "=v"(r) : "v"(m));
+  else asm("v_cvt_f32_ubyte3 %0, %1" : "=v"(r) : "v"(m));
+  return r;
+}
+
 // sum over the unit's 64 columns of w_c x_c
 __device__ __forceinline__ float unit_dot(const QUnit &u, const float *x, const float *xs) {
   float out = 0.0f;
@@ -97,8 +111,10 @@ __device__ __forceinline__ float unit_dot(const QUnit &u, const float *x, const 
     for (int t = 0; t < 4; ++t) {
       // byte j of m holds the code of column 4 j + t
       const uint32_t m = (w >> (2 * t)) & 0x03030303u;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc = fmaf((float)((m >> (8 * j)) & 0xFFu), x[16 * g + 4 * j + t], acc);
+      acc = fmaf(byte_to_f32<0>(m), x[16 * g + t], acc);
+      acc = fmaf(byte_to_f32<1>(m), x[16 * g + 4 + t], acc);
+      acc = fmaf(byte_to_f32<2>(m), x[16 * g + 8 + t], acc);
+      acc = fmaf(byte_to_f32<3>(m), x[16 * g + 12 + t], acc);
     }
     const uint32_t sb = (u.s[g >> 1] >> (16 * (g & 1))) & 0xFFFFu;
     const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)sb);
@@ -110,48 +126,76 @@ __device__ __forceinline__ float unit_dot(const QUnit &u, const float *x, const 
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }
 
-// act_r = SiLU(W1_r x) * (W3_r x), x = h / rms(h); d <= STEPS * 4096
+// act_r = SiLU(W1_r x) * (W3_r x), x = h / rms(h); d <= STEPS * 4096.
+// G workgroups per rank; each wave walks row groups of RPW rows with a stride
+// of G * 4 groups, loading the next group's weights before it works on the
+// current one, so memory latency hides behind the dequantising arithmetic.
 template <int STEPS, int RPW>
-__global__ __launch_bounds__(kThreads) void ffnq_up_kernel(FfnArgs a) {
-  const int bpr = (a.d_ff + kWpb * RPW - 1) / (kWpb * RPW);
-  const int rank = blockIdx.x / bpr;
-  const int rb = blockIdx.x - rank * bpr;
+__global__ __launch_bounds__(kThreads) void ffnq_up_kernel(FfnArgs a, int G) {
+  const int rank = blockIdx.x / G;
+  const int gb = blockIdx.x - rank * G;
   if (rank >= a.route->k) return;
   const int hit = a.route->hit[rank];
   if ((a.phase == 1 && !hit) || (a.phase == 2 && hit)) return;
   const int slot = a.route->slot[rank];
   if (slot < 0 || slot >= a.S) return;
   const int d = a.d, d_ff = a.d_ff;
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const float inv_r = a.route->inv_r;
-
-  float x[STEPS][kLaneCols], xs[STEPS][4];
-#pragma unroll
-  for (int s = 0; s < STEPS; ++s) load_x(a.h, s * kStepCols + lane * kLaneCols, d, inv_r, x[s], xs[s]);
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);  // wave-uniform
+  const int nrg = (d_ff + RPW - 1) / RPW;
+  const int stride = G * kWpb;
+  int rg = gb * kWpb + wave;
+  if (rg >= nrg) return;
 
   const uint8_t *base = a.arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes;
   const size_t mbytes = (size_t)d_ff * d / 16 * 7;
   const QMat w1 = qmat(base, d_ff, d), w3 = qmat(base + mbytes, d_ff, d);
-  const int row0 = rb * kWpb * RPW + wave * RPW;
-  QUnit u1[RPW][STEPS], u3[RPW][STEPS];
+  QUnit c1[RPW][STEPS], c3[RPW][STEPS];
 #pragma unroll
   for (int q = 0; q < RPW; ++q)
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
-      u1[q][s] = load_unit(w1, row0 + q, s * kStepCols + lane * kLaneCols);
-      u3[q][s] = load_unit(w3, row0 + q, s * kStepCols + lane * kLaneCols);
+      c1[q][s] = load_unit(w1, rg * RPW + q, s * kStepCols + lane * kLaneCols);
+      c3[q][s] = load_unit(w3, rg * RPW + q, s * kStepCols + lane * kLaneCols);
+    }
+  float x[STEPS][kLaneCols], xs[STEPS][4];
+#pragma unroll
+  for (int s = 0; s < STEPS; ++s) load_x(a.h, s * kStepCols + lane * kLaneCols, d, a.route->inv_r, x[s], xs[s]);
+
+  for (; rg < nrg; rg += stride) {
+    QUnit n1[RPW][STEPS], n3[RPW][STEPS];
+    const bool more = rg + stride < nrg;  // same for the whole wave
+    if (more) {
+#pragma unroll
+      for (int q = 0; q < RPW; ++q)
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s) {
+          n1[q][s] = load_unit(w1, (rg + stride) * RPW + q, s * kStepCols + lane * kLaneCols);
+          n3[q][s] = load_unit(w3, (rg + stride) * RPW + q, s * kStepCols + lane * kLaneCols);
+        }
     }
 #pragma unroll
-  for (int q = 0; q < RPW; ++q) {
-    float a1 = 0.0f, a3 = 0.0f;
+    for (int q = 0; q < RPW; ++q) {
+      float a1 = 0.0f, a3 = 0.0f;
 #pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      a1 += unit_dot(u1[q][s], x[s], xs[s]);
-      a3 += unit_dot(u3[q][s], x[s], xs[s]);
+      for (int s = 0; s < STEPS; ++s) {
+        a1 += unit_dot(c1[q][s], x[s], xs[s]);
+        a3 += unit_dot(c3[q][s], x[s], xs[s]);
+      }
+      a1 = wave_sum(a1);
+      a3 = wave_sum(a3);
+      const int row = rg * RPW + q;
+      if (lane == 0 && row < d_ff) a.act[(size_t)rank * d_ff + row] = silu(a1) * a3;
     }
-    a1 = wave_sum(a1);
-    a3 = wave_sum(a3);
-    if (lane == 0 && row0 + q < d_ff) a.act[(size_t)rank * d_ff + row0 + q] = silu(a1) * a3;
+    if (more) {
+#pragma unroll
+      for (int q = 0; q < RPW; ++q)
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s) {
+          c1[q][s] = n1[q][s];
+          c3[q][s] = n3[q][s];
+        }
+    }
   }
 }
 
@@ -173,13 +217,13 @@ __global__ __launch_bounds__(kThreads) void ffnq_down_kernel(FfnArgs a) {
   const bool valid = rank < K && slot >= 0 && slot < a.S;
   float acc[RPW] = {};
   if (valid) {
-    float x[kLaneCols], xs[4];
-    load_x(a.act + (size_t)rank * d_ff, c0 + lane * kLaneCols, d_ff, a.route->g[rank], x, xs);
     const uint8_t *base = a.arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes;
     const QMat w2 = qmat(base + 2 * ((size_t)d_ff * d / 16 * 7), d, d_ff);
     QUnit u[RPW];
 #pragma unroll
     for (int q = 0; q < RPW; ++q) u[q] = load_unit(w2, row0 + q, c0 + lane * kLaneCols);
+    float x[kLaneCols], xs[4];
+    load_x(a.act + (size_t)rank * d_ff, c0 + lane * kLaneCols, d_ff, a.route->g[rank], x, xs);
 #pragma unroll
     for (int q = 0; q < RPW; ++q) acc[q] = unit_dot(u[q], x, xs);
   }
@@ -195,11 +239,14 @@ __global__ __launch_bounds__(kThreads) void ffnq_down_kernel(FfnArgs a) {
 int ffnq_down_chunks(int K, int d_ff) { return K * ((d_ff + kStepCols - 1) / kStepCols); }
 
 hipError_t launch_ffnq_up(const FfnArgs &a, const Launch &l) {
-  const dim3 grid(a.K * ((a.d_ff + kWpb * kQUpRows - 1) / (kWpb * kQUpRows)));
+  // about kUpWaves waves in total, at most one row group each
+  const int groups = (a.d_ff + kQUpRows - 1) / kQUpRows;
+  const int G = max(1, min((groups + kWpb - 1) / kWpb, kUpWaves / (kWpb * max(1, a.K))));
+  const dim3 grid(a.K * G);
   if (a.d <= kStepCols)
-    MOE_LAUNCH((ffnq_up_kernel<1, kQUpRows>), grid, dim3(kThreads), 0, l, a);
+    MOE_LAUNCH((ffnq_up_kernel<1, kQUpRows>), grid, dim3(kThreads), 0, l, a, G);
   else
-    MOE_LAUNCH((ffnq_up_kernel<2, kQUpRows>), grid, dim3(kThreads), 0, l, a);
+    MOE_LAUNCH((ffnq_up_kernel<2, kQUpRows>), grid, dim3(kThreads), 0, l, a, G);
   return hipGetLastError();
 }
 
