@@ -306,7 +306,7 @@ def main():
         "runs": summary,
         "ffn_hbm_gbps": round((up_bytes + down_bytes) / ((up_ms + down_ms) * 1e-3) / 1e9, 1),
         "roofline": {
-            "kernel": "ffn_up_kernel",
+            "kernel": "ffnq_up_kernel" if cfg.dtype == "q2g16" else "ffn_up_kernel",
             "bound": "hbm",
             "achieved": round(up_gbps, 1),
             "peak": HBM_PEAK_GBPS,
@@ -317,7 +317,8 @@ def main():
             "avg_launch_us": round(up_ms * 1e3, 2),
             "launches": tim["ffn_up_n"],
         },
-        "ffn_down": {"achieved_gbps": round(down_gbps, 1), "frac": round(down_gbps / HBM_PEAK_GBPS, 4),
+        "ffn_down": {"kernel": "ffnq_down_kernel" if cfg.dtype == "q2g16" else "ffn_down_kernel",
+                     "achieved_gbps": round(down_gbps, 1), "frac": round(down_gbps / HBM_PEAK_GBPS, 4),
                      "bytes_per_launch": down_bytes, "avg_launch_us": round(down_ms * 1e3, 2),
                      "reduce_avg_us": round(1e3 * tim["ffn_reduce_ms"] / max(1, tim["ffn_reduce_n"]), 2)},
         "link_roofline": {
