@@ -105,10 +105,11 @@ def pmc_traffic():
         return None
 
 
-def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0):
-    """n passes (reset, [prefill], decode all tokens); returns seconds of
-    decode, seconds of prefill, summed timing, summed per-layer statistics and
-    the trace of the last pass."""
+def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0, batch=1):
+    """n passes (reset, [prefill], decode all tokens, one at a time or
+    `batch` at a time); returns seconds of decode, seconds of prefill, summed
+    timing, summed per-layer statistics, the trace of the last pass and the
+    prefill's share of the fetched bytes."""
     dec = pre = 0.0
     tim = None
     stats = None
@@ -129,7 +130,10 @@ def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0):
             pre += time.perf_counter() - t0
             prefill_bytes += sum(s["bytes_fetched"] for s in moe.stats())
         t0 = time.perf_counter()
-        moe.decode(H[prefill_tokens:], flags=flags)
+        if batch > 1:
+            moe.decode_batched(H[prefill_tokens:], batch)
+        else:
+            moe.decode(H[prefill_tokens:], flags=flags)
         moe.sync()
         torch.cuda.synchronize()
         dec += time.perf_counter() - t0
@@ -186,6 +190,66 @@ def summarize(cfg, r):
     return out
 
 
+def batch_report(args, cfg, results, link):
+    """JSON line of a batched-decode run: tokens/s, pair hit rate, link bytes,
+    and the grouped GEMMs (which stream each routed expert's weights once per
+    batch: HBM-bound at small batches)."""
+    head = results[0]
+    tim, steps = head["timing"], head["steps"]
+    mb = cfg.matrix_bytes
+
+    def rates(r):
+        hits = sum(s["hits"] for s in r["stats"])
+        misses = sum(s["misses"] for s in r["stats"])
+        return {"tokens_per_s": round(r["steps"] * cfg.tokens / r["dec"], 3),
+                "pair_hit_rate": round(hits / max(1, hits + misses), 4),
+                "decode_bytes_fetched_per_step": sum(s["bytes_fetched"] for s in r["stats"]) // r["steps"]}
+
+    # experts each batch routed tokens to (one batch record per expert; its
+    # rank field holds the number of (token, rank) pairs), in the last pass
+    used = sum(1 for x in head["recs"] if x[0] == 2 and x[3] > 0)
+    up_bytes = used * 2 * mb
+    down_bytes = used * mb
+    up_s = tim["gemm_up_ms"] * 1e-3 / steps
+    down_s = tim["gemm_down_ms"] * 1e-3 / steps
+    up_gbps = up_bytes / up_s / 1e9 if up_s > 0 else None
+    fetched = rates(head)["decode_bytes_fetched_per_step"]
+    link_gbps = fetched / (head["dec"] / steps) / 1e9
+    return {
+        "metric": METRIC,
+        "value": rates(head)["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * head["dec"] / steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": DESCRIPTIONS[args.workload] + f"; batched decode, {args.batch} tokens per step",
+                   "weights_dtype": cfg.dtype, "policy": head["policy"], "slots": head["slots"],
+                   "batch": args.batch, "decode_tokens_per_step": cfg.tokens},
+        "runs": {f"{r['policy']}-s{r['slots']}": rates(r) for r in results},
+        "roofline": {
+            "kernel": "prefill_gemm_kernel<true>", "bound": "hbm",
+            "achieved": round(up_gbps, 1) if up_gbps else None, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(up_gbps / HBM_PEAK_GBPS, 4) if up_gbps else None, "traffic": None,
+            "bytes_per_launch": up_bytes // max(1, tim["gemm_up_n"] // steps),
+            "avg_launch_us": round(1e3 * tim["gemm_up_ms"] / max(1, tim["gemm_up_n"]), 2),
+            "launches": tim["gemm_up_n"],
+            "note": "weights of every routed expert (W1, W3) streamed once per batch",
+        },
+        "gemm_down": {"achieved_gbps": round(down_bytes / down_s / 1e9, 1) if down_s > 0 else None,
+                      "avg_launch_us": round(1e3 * tim["gemm_down_ms"] / max(1, tim["gemm_down_n"]), 2)},
+        "experts_per_batch_layer": round(used / max(1, (cfg.tokens // args.batch) * cfg.layers), 3),
+        "link": {"bytes_per_step": fetched, "achieved_over_decode_gbps": round(link_gbps, 2),
+                 "peak": round(link, 2), "frac": round(link_gbps / link, 4)},
+        "batch_layer_ms": round(tim["prefill_ms"] / max(1, tim["prefill_n"]), 3),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +266,8 @@ def main():
     ap.add_argument("--tokens", type=int, default=0,
                     help="decode only the first N tokens of the workload (profiling passes)")
     ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
+    ap.add_argument("--batch", type=int, default=1,
+                    help="decode B tokens per step through the batch path (bf16 experts; no speculation)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -218,9 +284,16 @@ def main():
         cfg = cfg.with_(tokens=min(args.tokens, cfg.tokens))
     fetch_mode = {"kernel": b.MOE_FETCH_KERNEL, "dma": b.MOE_FETCH_DMA, "split": b.MOE_FETCH_SPLIT}[args.fetch]
     primary_slots = 16 if cfg.experts == 64 else 4
+    if args.batch > 1 and cfg.dtype != "bf16":
+        sys.exit("batched decode runs on bf16 experts (the grouped GEMMs use bf16 matrix cores)")
+    if args.batch > 1 and cfg.prefill_tokens:
+        sys.exit("batched decode is measured on the workloads without a prefill phase")
     # (policy, slots, speculate): the first entry is the timed headline run
-    runs = [("lfu", primary_slots, cfg.prefetch_max > 0)]
-    if not args.lfu_only:
+    runs = [("lfu", primary_slots, cfg.prefetch_max > 0 and args.batch == 1)]
+    if args.batch > 1:
+        if not args.lfu_only:
+            runs.append(("lru", primary_slots, False))
+    elif not args.lfu_only:
         if args.workload in ("mixtral-layer", "tiny-stack", "mixtral-layer-q2", "tiny-q2"):
             runs.append(("lru", primary_slots, False))
         elif args.workload == "mixtral-stack-q2":
@@ -249,17 +322,22 @@ def main():
         flags = b.MOE_PREFETCH_NEXT if spec else 0
         moe = offload.OffloadedMoE(cfg, store, gates, slots, policy,
                                    prefetch_max=cfg.prefetch_max if spec else 0, fetch_mode=fetch_mode,
-                                   max_prefill_tokens=cfg.prefill_tokens)
+                                   max_prefill_tokens=max(cfg.prefill_tokens, args.batch if args.batch > 1 else 0))
         steps = args.steps if i == 0 else 1
         if i == 0 and args.warmup:
-            run_steps(torch, b, moe, H0, H, args.warmup, False, flags, cfg.prefill_tokens)
+            run_steps(torch, b, moe, H0, H, args.warmup, False, flags, cfg.prefill_tokens, args.batch)
         dec, pre, tim, st, recs, pbytes = run_steps(torch, b, moe, H0, H, steps, True, flags,
-                                                    cfg.prefill_tokens)
+                                                    cfg.prefill_tokens, args.batch)
         results.append(dict(policy=policy, slots=slots, flags=flags, steps=steps, dec=dec, pre=pre,
                             prefill_bytes=pbytes,
                             timing=tim, stats=st, recs=recs))
         log(policy, slots, "prefetch" if spec else "", f"{steps * cfg.tokens / dec:.2f} tok/s")
         moe.close()
+
+    if args.batch > 1:
+        print(json.dumps(batch_report(args, cfg, results, link)), flush=True)
+        store.close()
+        return
 
     head = results[0]
     K, d, dff, mb = cfg.top_k, cfg.d_model, cfg.d_ff, cfg.matrix_bytes

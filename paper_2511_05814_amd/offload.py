@@ -201,6 +201,14 @@ class OffloadedMoE:
             if snapshots is not None:
                 snapshots[self.L].copy_(H)
 
+    def decode_batched(self, H, batch: int):
+        """Decode tokens H [T][d] (fp32, device) in place, `batch` tokens at a
+        time: each group of tokens goes through all layers as one batch
+        (moe_prefill_layer: batched routing, the batch residency rule and the
+        grouped GEMMs), which is batched decode of `batch` sequences."""
+        for g in range(0, H.shape[0], batch):
+            self.prefill(H[g:g + batch])
+
     def sync(self):
         b.moe_cache_sync(self.handle)
 

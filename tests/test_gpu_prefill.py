@@ -86,7 +86,7 @@ def test_prefill_fine_grained_two_layers(policy):
 
 
 def test_prefill_ragged_shapes():
-    # d, d_ff not multiples of the 64 x 64 GEMM tile or the 32-deep k step;
+    # d, d_ff not multiples of the 128 x 128 GEMM tile or the 32-deep k step;
     # T not a multiple of anything; 5 experts, top-3, 3 slots
     cfg = wl.CONFIGS["tiny-stack"].with_(layers=2, experts=5, top_k=3, d_model=136, d_ff=200,
                                          dtype="bf16", tokens=4, prefill_tokens=37)
@@ -107,5 +107,45 @@ def test_prefill_rejects_bad_token_counts():
         with pytest.raises(b.MoeError) as e:
             b.moe_prefill_layer(moe.handle, 0, H.data_ptr(), T)
         assert e.value.code == b.MOE_ERR_ARG
+    moe.close()
+    rig.store.close()
+
+
+def test_batched_decode_mixtral_shape():
+    # batched decode through the batch path: three batches of 8 tokens through
+    # the Mixtral-shaped layer (d 4096, d_ff 14336), LRU, 4 slots; each batch
+    # must continue from the state the previous one left
+    cfg = wl.CONFIGS["mixtral-layer"].with_(tokens=24)
+    _say("batched decode mixtral-layer", cfg)
+    rig = Rig(cfg)
+    B, K = 8, cfg.top_k
+    moe = rig.cache(4, "lru", max_prefill_tokens=B)
+    h = wl.hidden_states(cfg, cfg.tokens)
+    H = torch.from_numpy(np.ascontiguousarray(h)).to("cuda")
+    caches = make_caches(1, cfg.experts, 4, "lru")
+    worst = 0.0
+    for g in range(0, cfg.tokens, B):
+        rows = H[g:g + B]
+        hin = rows.cpu().numpy().astype(np.float64)
+        with torch.cuda.stream(moe.compute):
+            b.moe_prefill_layer(moe.handle, 0, rows.data_ptr(), B)
+        moe.sync()
+        gids, gg, n = b.moe_cache_last_routing(moe.handle, B * K)
+        gids = np.array(gids).reshape(B, K)
+        hout = rows.cpu().numpy().astype(np.float64)
+        _, ids, gw, cert, _ = stack.prefill_layer(rig.model, 0, hin, K, None, with_ffn=False)
+        assert np.array_equal(ids[cert], gids[cert]), f"batch {g}: routing differs"
+        merged = np.where(cert[:, None], ids, gids)
+        want = caches[0].prefill(merged)
+        recs, _ = moe.trace_records()
+        got = [r for r in recs if r[0] == 2][-cfg.experts:]
+        assert got == [w.astuple() for w in want], f"batch {g}: batch records differ"
+        for t in range(B):
+            r = omoe.rms(hin[t])
+            y = omoe.moe_output(lambda e: rig.model.expert(0, e), merged[t], gw[t], hin[t] / r)
+            worst = max(worst, rel_l2(hout[t] - hin[t], y))
+        assert moe.state(0) == caches[0].state()
+    _say("batched decode worst y", worst)
+    assert worst <= 2e-2
     moe.close()
     rig.store.close()
