@@ -410,7 +410,7 @@ struct TileRows {
 };
 
 template <bool UP>
-__global__ __launch_bounds__(256) void prefill_gemm_kernel(const GemmTile *tiles, const GemmJob *jobs,
+__global__ __launch_bounds__(256, 2) void prefill_gemm_kernel(const GemmTile *tiles, const GemmJob *jobs,
                                                               const uint16_t *a_src, const int32_t *perm_tok,
                                                               void *out, int d, int d_ff) {
   constexpr int NB = UP ? 2 : 1;  // B matrices: W1 and W3, or W2
