@@ -168,8 +168,9 @@ hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob 
                                float *Y, int d, int d_ff, const Launch &l);
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
                                     int d, int K, const Launch &l);
-int prefill_tile_rows();  // GEMM output tile: rows (tokens) ...
-int prefill_tile_cols();  // ... and columns
+int prefill_tile_rows();       // GEMM output tile: rows (sorted pairs) ...
+int prefill_tile_cols_up();    // ... columns of act per up tile
+int prefill_tile_cols_down();  // ... columns of Y per down tile
 
 // ---------------------------------------------------------------------------
 // device helpers

@@ -730,9 +730,9 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       }
     }
   }
-  const int rows = prefill_tile_rows(), cols = prefill_tile_cols();
+  const int rows = prefill_tile_rows(), cols_up = prefill_tile_cols_up(), cols_down = prefill_tile_cols_down();
   int nt = 0;
-  auto add_tiles = [&](const std::vector<int> &group, int ncols, int &first, int &count) {
+  auto add_tiles = [&](const std::vector<int> &group, int ncols, int cols, int &first, int &count) {
     first = nt;
     for (int e : group)
       for (int m0 = 0; m0 < pl[e].n; m0 += rows)
@@ -742,12 +742,12 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   const size_t ngroups = batches.size() + 1;
   std::vector<int> up_first(ngroups), up_n(ngroups), dn_first(ngroups), dn_n(ngroups);
   std::vector<double> group_rows(ngroups, 0.0);
-  add_tiles(resident, c->dff, up_first[0], up_n[0]);
-  add_tiles(resident, c->d, dn_first[0], dn_n[0]);
+  add_tiles(resident, c->dff, cols_up, up_first[0], up_n[0]);
+  add_tiles(resident, c->d, cols_down, dn_first[0], dn_n[0]);
   for (int e : resident) group_rows[0] += pl[e].n;
   for (size_t bi = 0; bi < batches.size(); ++bi) {
-    add_tiles(batches[bi], c->dff, up_first[bi + 1], up_n[bi + 1]);
-    add_tiles(batches[bi], c->d, dn_first[bi + 1], dn_n[bi + 1]);
+    add_tiles(batches[bi], c->dff, cols_up, up_first[bi + 1], up_n[bi + 1]);
+    add_tiles(batches[bi], c->d, cols_down, dn_first[bi + 1], dn_n[bi + 1]);
     for (int e : batches[bi]) group_rows[bi + 1] += pl[e].n;
   }
   if (nt > p.tile_cap) {

@@ -398,21 +398,27 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row
   return r;
 }
 
-// 128 x 128 output tile per workgroup (four waves of 64 x 64,
-// 4 x 4 blocks of v_mfma_f32_16x16x32_bf16 each).  The next 32-deep K slice
-// is loaded from global memory into registers while the current one is
-// multiplied out of LDS; LDS is double-buffered so one barrier per step
-// suffices.  Every output accumulates its K slices in ascending order.
+// A workgroup takes a 128 x 128 output tile, against both W1 and W3 in the
+// up projection and against W2 in the down projection.  Four waves each own
+// 64 x 64 of it as 4 x 4 v_mfma_f32_16x16x32_bf16 tiles.  (A 128 x 256 down
+// tile streams W2 no faster in isolation and halves the workgroups of the
+// small per-batch launches.)  The next 32-deep K slice is loaded from global memory into
+// registers kGemmStages slices ahead of the one multiplied out of LDS; LDS
+// is double-buffered so one barrier per step suffices.  Every output
+// accumulates its K slices in ascending order.
 constexpr int kBM = 128, kBN = 128;
+constexpr int kGemmStages = 2;  // K slices loaded ahead of the one being multiplied
 
 struct TileRows {
   const uint16_t *p[2];  // this thread's two rows of the 128-row tile (or nullptr)
 };
 
-template <bool UP>
-__global__ __launch_bounds__(256, 2) void prefill_gemm_kernel(const GemmTile *tiles, const GemmJob *jobs,
-                                                              const uint16_t *a_src, const int32_t *perm_tok,
-                                                              void *out, int d, int d_ff) {
+template <bool UP, int P>
+__global__ __launch_bounds__(256, P <= 2 ? 2 : 1) void prefill_gemm_kernel(const GemmTile *tiles,
+                                                                           const GemmJob *jobs,
+                                                                           const uint16_t *a_src,
+                                                                           const int32_t *perm_tok, void *out,
+                                                                           int d, int d_ff) {
   constexpr int NB = UP ? 2 : 1;  // B matrices: W1 and W3, or W2
   __shared__ uint16_t As[2][kBM][kLdsK];
   __shared__ uint16_t Bs[2][NB][kBN][kLdsK];
@@ -440,24 +446,27 @@ __global__ __launch_bounds__(256, 2) void prefill_gemm_kernel(const GemmTile *ti
       br[b].p[h] = n < N ? w + (size_t)n * K : nullptr;
     }
   }
-  uint4 ra[2], rb[NB][2];
-  auto gload = [&](int k0) {
+  // K slices loaded ahead live in a ring of P register slots: slice t >= 1
+  // sits in slot (t - 1) % P until it is stored to LDS.
+  uint4 ra[P][2], rb[P][NB][2];
+  auto gload = [&](int slot, int k0) {
     const int k = k0 + q * 8;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      ra[h] = (ar.p[h] && k < K) ? *reinterpret_cast<const uint4 *>(ar.p[h] + k) : make_uint4(0, 0, 0, 0);
+      ra[slot][h] = (ar.p[h] && k < K) ? *reinterpret_cast<const uint4 *>(ar.p[h] + k) : make_uint4(0, 0, 0, 0);
 #pragma unroll
       for (int b = 0; b < NB; ++b)
-        rb[b][h] = (br[b].p[h] && k < K) ? *reinterpret_cast<const uint4 *>(br[b].p[h] + k)
-                                         : make_uint4(0, 0, 0, 0);
+        rb[slot][b][h] = (br[b].p[h] && k < K) ? *reinterpret_cast<const uint4 *>(br[b].p[h] + k)
+                                               : make_uint4(0, 0, 0, 0);
     }
   };
-  auto lstore = [&](int buf) {
+  auto lstore = [&](int slot, int buf) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][q * 8]) = ra[h];
+      *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][q * 8]) = ra[slot][h];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][q * 8]) = rb[b][h];
+      for (int b = 0; b < NB; ++b)
+        *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][q * 8]) = rb[slot][b][h];
     }
   };
   floatx4 c[NB][4][4];
@@ -471,28 +480,39 @@ __global__ __launch_bounds__(256, 2) void prefill_gemm_kernel(const GemmTile *ti
         for (int i = 0; i < 4; ++i) c[b][x][y][i] = 0.0f;
 
   const int nk = (K + kKStep - 1) / kKStep;
-  gload(0);
-  lstore(0);
+  gload(0, 0);
+  lstore(0, 0);
+#pragma unroll
+  for (int t = 1; t <= P; ++t)
+    if (t < nk) gload(t - 1, t * kKStep);
   __syncthreads();
-  for (int s = 0; s < nk; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nk) gload((s + 1) * kKStep);
-    bf16x8 af[4];
+  for (int i = 0; i < nk; i += P) {
 #pragma unroll
-    for (int x = 0; x < 4; ++x) af[x] = lds_frag(As[buf], wm * 64 + x * 16 + lane % 16, lane);
+    for (int u = 0; u < P; ++u) {
+      const int s = i + u;  // slice multiplied now, out of LDS buffer s & 1
+      if (s < nk) {
+        const int buf = s & 1;
+        bf16x8 af[4];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      bf16x8 bf[4];
+        for (int x = 0; x < 4; ++x) af[x] = lds_frag(As[buf], wm * 64 + x * 16 + lane % 16, lane);
 #pragma unroll
-      for (int y = 0; y < 4; ++y) bf[y] = lds_frag(Bs[buf][b], wn * 64 + y * 16 + lane % 16, lane);
+        for (int b = 0; b < NB; ++b) {
+          bf16x8 bf[4];
 #pragma unroll
-      for (int x = 0; x < 4; ++x)
+          for (int y = 0; y < 4; ++y) bf[y] = lds_frag(Bs[buf][b], wn * 64 + y * 16 + lane % 16, lane);
 #pragma unroll
-        for (int y = 0; y < 4; ++y)
-          c[b][x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y)
+              c[b][x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
+        }
+        if (s + 1 < nk) {
+          lstore(u, buf ^ 1);                                // slice s + 1 lives in slot s % P = u
+          if (s + 1 + P < nk) gload(u, (s + 1 + P) * kKStep);  // slot u is free again
+        }
+        __syncthreads();
+      }
     }
-    if (s + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
   }
 #pragma unroll
   for (int x = 0; x < 4; ++x)
@@ -501,13 +521,14 @@ __global__ __launch_bounds__(256, 2) void prefill_gemm_kernel(const GemmTile *ti
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int m = t.m0 + wm * 64 + x * 16 + (lane / 16) * 4 + i;
+        if (m >= j.nrows) continue;
         const int n = t.n0 + wn * 64 + y * 16 + lane % 16;
-        if (m < j.nrows && n < N) {
-          const size_t o = (size_t)(j.row0 + m) * ldo + n;
+        if (n < N) {
           if (UP)
-            static_cast<uint16_t *>(out)[o] = f32_to_bf16_rne(silu(c[0][x][y][i]) * c[NB - 1][x][y][i]);
+            static_cast<uint16_t *>(out)[(size_t)(j.row0 + m) * ldo + n] =
+                f32_to_bf16_rne(silu(c[0][x][y][i]) * c[NB - 1][x][y][i]);
           else
-            static_cast<float *>(out)[o] = c[0][x][y][i];
+            static_cast<float *>(out)[(size_t)(j.row0 + m) * ldo + n] = c[0][x][y][i];
         }
       }
 }
@@ -542,7 +563,7 @@ hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l) {
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH(prefill_gemm_kernel<true>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, perm_tok,
+  MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, perm_tok,
              (void *)act, d, d_ff);
   return hipGetLastError();
 }
@@ -550,7 +571,7 @@ hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *j
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
                                float *Y, int d, int d_ff, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH(prefill_gemm_kernel<false>, dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
+  MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
              (const int32_t *)nullptr, (void *)Y, d, d_ff);
   return hipGetLastError();
 }
@@ -562,6 +583,7 @@ hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, co
 }
 
 int prefill_tile_rows() { return kBM; }
-int prefill_tile_cols() { return kBN; }
+int prefill_tile_cols_up() { return kBN; }
+int prefill_tile_cols_down() { return kBN; }
 
 }  // namespace moe
