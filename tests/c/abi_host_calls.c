@@ -1,0 +1,51 @@
+/* A plain C99 client of moe_offload.h: the calls that need no GPU (handle
+ * lifetime, workspace sizing, argument and state errors). */
+#include <stdio.h>
+#include <string.h>
+
+#include "moe_offload.h"
+
+static int fails = 0;
+#define CHECK(cond)                                                   \
+  do {                                                                \
+    if (!(cond)) {                                                    \
+      printf("FAIL %s:%d %s\n", __FILE__, __LINE__, #cond);           \
+      ++fails;                                                        \
+    }                                                                 \
+  } while (0)
+
+int main(void) {
+  moe_cache_t *c = NULL;
+  moe_model_desc d;
+  float h[64];
+  const char *msg;
+
+  CHECK(moe_cache_create(0, 8, 4, MOE_POLICY_LFU, &c) == MOE_ERR_ARG);
+  msg = moe_last_error();
+  CHECK(msg != NULL && msg[0] != '\0');
+  CHECK(moe_cache_create(2, 8, 4, MOE_POLICY_LFU, &c) == MOE_OK && c != NULL);
+
+  memset(&d, 0, sizeof d);
+  d.d_model = 64;
+  d.d_ff = 64;
+  d.top_k = 2;
+  d.dtype = MOE_DTYPE_BF16;
+  CHECK(moe_cache_workspace_bytes(c, &d) > 0);
+  d.dtype = MOE_DTYPE_Q2G16;
+  CHECK(moe_cache_workspace_bytes(c, &d) > 0);
+  d.d_model = 72; /* quantised experts need multiples of 64 */
+  CHECK(moe_cache_workspace_bytes(c, &d) == 0);
+  d.d_model = 64;
+  d.dtype = MOE_DTYPE_BF16;
+  d.fetch_mode = MOE_FETCH_SPLIT;
+  CHECK(moe_cache_bind(c, &d) == MOE_ERR_ARG); /* NULL buffers */
+
+  memset(h, 0, sizeof h);
+  CHECK(moe_decode_layer(c, 0, h, 0) == MOE_ERR_STATE); /* not bound */
+  CHECK(moe_cache_sync(c) == MOE_ERR_STATE);
+
+  moe_cache_destroy(c);
+  moe_cache_destroy(NULL);
+  if (fails == 0) printf("ok\n");
+  return fails != 0;
+}
