@@ -74,6 +74,29 @@ enum {
                            library owns, after enqueueing the layer's FFN.   */
 };
 
+/* Layout of the pinned host store (moe_model_desc.host_format). */
+enum {
+  MOE_HOST_PLAIN = 0,  /* experts stored as dtype, exactly as in the HBM slots   */
+  MOE_HOST_PACKED = 1  /* bf16 experts packed losslessly to ~12.25 bits a weight:
+                          each of W1, W3, W2 (n = d_model * d_ff weights) is cut
+                          into blocks of 8192 weights of 12560 bytes each:
+                            16-byte header: uint32 first exception of the
+                              block, uint32 exceptions in the block, 8 zeros;
+                            8192 bytes (sign << 7) | mantissa per weight;
+                            4096 bytes of 4-bit exponent offsets (low nibble
+                              for even weights) below the group maximum;
+                            256 bytes: largest exponent of each group of 32;
+                          then the matrix's exceptions, uint32
+                          ((index in block) << 8) | exponent, for every weight
+                          whose offset would be 15 or more (stored offset 15);
+                          the matrix is padded to a capacity of
+                          blocks * 12560 + 4 * packed_exc_cap bytes rounded up
+                          to 16, and an expert is W1 | W3 | W2 at that stride.
+                          Copies move the packed bytes; a kernel on the copy
+                          stream rebuilds the identical bf16 expert in its slot.
+                          Needs dtype bf16 and max_prefill_tokens = 0.       */
+};
+
 /* Limits of this build. */
 #define MOE_MAX_EXPERTS 64
 #define MOE_MAX_TOPK 16
@@ -86,11 +109,12 @@ typedef struct {
   int prefetch_max;       /* at most this many guesses fetched per layer, 0..K      */
   int fetch_mode;         /* MOE_FETCH_*                                             */
   int max_prefill_tokens; /* largest T passed to moe_prefill_layer (0: no prefill)   */
-  int reserved;
+  int host_format;        /* MOE_HOST_*                                              */
   const void *gate_w;        /* device [L][E][d], dtype, row-major                     */
   const void *host_experts;  /* pinned host [L][E][W1|W3|W2]; W1, W3 [d_ff x d],
-                                W2 [d x d_ff], each row-major (out x in), dtype;
-                                16-byte aligned (may be NULL if host_layers is set)  */
+                                W2 [d x d_ff], each row-major (out x in), dtype (or
+                                packed, see MOE_HOST_PACKED); 16-byte aligned (may
+                                be NULL if host_layers is set)                      */
   void *arena;               /* device [L][S][W1|W3|W2], 16-byte aligned              */
   void *workspace;           /* device, >= moe_cache_workspace_bytes(), 256-aligned   */
   size_t workspace_bytes;
@@ -102,6 +126,8 @@ typedef struct {
                                      [E][W1|W3|W2] at host_layers[l]; when non-NULL it
                                      replaces host_experts, so a store can span several
                                      allocations (entries may repeat); 16-byte aligned */
+  int packed_exc_cap;        /* MOE_HOST_PACKED: exception capacity per matrix       */
+  int reserved;
 } moe_model_desc;
 
 /* One trace record.  kind 0 (access): a token's lookup of one of its K
@@ -200,6 +226,8 @@ typedef struct {
       ffn_reduce_ms;
   uint64_t router_n, fetch_n, ffn_up_n, ffn_down_n, prefill_n, gemm_up_n, gemm_down_n, ffn_reduce_n;
   double gemm_up_flop, gemm_down_flop; /* algorithmic flops of the timed GEMM launches */
+  double unpack_ms;                    /* MOE_HOST_PACKED: rebuilding copied experts  */
+  uint64_t unpack_n;
 } moe_timing;
 
 /* Kernel timing with HIP events, off by default.  While enabled, every router,

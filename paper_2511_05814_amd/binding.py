@@ -20,6 +20,7 @@ MOE_DTYPE_F32, MOE_DTYPE_BF16, MOE_DTYPE_Q2G16 = 0, 1, 2
 MOE_OK, MOE_ERR_ARG, MOE_ERR_STATE, MOE_ERR_HIP, MOE_ERR_NOMEM = 0, -1, -2, -3, -4
 MOE_PREFETCH_NEXT = 1
 MOE_FETCH_KERNEL, MOE_FETCH_DMA, MOE_FETCH_SPLIT = 0, 1, 2
+MOE_HOST_PLAIN, MOE_HOST_PACKED = 0, 1
 MOE_MAX_EXPERTS, MOE_MAX_TOPK = 64, 16
 
 POLICIES = {"lru": MOE_POLICY_LRU, "lfu": MOE_POLICY_LFU}
@@ -36,12 +37,13 @@ class moe_model_desc(ctypes.Structure):
     _fields_ = [
         ("d_model", ctypes.c_int), ("d_ff", ctypes.c_int), ("top_k", ctypes.c_int),
         ("dtype", ctypes.c_int), ("prefetch_max", ctypes.c_int), ("fetch_mode", ctypes.c_int),
-        ("max_prefill_tokens", ctypes.c_int), ("reserved", ctypes.c_int),
+        ("max_prefill_tokens", ctypes.c_int), ("host_format", ctypes.c_int),
         ("gate_w", ctypes.c_void_p), ("host_experts", ctypes.c_void_p),
         ("arena", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t), ("trace", ctypes.c_void_p),
         ("trace_cap", ctypes.c_size_t), ("compute_stream", ctypes.c_void_p),
         ("copy_stream", ctypes.c_void_p), ("host_layers", ctypes.POINTER(ctypes.c_void_p)),
+        ("packed_exc_cap", ctypes.c_int), ("reserved", ctypes.c_int),
     ]
 
 
@@ -63,7 +65,8 @@ class moe_timing(ctypes.Structure):
                 + [(n, ctypes.c_uint64) for n in
                    ("router_n", "fetch_n", "ffn_up_n", "ffn_down_n", "prefill_n", "gemm_up_n",
                     "gemm_down_n", "ffn_reduce_n")]
-                + [(n, ctypes.c_double) for n in ("gemm_up_flop", "gemm_down_flop")])
+                + [(n, ctypes.c_double) for n in ("gemm_up_flop", "gemm_down_flop", "unpack_ms")]
+                + [("unpack_n", ctypes.c_uint64)])
 
 
 # (name, restype, argtypes) of every exported function, in header order

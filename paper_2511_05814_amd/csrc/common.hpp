@@ -61,7 +61,7 @@ struct TraceRec {
 };
 
 enum { REC_ACCESS = 0, REC_PREFETCH = 1, REC_PREFILL = 2 };
-enum { ERR_NONE = 0, ERR_BAD_IDS = 1, ERR_BAD_LIST = 2 };
+enum { ERR_NONE = 0, ERR_BAD_IDS = 1, ERR_BAD_LIST = 2, ERR_BAD_PACK = 3 };
 
 struct RouterArgs {
   const void *gate;        // [L][E][d]
@@ -150,8 +150,16 @@ struct Launch {
 
 // launchers (one per translation unit that owns the kernel)
 hipError_t launch_router(const RouterArgs &a, const Launch &l);
+// Copies of a fetch list: expert e of the list's layer from its host store
+// (stride src_stride) into its HBM slot (stride expert_bytes), or, when
+// staging is non-NULL, entry i into staging + i * src_stride.
 hipError_t launch_fetch(const FetchList *list, const uint8_t *const *layers, uint8_t *arena, int L, int E,
-                        int S, int K, uint64_t expert_bytes, int32_t *err, const Launch &l);
+                        int S, int K, uint64_t expert_bytes, uint64_t src_stride, uint8_t *staging,
+                        int32_t *err, const Launch &l);
+// Packed experts of a fetch list, entry i at staging + i * 3 * mat_cap, rebuilt
+// as bf16 into their slots; n = weights per matrix.
+hipError_t launch_unpack(const FetchList *list, const uint8_t *staging, uint8_t *arena, int L, int S, int K,
+                         uint64_t mat_cap, uint64_t expert_bytes, uint64_t n, int32_t *err, const Launch &l);
 hipError_t launch_ffn_up(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_down(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, const Launch &l);

@@ -43,7 +43,7 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
   size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, act = 0, part = 0,
-         hostptrs = 0, prefill = 0, total = 0;
+         hostptrs = 0, prefill = 0, staging = 0, total = 0;
 };
 
 bool misaligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) != 0; }
@@ -96,7 +96,12 @@ struct moe_cache {
   bool bound = false;
   moe_model_desc desc{};
   int K = 0, d = 0, dff = 0, dtype = 0, pmax = 0, fetch_mode = 0, max_T = 0;
-  uint64_t B = 0;
+  uint64_t B = 0;        // bytes of one expert in an HBM slot
+  int host_format = 0;   // MOE_HOST_*
+  uint64_t Bh = 0;       // stride of one expert in the host store (bytes a miss moves)
+  uint64_t mat_cap = 0;  // packed store: bytes of one matrix
+  uint64_t n_mat = 0;    // weights per matrix
+  uint8_t *staging = nullptr;  // packed store: K copied experts before unpacking
   hipStream_t cs = nullptr, xs = nullptr;
   bool one_stream = true;
   Layout lay;
@@ -139,7 +144,7 @@ struct moe_cache {
 namespace moe {
 enum SpanKind {
   SPAN_ROUTER = 0, SPAN_FETCH, SPAN_UP, SPAN_DOWN, SPAN_PREFILL, SPAN_GEMM_UP, SPAN_GEMM_DOWN, SPAN_REDUCE,
-  SPAN_KINDS
+  SPAN_UNPACK, SPAN_KINDS
 };
 
 // Start/stop a timed span on stream s (no-op unless timing is on).
@@ -230,6 +235,19 @@ static uint64_t expert_bytes(const moe_model_desc *d) {
   return 3 * n * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
 }
 
+// Packed host store (MOE_HOST_PACKED): blocks of 8192 weights in 12560 bytes,
+// then packed_exc_cap exception words, per matrix, rounded up to 16 bytes.
+static uint64_t packed_matrix_bytes(const moe_model_desc *d) {
+  const uint64_t n = (uint64_t)d->d_model * d->d_ff;
+  const uint64_t nb = (n + 8191) / 8192;
+  return (nb * 12560 + 4ull * (uint64_t)d->packed_exc_cap + 15) / 16 * 16;
+}
+
+// Stride of one expert in the host store: the bytes one miss moves.
+static uint64_t host_expert_bytes(const moe_model_desc *d) {
+  return d->host_format == MOE_HOST_PACKED ? 3 * packed_matrix_bytes(d) : expert_bytes(d);
+}
+
 // Element type of the gate: fp32 for fp32 models, bf16 otherwise (router dtype code).
 static int gate_dtype(int dtype) { return dtype == MOE_DTYPE_F32 ? 0 : 1; }
 
@@ -250,6 +268,14 @@ static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
   if (d->fetch_mode != MOE_FETCH_KERNEL && d->fetch_mode != MOE_FETCH_DMA && d->fetch_mode != MOE_FETCH_SPLIT)
     return fail(MOE_ERR_ARG, "bad fetch_mode");
   if (d->max_prefill_tokens < 0) return fail(MOE_ERR_ARG, "max_prefill_tokens < 0");
+  if (d->host_format != MOE_HOST_PLAIN && d->host_format != MOE_HOST_PACKED)
+    return fail(MOE_ERR_ARG, "bad host_format");
+  if (d->host_format == MOE_HOST_PACKED) {
+    if (d->dtype != MOE_DTYPE_BF16) return fail(MOE_ERR_ARG, "a packed host store holds bf16 experts");
+    if (d->max_prefill_tokens > 0) return fail(MOE_ERR_ARG, "a packed host store serves decode only");
+    if (d->packed_exc_cap < 0 || (uint64_t)d->packed_exc_cap > (uint64_t)d->d_model * d->d_ff)
+      return fail(MOE_ERR_ARG, "packed_exc_cap out of range");
+  }
   if (d->max_prefill_tokens > 0 && d->dtype != MOE_DTYPE_BF16)
     return fail(MOE_ERR_ARG, "batched prefill runs on bf16 experts (matrix cores); dtype must be bf16");
   if ((int64_t)d->max_prefill_tokens * d->top_k > (1 << 28))
@@ -276,6 +302,7 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff, d->dtype) * d->d_model);
   const uint64_t B = expert_bytes(d);
   l.prefill = take(prefill_layout(d->top_k, d->d_model, d->d_ff, c->E, c->S, d->max_prefill_tokens, B).total);
+  l.staging = take(d->host_format == MOE_HOST_PACKED ? (size_t)d->top_k * host_expert_bytes(d) : 0);
   l.total = off;
   return l;
 }
@@ -323,11 +350,11 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
     return fail(MOE_ERR_ARG, "workspace too small: %zu < %zu bytes", d->workspace_bytes, lay.total);
 
   // per-layer host bases (one contiguous store, or the caller's per-layer table)
-  const uint64_t B = expert_bytes(d);
+  const uint64_t Bh = host_expert_bytes(d);
   std::vector<const uint8_t *> hl(c->L), dl(c->L, nullptr);
   for (int l = 0; l < c->L; ++l) {
     hl[l] = d->host_layers ? static_cast<const uint8_t *>(d->host_layers[l])
-                           : static_cast<const uint8_t *>(d->host_experts) + (size_t)l * c->E * B;
+                           : static_cast<const uint8_t *>(d->host_experts) + (size_t)l * c->E * Bh;
     if (!hl[l] || misaligned(hl[l], 16))
       return fail(MOE_ERR_ARG, "host store of layer %d is NULL or not 16-byte aligned", l);
   }
@@ -353,6 +380,10 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->fetch_mode = d->fetch_mode;
   c->max_T = d->max_prefill_tokens;
   c->B = expert_bytes(d);
+  c->host_format = d->host_format;
+  c->Bh = host_expert_bytes(d);
+  c->mat_cap = d->host_format == MOE_HOST_PACKED ? packed_matrix_bytes(d) : 0;
+  c->n_mat = (uint64_t)d->d_model * d->d_ff;
   c->cs = static_cast<hipStream_t>(d->compute_stream);
   c->xs = d->copy_stream ? static_cast<hipStream_t>(d->copy_stream) : c->cs;
   c->one_stream = (c->xs == c->cs);
@@ -368,6 +399,7 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->act = reinterpret_cast<float *>(c->ws + lay.act);
   c->part = reinterpret_cast<float *>(c->ws + lay.part);
   c->prefill_ws = c->ws + lay.prefill;
+  c->staging = d->host_format == MOE_HOST_PACKED ? c->ws + lay.staging : nullptr;
   c->dev_layers = reinterpret_cast<const uint8_t *const *>(c->ws + lay.hostptrs);
   c->dev_layer_host = dl;
   HIP_TRY0(hipMemcpy(c->ws + lay.hostptrs, dl.data(), sizeof(void *) * c->L, hipMemcpyHostToDevice));
@@ -437,10 +469,36 @@ int moe_cache_reset(moe_cache_t *c) {
   }
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
-  for (int l = 0; l < c->L; ++l)
-    for (int s = 0; s < c->S; ++s)
-      HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)l * c->S + s) * c->B, c->host_layer[l] + (size_t)s * c->B,
-                                c->B, hipMemcpyHostToDevice, c->xs));
+  if (c->host_format == MOE_HOST_PACKED) {
+    // copy each packed expert to staging and rebuild it in its slot, through
+    // the layer's demand list (cleared again afterwards)
+    for (int l = 0; l < c->L; ++l)
+      for (int s = 0; s < c->S; ++s) {
+        FetchList f{};
+        f.n = 1;
+        f.layer = l;
+        f.expert[0] = s;
+        f.slot[0] = s;
+        HIP_TRY(c, hipMemcpy(c->dl + l, &f, sizeof f, hipMemcpyHostToDevice));
+        HIP_TRY(c, hipMemcpy(c->staging, c->host_layer[l] + (size_t)s * c->Bh, c->Bh, hipMemcpyHostToDevice));
+        HIP_TRY(c, launch_unpack(c->dl + l, c->staging, arena, c->L, c->S, c->K, c->mat_cap, c->B, c->n_mat,
+                                 c->err, Launch{c->xs}));
+        HIP_TRY(c, hipStreamSynchronize(c->xs));
+      }
+    HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.dlists, 0, sizeof(FetchList) * c->L, c->xs));
+    int32_t e = 0;
+    HIP_TRY(c, hipMemcpyAsync(&e, c->err, sizeof e, hipMemcpyDeviceToHost, c->xs));
+    HIP_TRY(c, hipStreamSynchronize(c->xs));
+    if (e != ERR_NONE) {
+      c->sticky = MOE_ERR_ARG;
+      return fail(MOE_ERR_ARG, "packed host store is corrupt (an exception entry is missing)");
+    }
+  } else {
+    for (int l = 0; l < c->L; ++l)
+      for (int s = 0; s < c->S; ++s)
+        HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)l * c->S + s) * c->B, c->host_layer[l] + (size_t)s * c->B,
+                                  c->B, hipMemcpyHostToDevice, c->xs));
+  }
   HIP_TRY(c, hipStreamSynchronize(c->xs));
   std::fill(c->demand_pending.begin(), c->demand_pending.end(), 0);
   std::fill(c->pf_pending.begin(), c->pf_pending.end(), 0);
@@ -453,15 +511,27 @@ int moe_cache_reset(moe_cache_t *c) {
 }  // extern "C"
 
 // Issue the copies for one fetch list that the router just wrote.
+// A packed store's experts land in staging and are rebuilt into their slots
+// by an unpack kernel behind the copies on the same stream.
+static int unpack_list(moe_cache *c, FetchList *list, hipStream_t q) {
+  Launch l;
+  HIP_TRY(c, kernel_span(c, q, &l));
+  HIP_TRY(c, launch_unpack(list, c->staging, static_cast<uint8_t *>(c->desc.arena), c->L, c->S, c->K, c->mat_cap,
+                           c->B, c->n_mat, c->err, l));
+  kernel_span_done(c, SPAN_UNPACK, l);
+  return MOE_OK;
+}
+
 static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_t q) {
   const bool by_kernel = c->fetch_mode == MOE_FETCH_KERNEL || (c->fetch_mode == MOE_FETCH_SPLIT && mirror_idx == 0);
+  const bool packed = c->host_format == MOE_HOST_PACKED;
   if (by_kernel) {
     Launch l;
     HIP_TRY(c, kernel_span(c, q, &l));
     HIP_TRY(c, launch_fetch(list, c->dev_layers, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
-                            c->K, c->B, c->err, l));
+                            c->K, c->B, c->Bh, c->staging, c->err, l));
     kernel_span_done(c, SPAN_FETCH, l);
-    return MOE_OK;
+    return packed ? unpack_list(c, list, q) : MOE_OK;
   }
   const FetchList &m = c->mirror[mirror_idx];
   if (m.n < 0 || m.n > c->K || m.layer < 0 || m.layer >= c->L) {
@@ -479,11 +549,11 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
       c->sticky = MOE_ERR_HIP;
       return fail(MOE_ERR_HIP, "inconsistent fetch entry from the device");
     }
-    HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)m.layer * c->S + s) * c->B,
-                              host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
+    uint8_t *dst = packed ? c->staging + (size_t)i * c->Bh : arena + ((size_t)m.layer * c->S + s) * c->B;
+    HIP_TRY(c, hipMemcpyAsync(dst, host + (size_t)e * c->Bh, c->Bh, hipMemcpyHostToDevice, q));
   }
   HIP_TRY(c, span_end(c, q, SPAN_FETCH, t0));
-  return MOE_OK;
+  return packed ? unpack_list(c, list, q) : MOE_OK;
 }
 
 // Router (+ fetches, + FFN) for one call.  spec_layer < 0: no speculation.
@@ -507,7 +577,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.err = c->err;
   a.trace_count = c->trace_count;
   a.trace_cap = c->desc.trace ? c->desc.trace_cap : 0;
-  a.expert_bytes = c->B;
+  a.expert_bytes = c->Bh;  // bytes one fetch moves (counters)
   a.layer = layer;
   a.L = c->L;
   a.E = c->E;
@@ -990,10 +1060,10 @@ int moe_cache_read_timing(moe_cache_t *c, moe_timing *out) {
   if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
   double *ms[SPAN_KINDS] = {&out->router_ms,  &out->fetch_ms,     &out->ffn_up_ms,
                             &out->ffn_down_ms, &out->prefill_ms,   &out->gemm_up_ms,
-                            &out->gemm_down_ms, &out->ffn_reduce_ms};
+                            &out->gemm_down_ms, &out->ffn_reduce_ms, &out->unpack_ms};
   uint64_t *n[SPAN_KINDS] = {&out->router_n,  &out->fetch_n,     &out->ffn_up_n,
                              &out->ffn_down_n, &out->prefill_n,   &out->gemm_up_n,
-                             &out->gemm_down_n, &out->ffn_reduce_n};
+                             &out->gemm_down_n, &out->ffn_reduce_n, &out->unpack_n};
   int rc = MOE_OK;
   for (const auto &sp : c->spans) {
     float t = 0.0f;

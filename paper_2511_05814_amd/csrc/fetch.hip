@@ -24,14 +24,14 @@ constexpr int kBlocks = MOE_FETCH_BLOCKS;
 __global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list,
                                                          const uint8_t *const *layers, uint8_t *arena,
                                                          int L, int E, int S, int K, uint64_t expert_bytes,
-                                                         int32_t *err) {
+                                                         uint64_t src_stride, uint8_t *staging, int32_t *err) {
   const int n = list->n;
   const int layer = list->layer;
   if (n < 0 || n > K || layer < 0 || layer >= L) {
     if (n != 0 && blockIdx.x == 0 && threadIdx.x == 0) *err = ERR_BAD_LIST;
     return;
   }
-  const size_t nv = expert_bytes / sizeof(uint4);
+  const size_t nv = (staging ? src_stride : expert_bytes) / sizeof(uint4);
   const size_t stride = (size_t)gridDim.x * kThreads;
   const uint8_t *base = layers[layer];
   if (base == nullptr) {  // no mapped host store for this layer: refuse, never dereference
@@ -45,8 +45,9 @@ __global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list,
       if (blockIdx.x == 0 && threadIdx.x == 0) *err = ERR_BAD_LIST;
       continue;
     }
-    const uint4 *src = reinterpret_cast<const uint4 *>(base + (size_t)e * expert_bytes);
-    uint4 *dst = reinterpret_cast<uint4 *>(arena + ((size_t)layer * S + s) * expert_bytes);
+    const uint4 *src = reinterpret_cast<const uint4 *>(base + (size_t)e * src_stride);
+    uint4 *dst = reinterpret_cast<uint4 *>(staging ? staging + (size_t)i * src_stride
+                                                   : arena + ((size_t)layer * S + s) * expert_bytes);
     size_t j = (size_t)blockIdx.x * kThreads + threadIdx.x;
     for (; j + 3 * stride < nv; j += 4 * stride) {
       const uint4 a = src[j], b = src[j + stride], c = src[j + 2 * stride], d = src[j + 3 * stride];
@@ -62,9 +63,10 @@ __global__ __launch_bounds__(kThreads) void fetch_kernel(const FetchList *list,
 }  // namespace
 
 hipError_t launch_fetch(const FetchList *list, const uint8_t *const *layers, uint8_t *arena, int L, int E,
-                        int S, int K, uint64_t expert_bytes, int32_t *err, const Launch &l) {
+                        int S, int K, uint64_t expert_bytes, uint64_t src_stride, uint8_t *staging,
+                        int32_t *err, const Launch &l) {
   MOE_LAUNCH(fetch_kernel, dim3(kBlocks), dim3(kThreads), 0, l, list, layers, arena, L, E, S, K, expert_bytes,
-             err);
+             src_stride, staging, err);
   return hipGetLastError();
 }
 

@@ -17,6 +17,7 @@ from typing import Optional
 import numpy as np
 
 from . import binding as b
+from . import pack
 from . import workload as wl
 
 
@@ -36,12 +37,28 @@ class HostStore:
     stack needs.  When the store would exceed `max_pinned_bytes`, only the
     first `distinct` layers get pages of their own and layer l uses the pages
     of layer l mod distinct: every fetch still moves a whole expert over the
-    host link, only the weight values repeat (gates stay per layer)."""
+    host link, only the weight values repeat (gates stay per layer).
+
+    packed=True stores bf16 experts in the lossless packed format of
+    paper_2511_05814_amd.pack (about 12.25 bits a weight); exc_cap is the
+    exception capacity of every matrix (default n / 4096 + 64, about three
+    times what N(0, sigma) weights need)."""
 
     def __init__(self, cfg: wl.Config, fill: bool = True, workers: Optional[int] = None,
-                 max_pinned_bytes: int = 64 << 30):
+                 max_pinned_bytes: int = 64 << 30, packed: bool = False, exc_cap: Optional[int] = None):
         self.cfg = cfg
-        self.layer_bytes = cfg.experts * cfg.expert_bytes
+        self.packed = packed
+        if packed:
+            if cfg.dtype != "bf16":
+                raise ValueError("the packed host store holds bf16 experts")
+            n = cfg.matrix_elems
+            self.exc_cap = exc_cap if exc_cap is not None else n // 4096 + 64
+            self.matrix_stride = pack.matrix_capacity(n, self.exc_cap)
+            self.expert_stride = 3 * self.matrix_stride
+        else:
+            self.exc_cap = 0
+            self.expert_stride = cfg.expert_bytes
+        self.layer_bytes = cfg.experts * self.expert_stride
         self.distinct = int(max(1, min(cfg.layers, max_pinned_bytes // self.layer_bytes)))
         self.nbytes = self.distinct * self.layer_bytes
         self.ptrs = []
@@ -68,6 +85,14 @@ class HostStore:
 
         def one(le):
             l, e = le
+            if self.packed:
+                raw = wl.expert_weights(cfg, l, e)
+                n = cfg.matrix_elems
+                row = self.arrays[l].reshape(cfg.experts, self.expert_stride)[e]
+                for m in range(3):
+                    dst = row[m * self.matrix_stride:(m + 1) * self.matrix_stride]
+                    pack.pack_matrix(raw[m * n:(m + 1) * n], self.exc_cap, out=dst)
+                return
             view = self.arrays[l].view(sdt).reshape(cfg.experts, cfg.expert_storage_len)
             wl.fill_expert(cfg, l, e, view[e])
 
@@ -80,8 +105,12 @@ class HostStore:
         return self.distinct < self.cfg.layers
 
     def expert(self, layer: int, expert: int) -> np.ndarray:
-        """Storage-dtype view of one expert (W1|W3|W2)."""
+        """Storage-dtype view of one expert (W1|W3|W2).  A packed store holds
+        an exact encoding of the generator's bf16 weights, so those are
+        returned (drawn again) rather than the packed bytes."""
         cfg = self.cfg
+        if self.packed:
+            return wl.expert_weights(cfg, self.layer_src[layer], expert)
         off = expert * cfg.expert_bytes
         raw = self.arrays[self.layer_src[layer]][off:off + cfg.expert_bytes]
         return raw.view(cfg.storage_dtype)
@@ -141,6 +170,8 @@ class OffloadedMoE:
             d.prefetch_max = prefetch_max
             d.fetch_mode = fetch_mode
             d.max_prefill_tokens = max_prefill_tokens
+            d.host_format = b.MOE_HOST_PACKED if store.packed else b.MOE_HOST_PLAIN
+            d.packed_exc_cap = store.exc_cap
             d.gate_w = gates.ptr
             d.host_experts = None
             d.host_layers = ctypes.cast(store.layer_ptrs, ctypes.POINTER(ctypes.c_void_p))

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
 def test_struct_sizes_match_the_header_layout():
     assert ctypes.sizeof(b.moe_trace_rec) == 32
     assert ctypes.sizeof(b.moe_layer_stats) == 9 * 8
-    assert ctypes.sizeof(b.moe_model_desc) == 8 * 4 + 10 * 8
+    assert ctypes.sizeof(b.moe_model_desc) == 8 * 4 + 10 * 8 + 2 * 4
 
 
 @pytest.mark.parametrize("args", [

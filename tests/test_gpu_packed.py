@@ -1,0 +1,80 @@
+"""The packed host store (lossless ~12.25-bit bf16 experts rebuilt on the GPU
+after each copy) must give exactly what the plain bf16 store gives: the same
+outputs bit for bit and the same cache traces, with fewer bytes per miss."""
+import numpy as np
+import pytest
+
+from paper_2511_05814_amd import binding as b
+from paper_2511_05814_amd import offload
+from paper_2511_05814_amd import workload as wl
+from tests._gpu_rig import _say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def run(cfg, store, gates, slots, policy, tokens, flags=0, **kw):
+    moe = offload.OffloadedMoE(cfg, store, gates, slots, policy, **kw)
+    H = torch.from_numpy(np.ascontiguousarray(wl.hidden_states(cfg, tokens))).to("cuda")
+    moe.decode(H, flags=flags)
+    moe.sync()
+    recs, dropped = moe.trace_records()
+    assert dropped == 0
+    st = moe.stats()
+    moe.close()
+    return H.cpu().numpy(), recs, st
+
+
+def compare(cfg, slots, policy, tokens, modes, pmax):
+    gates = offload.DeviceGates(cfg)
+    plain = offload.HostStore(cfg)
+    packed = offload.HostStore(cfg, packed=True)
+    assert packed.expert_stride < cfg.expert_bytes
+    flags = b.MOE_PREFETCH_NEXT if pmax else 0
+    ref = run(cfg, plain, gates, slots, policy, tokens, flags, prefetch_max=pmax)
+    for mode in modes:
+        _say("packed store, fetch mode", mode)
+        H, recs, st = run(cfg, packed, gates, slots, policy, tokens, flags, prefetch_max=pmax, fetch_mode=mode)
+        assert H.tobytes() == ref[0].tobytes()
+        assert recs == ref[1]
+        for a, c in zip(st, ref[2]):
+            moves = a["misses"] + a["pf_issued"]
+            assert a["bytes_fetched"] == moves * packed.expert_stride
+            assert c["bytes_fetched"] == moves * cfg.expert_bytes
+    plain.close()
+    packed.close()
+
+
+def test_packed_store_matches_plain_all_fetch_modes():
+    cfg = wl.CONFIGS["tiny-stack"].with_(dtype="bf16", tokens=40)
+    compare(cfg, 4, "lfu", cfg.tokens, (b.MOE_FETCH_SPLIT, b.MOE_FETCH_KERNEL, b.MOE_FETCH_DMA), pmax=2)
+
+
+def test_packed_store_ragged_shape_partial_block():
+    # n = 136 * 200 = 27200 weights per matrix: the last block is partial
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=3, experts=5, top_k=3, d_model=136, d_ff=200,
+                                         dtype="bf16", tokens=20)
+    compare(cfg, 3, "lru", cfg.tokens, (b.MOE_FETCH_SPLIT, b.MOE_FETCH_DMA), pmax=1)
+
+
+def test_packed_store_mixtral_layer():
+    cfg = wl.CONFIGS["mixtral-layer"].with_(tokens=16)
+    compare(cfg, 4, "lfu", cfg.tokens, (b.MOE_FETCH_SPLIT,), pmax=0)
+
+
+def test_corrupt_packed_store_is_reported():
+    cfg = wl.CONFIGS["tiny-stack"].with_(dtype="bf16", layers=1, tokens=4)
+    gates = offload.DeviceGates(cfg)
+    store = offload.HostStore(cfg, packed=True)
+    # expert 0, W1: wipe its exception list (the tiny model's W1 has some)
+    n = cfg.matrix_elems
+    nb = (n + 8191) // 8192
+    row = store.arrays[0].reshape(cfg.experts, store.expert_stride)[0]
+    first_block_hdr = row[:16].view("<u4")
+    assert row[nb * 12560:store.matrix_stride].view("<u4").any() or first_block_hdr[1] > 0
+    row[nb * 12560:store.matrix_stride] = 0xFF
+    with pytest.raises(b.MoeError) as e:
+        offload.OffloadedMoE(cfg, store, gates, 4, "lfu")
+    assert e.value.code == b.MOE_ERR_ARG and "corrupt" in str(e.value)
+    store.close()
