@@ -7,6 +7,8 @@ What the paper fixes:
 * the baseline evicts the least recently used expert (Sec. 3.1);
 * the proposed policy keeps one usage count per expert and evicts the least
   frequently used one (Sec. 4.2);
+* a better policy would weigh popularity together with how long an expert has
+  gone unused (Sec. 6.1); the third policy here is one such key;
 * speculative loading applies layer l+1's gate to layer l's hidden state and
   takes its top-K as the guess for layer l+1 (Sec. 3.2, Sec. 4.3).
 
@@ -16,6 +18,10 @@ Readings where the paper is silent (each is listed in the design notes):
   lookup; hit <=> resident when the token arrives at the layer;
 * the victim of a miss is the resident expert outside the token's selected
   set that minimises (last, slot) for LRU or (count, last, slot) for LFU;
+* aged LFU ("lfu-aged:A", A >= 1 ticks): the victim minimises
+  (floor(count / 2^floor(age / A)), last, slot) with age = clock - last at the
+  moment of the choice: the usage count halves once per A ticks without use
+  (the stored count itself is never changed); with A beyond any age it is LFU;
 * counts persist across eviction;
 * a prefetch inserts up to `max_n` non-resident guesses in rank order, each
   taking one clock tick, victim chosen by the same key with all K guesses
@@ -24,8 +30,8 @@ Readings where the paper is silent (each is listed in the design notes):
   it; otherwise it is wasted (also when evicted before that lookup);
 * batched prefill: counts += per-expert routing counts, the clock ticks once
   per (token, rank) in token-major order, then the S experts with the largest
-  key (LFU: count, LRU: last; ties: resident first, then lower id) become the
-  resident set; kept experts keep their slots, newcomers take the freed slots
+  key (LFU: count, aged LFU: the aged count at the batch's last tick, LRU:
+  last; ties: resident first, then lower id) become the resident set; kept experts keep their slots, newcomers take the freed slots
   (both ascending).
 
 A cold start (`initial` with -1 entries) is supported for textbook checks:
@@ -36,7 +42,19 @@ from __future__ import annotations
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence
 
-LRU, LFU = "lru", "lfu"
+LRU, LFU, LFU_AGED = "lru", "lfu", "lfu-aged"
+
+
+def parse_policy(spec: str):
+    """'lru', 'lfu' or 'lfu-aged:A' -> (name, A or None)."""
+    name, _, arg = spec.partition(":")
+    if name == LFU_AGED:
+        if not arg.isdigit() or int(arg) < 1:
+            raise ValueError(f"aged LFU needs a period of at least one tick: {spec!r}")
+        return name, int(arg)
+    if name not in (LRU, LFU) or arg:
+        raise ValueError(spec)
+    return name, None
 
 # record kinds and flag bits (shared vocabulary with the trace format)
 KIND_ACCESS, KIND_PREFETCH, KIND_PREFILL = 0, 1, 2
@@ -78,8 +96,7 @@ class LayerCache:
 
     def __init__(self, experts: int, slots: int, policy: str, layer: int = 0,
                  initial: Optional[Sequence[int]] = None):
-        if policy not in (LRU, LFU):
-            raise ValueError(policy)
+        policy, self.aging = parse_policy(policy)
         if not (1 <= slots <= experts):
             raise ValueError("need 1 <= slots <= experts")
         self.E, self.S, self.policy, self.layer = experts, slots, policy, layer
@@ -99,10 +116,18 @@ class LayerCache:
         self.stats = Stats()
 
     # -- policy ------------------------------------------------------------
+    def aged_count(self, e: int) -> int:
+        """Usage count halved (rounding down) once per `aging` ticks since the
+        expert's last use, at the current clock."""
+        halvings = (self.clock - self.last[e]) // self.aging
+        return self.count[e] // (2 ** halvings)
+
     def key(self, e: int):
         s = self.expert_slot[e]
         if self.policy == LRU:
             return (self.last[e], s)
+        if self.policy == LFU_AGED:
+            return (self.aged_count(e), self.last[e], s)
         return (self.count[e], self.last[e], s)
 
     def choose_victim(self, pinned) -> tuple:
@@ -220,6 +245,8 @@ class LayerCache:
 
         if self.policy == LFU:
             prio = lambda e: (-self.count[e], 0 if e in start else 1, e)
+        elif self.policy == LFU_AGED:
+            prio = lambda e: (-self.aged_count(e), 0 if e in start else 1, e)
         else:
             prio = lambda e: (-self.last[e], 0 if e in start else 1, e)
         rstar = set(sorted(range(self.E), key=prio)[:self.S])

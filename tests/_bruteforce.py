@@ -4,14 +4,19 @@ only to pin the oracle's cache.
 The oracle keeps per-expert clocks and counters and takes a keyed minimum.
 This checker keeps a recency list (least recent first) and scans it: LRU
 evicts the first unpinned entry, LFU the unpinned entry with the smallest
-count, earliest in the list on equal counts.  Record tuples use the same
+count, earliest in the list on equal counts.  Aged LFU ("lfu-aged:A") keeps
+an idle counter per expert that every tick raises and a use clears, and
+halves a copy of the count step by step, once per A idle ticks, before the
+same smallest-count scan.  Record tuples use the same
 layout as the oracle's: (kind, token, layer, rank, expert, flags, slot, victim).
 """
 
 
 class ListCache:
     def __init__(self, E, S, policy, layer=0, initial=None):
-        self.E, self.S, self.policy, self.layer = E, S, policy, layer
+        self.policy, _, period = policy.partition(":")
+        self.period = int(period) if period else None
+        self.E, self.S, self.layer = E, S, layer
         init = list(initial) if initial is not None else list(range(S))
         self.slot = {e: s for s, e in enumerate(init) if e >= 0}
         self.free = [s for s, e in enumerate(init) if e < 0]
@@ -19,6 +24,22 @@ class ListCache:
         self.count = {e: 0 for e in range(E)}
         self.pf = set()
         self.t = 0
+        # warm start: the expert in slot s was last used S - s ticks ago
+        self.idle = {e: 0 for e in range(E)}
+        for e, s in self.slot.items():
+            self.idle[e] = S - s
+
+    def _tick(self, used):
+        for e in self.idle:
+            self.idle[e] += 1
+        self.idle[used] = 0
+
+    def _weight(self, e):
+        c = self.count[e]
+        if self.policy == "lfu-aged":
+            for _ in range(self.idle[e] // self.period):
+                c //= 2
+        return c
 
     def _evict_for(self, pinned):
         if self.free:
@@ -29,8 +50,8 @@ class ListCache:
         if self.policy == "lru":
             v = cands[0]
         else:
-            low = min(self.count[e] for e in cands)
-            v = [e for e in cands if self.count[e] == low][0]
+            low = min(self._weight(e) for e in cands)
+            v = [e for e in cands if self._weight(e) == low][0]
         s = self.slot.pop(v)
         self.order.remove(v)
         self.pf.discard(v)
@@ -43,6 +64,7 @@ class ListCache:
         self.t += 1
         for r, j in enumerate(ids):
             self.count[j] += 1
+            self._tick(j)
             if j in self.slot:
                 useful = j in self.pf
                 self.pf.discard(j)
@@ -65,6 +87,7 @@ class ListCache:
             if j in self.slot:
                 out.append((1, self.t, self.layer, r, j, 1, self.slot[j], -1))
             elif n < max_n:
+                self._tick(j)
                 s, v = self._evict_for(pinned)
                 self.slot[j] = s
                 self.order.append(j)

@@ -30,9 +30,12 @@ def _random_trace(rng, E, k, T, skew=True):
 
 
 # ---- the oracle against the list-scan formulation -----------------------------
-@pytest.mark.parametrize("policy", ["lru", "lfu"])
+POLICIES = ["lru", "lfu", "lfu-aged:1", "lfu-aged:4", "lfu-aged:32"]
+
+
+@pytest.mark.parametrize("policy", POLICIES)
 def test_cache_matches_list_scan_on_random_traces(policy):
-    rng = np.random.default_rng(11 if policy == "lru" else 12)
+    rng = np.random.default_rng(11 + POLICIES.index(policy))
     for _ in range(300):
         E = int(rng.integers(2, 9))
         k = int(rng.integers(1, min(E, 4) + 1))
@@ -44,7 +47,7 @@ def test_cache_matches_list_scan_on_random_traces(policy):
             assert [r.astuple() for r in a.access(ids)] == b.access(ids)
 
 
-@pytest.mark.parametrize("policy", ["lru", "lfu"])
+@pytest.mark.parametrize("policy", POLICIES)
 def test_prefetch_matches_list_scan(policy):
     rng = np.random.default_rng(13)
     for _ in range(200):
@@ -92,6 +95,52 @@ def test_hand_worked_lru_and_lfu():
     assert belady.min_hits(seq, 2, [0, 1]) == 4
 
 
+def test_hand_worked_aged_lfu():
+    # E = 4, S = 3, K = 1, warm start slots [0, 1, 2], period A = 2,
+    # demand 0 0 0 0 1 1 2 3 0 (one clock tick per lookup, ticks 1..9).
+    # Ticks 1-7 hit: count 0/1/2 = 4/2/1, last 0/1/2 = 4/6/7.
+    # Tick 8, 3 misses: ages 4/2/1 give aged counts 4>>2 = 1, 2>>1 = 1,
+    #   1>>0 = 1; equal, so the least recent goes: 0 leaves slot 0.
+    #   (LFU would evict 2, the smallest count.)
+    # Tick 9, 0 misses: candidates 3 (count 1, age 1 -> 1), 1 (count 2, age 3
+    #   -> 2>>1 = 1), 2 (count 1, age 2 -> 1>>1 = 0): 2 leaves slot 2.
+    #   (LRU would evict 1, the least recent.)
+    seq = [0, 0, 0, 0, 1, 1, 2, 3, 0]
+    want = [(1, 0, -1)] * 4 + [(1, 1, -1)] * 2 + [(1, 2, -1), (0, 0, 0), (0, 2, 2)]
+    got = {}
+    for policy in ("lfu-aged:2", "lru", "lfu"):
+        c = LayerCache(4, 3, policy)
+        got[policy] = [(r.flags & F_HIT, r.slot, r.victim) for x in seq for r in c.access([x])]
+    assert got["lfu-aged:2"] == want
+    assert got["lru"] != want and got["lfu"] != want
+    assert LayerCache(4, 3, "lfu-aged:2").key(0)[0] == 0   # count 0 ages to 0
+
+
+def test_aged_lfu_with_a_long_period_is_lfu():
+    rng = np.random.default_rng(23)
+    for _ in range(100):
+        E = int(rng.integers(2, 12))
+        k = int(rng.integers(1, min(E, 4) + 1))
+        S = int(rng.integers(k, E + 1))
+        a, b = LayerCache(E, S, "lfu-aged:1000000"), LayerCache(E, S, "lfu")
+        for ids in _random_trace(rng, E, k, int(rng.integers(1, 100))):
+            if rng.random() < 0.3:
+                g = list(rng.choice(E, size=k, replace=False))
+                assert [r.astuple() for r in a.prefetch(g, 1)] == [r.astuple() for r in b.prefetch(g, 1)]
+            assert [r.astuple() for r in a.access(ids)] == [r.astuple() for r in b.access(ids)]
+        batch = _random_trace(rng, E, k, int(rng.integers(1, 30)))
+        assert [r.astuple() for r in a.prefill(batch)] == [r.astuple() for r in b.prefill(batch)]
+
+
+def test_aged_lfu_policy_spec():
+    from oracle.cache import parse_policy
+    assert parse_policy("lfu-aged:32") == ("lfu-aged", 32)
+    assert parse_policy("lru") == ("lru", None)
+    for bad in ("lfu-aged", "lfu-aged:0", "lfu-aged:-3", "lru:2", "mru"):
+        with pytest.raises(ValueError):
+            LayerCache(4, 2, bad)
+
+
 def test_all_slots_means_all_hits_and_persistent_routing_means_no_later_misses():
     rng = np.random.default_rng(14)
     for policy in ("lru", "lfu"):
@@ -136,7 +185,7 @@ def test_min_equals_exhaustive_on_tiny_traces():
         assert belady.min_hits(seq, S, init) == belady.exhaustive_max_hits(seq, S, init)
 
 
-@pytest.mark.parametrize("policy", ["lru", "lfu"])
+@pytest.mark.parametrize("policy", POLICIES)
 def test_policies_never_beat_min(policy):
     rng = np.random.default_rng(17)
     for _ in range(200):
@@ -224,7 +273,7 @@ def test_table2_lfu_speedup_on_a6000_is_846_percent():
 # ---- prefill residency rule ------------------------------------------------------
 def test_prefill_counts_and_residency_rule():
     rng = np.random.default_rng(22)
-    for policy in ("lfu", "lru"):
+    for policy in ("lfu", "lru", "lfu-aged:3"):
         for _ in range(100):
             E = int(rng.integers(4, 17))
             k = int(rng.integers(1, min(4, E) + 1))
@@ -243,6 +292,9 @@ def test_prefill_counts_and_residency_rule():
             # brute force R*: sort every expert by the stated key
             if policy == "lfu":
                 order = sorted(range(E), key=lambda e: (-(cnt0[e] + n[e]), e not in start, e))
+            elif policy == "lfu-aged:3":
+                aged = [(cnt0[e] + n[e]) >> ((c.clock - c.last[e]) // 3) for e in range(E)]
+                order = sorted(range(E), key=lambda e: (-aged[e], e not in start, e))
             else:
                 order = sorted(range(E), key=lambda e: (-c.last[e], e not in start, e))
             rstar = set(order[:S])
@@ -253,3 +305,25 @@ def test_prefill_counts_and_residency_rule():
             for r in recs:
                 assert bool(r.flags & F_RES_START) == (r.expert in start)
                 assert bool(r.flags & F_RES_AFTER) == (r.expert in rstar)
+
+
+def test_hand_worked_aged_lfu_prefill():
+    # E = 4, S = 2, K = 1, warm start slots [0, 1], period A = 2.  Lookups
+    # 0 0 0 (ticks 1-3: count(0) = 3, last(0) = 3), then one batch of rows
+    # 2 2 1 3 (ticks 4-7).  At tick 7: counts 3/1/2/1, last 3/6/5/7, so the
+    # aged counts are 3>>2 = 0, 1>>0 = 1, 2>>1 = 1, 1>>0 = 1.  The three
+    # tied at 1 order resident-first (1), then by id (2): R* = {1, 2}.
+    # (LFU would keep {0, 2}, LRU {3, 1}.)  Expert 1 keeps slot 1; 2 takes
+    # slot 0 from 0; 3 streams through without a slot.
+    c = LayerCache(4, 2, "lfu-aged:2")
+    for _ in range(3):
+        c.access([0])
+    recs = [r.astuple() for r in c.prefill([[2], [2], [1], [3]])]
+    assert recs == [(2, 3, 0, 0, 0, 1, -1, -1), (2, 3, 0, 1, 1, 3, 1, -1),
+                    (2, 3, 0, 2, 2, 6, 0, 0), (2, 3, 0, 1, 3, 4, -1, -1)]
+    for policy, keep in (("lfu", {0, 2}), ("lru", {1, 3})):
+        c = LayerCache(4, 2, policy)
+        for _ in range(3):
+            c.access([0])
+        c.prefill([[2], [2], [1], [3]])
+        assert set(c.resident()) == keep
