@@ -181,6 +181,12 @@ def summarize(cfg, r):
         "decode_bytes_fetched_per_step":
             (sum(s["bytes_fetched"] for s in r["stats"]) - r["prefill_bytes"]) // r["steps"],
     }
+    if not r["flags"] and not r["pre"]:
+        # Belady MIN on the same demand sequences from the same warm start:
+        # the most hits any demand-fetching policy could have had
+        out["belady_min_hit_rate"] = round(analysis.belady_hit_rate(acc, r["slots"]), 4)
+    if cfg.layers > 1:
+        out["per_layer_hit_rate"] = [round(v, 3) for v in analysis.per_layer_hit_rate(acc).values()]
     if r["flags"]:
         p, rc = analysis.guess_precision_recall(acc)
         out["guess_precision_recall"] = [round(p, 4), round(rc, 4)]
@@ -298,7 +304,7 @@ def main():
             runs.append(("lru", primary_slots, False))
     elif not args.lfu_only:
         if args.workload in ("mixtral-layer", "tiny-stack", "mixtral-layer-q2", "tiny-q2"):
-            runs.append(("lru", primary_slots, False))
+            runs += [("lru", primary_slots, False), ("lfu-aged:32", primary_slots, False)]
         elif args.workload == "mixtral-stack-q2":
             runs.append(("lfu", 4, False))
         elif args.workload == "mixtral-stack":
@@ -439,6 +445,15 @@ def main():
         },
         "router_us": round(1e3 * tim["router_ms"] / tim["router_n"], 2),
     }
+    # the whole decode step against its two rooflines: the bytes this run
+    # fetched over the host link at the measured link rate plus the selected
+    # experts' weights streamed from HBM at peak
+    ffn_step_bytes = cfg.tokens * cfg.layers * (up_bytes + down_bytes)
+    bound_s = fetched / head["steps"] / (link * 1e9) + ffn_step_bytes / (HBM_PEAK_GBPS * 1e9)
+    out["step_roofline"] = {"bound_ms_per_step": round(1e3 * bound_s, 3),
+                            "achieved_ms_per_step": round(1e3 * head["dec"] / head["steps"], 3),
+                            "frac": round(bound_s / (head["dec"] / head["steps"]), 4),
+                            "terms": "link bytes / measured link + FFN weight bytes / 8 TB/s"}
     pk = next((r for r in results if r["packed"]), None)
     if pk is not None:
         t = pk["timing"]

@@ -43,7 +43,14 @@ extern "C" {
 
 typedef struct moe_cache moe_cache_t; /* opaque, library-owned */
 
-enum { MOE_POLICY_LRU = 0, MOE_POLICY_LFU = 1 };
+/* Eviction policies.  LRU (Sec. 3.1) evicts the expert unused for longest;
+ * LFU (Sec. 4.2) the one with the smallest usage count, ties by recency.
+ * MOE_POLICY_LFU_AGED weighs popularity together with how long an expert has
+ * gone unused (the combination Sec. 6.1 proposes): its key is the usage count
+ * halved, rounding down, once per moe_model_desc.aging_ticks ticks of the
+ * layer's lookup clock since the expert's last use, evaluated at the moment of
+ * the choice (the stored count is not changed); ties by recency, then slot. */
+enum { MOE_POLICY_LRU = 0, MOE_POLICY_LFU = 1, MOE_POLICY_LFU_AGED = 2 };
 enum {
   MOE_DTYPE_F32 = 0,  /* fp32 gates and experts                                   */
   MOE_DTYPE_BF16 = 1, /* bf16 gates and experts                                   */
@@ -127,7 +134,8 @@ typedef struct {
                                      replaces host_experts, so a store can span several
                                      allocations (entries may repeat); 16-byte aligned */
   int packed_exc_cap;        /* MOE_HOST_PACKED: exception capacity per matrix       */
-  int reserved;
+  int aging_ticks;           /* MOE_POLICY_LFU_AGED: ticks per halving, >= 1;
+                                ignored by the other policies                     */
 } moe_model_desc;
 
 /* One trace record.  kind 0 (access): a token's lookup of one of its K
@@ -153,7 +161,8 @@ typedef struct {
 } moe_layer_stats;
 
 /* Create a handle for `layers` layers of `experts` experts with `slots` HBM
- * slots per layer, evicting by `policy` (Sec. 3.1 LRU, Sec. 4.2 LFU).
+ * slots per layer, evicting by `policy` (Sec. 3.1 LRU, Sec. 4.2 LFU, Sec. 6.1
+ * aged LFU; see MOE_POLICY_*).
  * MOE_ERR_ARG: layers < 1, experts < 1 or > 64, slots < 1 or > experts, bad
  * policy, out == NULL.  No GPU work. */
 int moe_cache_create(int layers, int experts, int slots, int policy, moe_cache_t **out);
@@ -188,7 +197,10 @@ int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts
 /* A batch of `tokens` rows H [tokens][d] (device fp32, in place) through one
  * layer: every row is routed and computed as a decode token would be; the
  * layer's cache takes the batch's routing at once (counts += per-expert
- * routings, then the S highest-ranked experts stay resident).  tokens must be
+ * routings, the clock ticks once per (token, rank), then the S experts with the
+ * largest key stay resident: LFU the count, aged LFU the aged count at the
+ * batch's last tick, LRU the last use; ties: resident first, lower id).  Kept
+ * experts keep their slots; newcomers take the freed slots.  tokens must be
  * in 1..max_prefill_tokens. Enqueue only. */
 int moe_prefill_layer(moe_cache_t *c, int layer, float *H, int tokens);
 

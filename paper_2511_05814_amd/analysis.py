@@ -96,3 +96,49 @@ def repeat_rate(records, layer: int) -> float:
             same += len(by_tok[a] & by_tok[b])
             total += len(by_tok[b])
     return same / total if total else 0.0
+
+
+def demand_sequences(records):
+    """Per layer, the experts of its access records in (token, rank) order."""
+    acc, _, _ = split(records)
+    by_layer = defaultdict(list)
+    for r in sorted(acc, key=lambda r: (r[2], r[1], r[3])):
+        by_layer[r[2]].append(r[4])
+    return dict(by_layer)
+
+
+def belady_hits(seq, slots: int) -> int:
+    """Hits of Belady's MIN (evict the resident expert whose next use lies
+    furthest ahead; never-again experts first, lower id first among those) on
+    one layer's demand sequence from the warm start (experts 0..slots-1
+    resident).  An upper bound for any demand-fetching policy on the same
+    sequence; next uses come from one backward pass, so the cost is
+    O(len(seq) * slots)."""
+    n = len(seq)
+    never = n  # beyond every position
+    nxt = [never] * n
+    seen = {}
+    for i in range(n - 1, -1, -1):
+        nxt[i] = seen.get(seq[i], never)
+        seen[seq[i]] = i
+    # next use of each warm-start expert from position 0
+    first = {}
+    for i, e in enumerate(seq):
+        first.setdefault(e, i)
+    resident = {e: first.get(e, never) for e in range(slots)}
+    hits = 0
+    for i, x in enumerate(seq):
+        if x in resident:
+            hits += 1
+        else:
+            victim = max(resident, key=lambda e: (resident[e], -e))
+            del resident[victim]
+        resident[x] = nxt[i]
+    return hits
+
+
+def belady_hit_rate(records, slots: int) -> float:
+    """Belady MIN hit rate over every layer's demand sequence in the trace."""
+    seqs = demand_sequences(records)
+    total = sum(len(s) for s in seqs.values())
+    return sum(belady_hits(s, slots) for s in seqs.values()) / max(1, total)

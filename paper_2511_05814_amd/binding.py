@@ -15,7 +15,7 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_lib", "libmoe_offload.so")
 
-MOE_POLICY_LRU, MOE_POLICY_LFU = 0, 1
+MOE_POLICY_LRU, MOE_POLICY_LFU, MOE_POLICY_LFU_AGED = 0, 1, 2
 MOE_DTYPE_F32, MOE_DTYPE_BF16, MOE_DTYPE_Q2G16 = 0, 1, 2
 MOE_OK, MOE_ERR_ARG, MOE_ERR_STATE, MOE_ERR_HIP, MOE_ERR_NOMEM = 0, -1, -2, -3, -4
 MOE_PREFETCH_NEXT = 1
@@ -23,7 +23,19 @@ MOE_FETCH_KERNEL, MOE_FETCH_DMA, MOE_FETCH_SPLIT = 0, 1, 2
 MOE_HOST_PLAIN, MOE_HOST_PACKED = 0, 1
 MOE_MAX_EXPERTS, MOE_MAX_TOPK = 64, 16
 
-POLICIES = {"lru": MOE_POLICY_LRU, "lfu": MOE_POLICY_LFU}
+POLICIES = {"lru": MOE_POLICY_LRU, "lfu": MOE_POLICY_LFU, "lfu-aged": MOE_POLICY_LFU_AGED}
+
+
+def parse_policy(spec: str):
+    """'lru', 'lfu' or 'lfu-aged:A' -> (MOE_POLICY_*, aging_ticks)."""
+    name, _, arg = spec.partition(":")
+    if name == "lfu-aged":
+        if not arg.isdigit() or int(arg) < 1:
+            raise ValueError(f"aged LFU needs a period of at least one tick: {spec!r}")
+        return MOE_POLICY_LFU_AGED, int(arg)
+    if name not in POLICIES or arg:
+        raise ValueError(f"unknown policy {spec!r}")
+    return POLICIES[name], 0
 DTYPES = {"f32": MOE_DTYPE_F32, "bf16": MOE_DTYPE_BF16, "q2g16": MOE_DTYPE_Q2G16}
 
 
@@ -43,7 +55,7 @@ class moe_model_desc(ctypes.Structure):
         ("workspace_bytes", ctypes.c_size_t), ("trace", ctypes.c_void_p),
         ("trace_cap", ctypes.c_size_t), ("compute_stream", ctypes.c_void_p),
         ("copy_stream", ctypes.c_void_p), ("host_layers", ctypes.POINTER(ctypes.c_void_p)),
-        ("packed_exc_cap", ctypes.c_int), ("reserved", ctypes.c_int),
+        ("packed_exc_cap", ctypes.c_int), ("aging_ticks", ctypes.c_int),
     ]
 
 

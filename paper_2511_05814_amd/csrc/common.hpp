@@ -78,6 +78,7 @@ struct RouterArgs {
   uint64_t trace_cap;
   uint64_t expert_bytes;
   int layer, L, E, S, K, d, dtype, policy;
+  int aging;               // aged LFU: lookup-clock ticks per halving of a count
   int demand;              // 1: route + look up `layer`
   int spec_layer;          // >= 0: guess that layer's experts from h and prefetch
   int pmax;                // prefetch at most this many guesses
@@ -137,6 +138,7 @@ struct PlanArgs {
   int32_t *err;
   uint64_t expert_bytes;
   int T, K, E, S, layer, policy;
+  int aging;  // aged LFU: lookup-clock ticks per halving of a count
 };
 
 // Where a kernel goes: its stream and, when kernel timing is on, two events
@@ -193,6 +195,13 @@ __device__ __forceinline__ void bf16x8_to_f32(const uint4 v, float *f) {
   f[5] = __uint_as_float(v.z & 0xFFFF0000u);
   f[6] = __uint_as_float(v.w << 16);
   f[7] = __uint_as_float(v.w & 0xFFFF0000u);
+}
+
+// Aged LFU key: the usage count halved (rounding down) once per `aging` ticks
+// between the expert's last use and `clock`.
+__device__ __forceinline__ uint32_t aged_count(uint32_t count, int64_t last, int64_t clock, int aging) {
+  const int64_t halvings = (clock - last) / aging;
+  return halvings >= 32 ? 0u : count >> (int)halvings;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

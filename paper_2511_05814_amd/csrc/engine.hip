@@ -276,6 +276,8 @@ static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
     if (d->packed_exc_cap < 0 || (uint64_t)d->packed_exc_cap > (uint64_t)d->d_model * d->d_ff)
       return fail(MOE_ERR_ARG, "packed_exc_cap out of range");
   }
+  if (c->policy == MOE_POLICY_LFU_AGED && d->aging_ticks < 1)
+    return fail(MOE_ERR_ARG, "aged LFU needs aging_ticks >= 1");
   if (d->max_prefill_tokens > 0 && d->dtype != MOE_DTYPE_BF16)
     return fail(MOE_ERR_ARG, "batched prefill runs on bf16 experts (matrix cores); dtype must be bf16");
   if ((int64_t)d->max_prefill_tokens * d->top_k > (1 << 28))
@@ -318,7 +320,8 @@ int moe_cache_create(int layers, int experts, int slots, int policy, moe_cache_t
   if (experts < 1 || experts > MOE_MAX_EXPERTS)
     return fail(MOE_ERR_ARG, "experts must be in [1, %d]", MOE_MAX_EXPERTS);
   if (slots < 1 || slots > experts) return fail(MOE_ERR_ARG, "slots must be in [1, experts]");
-  if (policy != MOE_POLICY_LRU && policy != MOE_POLICY_LFU) return fail(MOE_ERR_ARG, "bad policy");
+  if (policy != MOE_POLICY_LRU && policy != MOE_POLICY_LFU && policy != MOE_POLICY_LFU_AGED)
+    return fail(MOE_ERR_ARG, "bad policy");
   moe_cache *c = new (std::nothrow) moe_cache();
   if (!c) return fail(MOE_ERR_NOMEM, "out of host memory");
   c->L = layers;
@@ -586,6 +589,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.d = c->d;
   a.dtype = gate_dtype(c->dtype);
   a.policy = c->policy;
+  a.aging = c->policy == MOE_POLICY_LFU_AGED ? c->desc.aging_ticks : 0;
   a.demand = demand;
   a.spec_layer = spec_layer;
   a.pmax = pmax;
@@ -743,6 +747,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   pa.S = c->S;
   pa.layer = layer;
   pa.policy = c->policy;
+  pa.aging = c->policy == MOE_POLICY_LFU_AGED ? c->desc.aging_ticks : 0;
   HIP_TRY(c, launch_prefill_plan(pa, Launch{c->cs}));
   HIP_TRY(c, hipMemcpyAsync(c->h_plan, plan, sizeof(PrefillPlan) * c->E, hipMemcpyDeviceToHost, c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->cs));

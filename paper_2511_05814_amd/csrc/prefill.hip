@@ -10,8 +10,9 @@
 //              scan, scatter into expert-sorted order; the cache table takes
 //              the batch at once: counts += per-expert routings, the clock
 //              ticks once per pair, then the S highest-ranked experts stay
-//              resident (LFU: count; LRU: last use; ties: resident first,
-//              lower id); kept experts keep their slots, newcomers take the
+//              resident (LFU: count; aged LFU: the count aged to the batch's
+//              last tick; LRU: last use; ties: resident first, lower id);
+//              kept experts keep their slots, newcomers take the
 //              freed slots in ascending order
 //   3. experts the host schedules: grouped GEMMs (MFMA bf16, fp32 accumulate)
 //              on experts resident at the start, while the copy stream streams
@@ -274,12 +275,15 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
   const bool res_start = slot0 >= 0;
   count += (uint32_t)n;
   if (in_range && lastp[lane] > 0) last = clock0 + lastp[lane];
+  const int64_t clock1 = clock0 + (int64_t)P;  // the batch's last tick
 
   // R*: the S highest-ranked experts
   bool chosen = false;
   for (int s = 0; s < a.S; ++s) {
     bool cand = in_range && !chosen;
-    uint64_t k1 = a.policy == 1 ? (uint64_t)count : (uint64_t)(last + (1ll << 40));
+    uint64_t k1 = a.policy == 1   ? (uint64_t)count
+                : a.policy == 2 ? (uint64_t)aged_count(count, last, clock1, a.aging)
+                                : (uint64_t)(last + (1ll << 40));
     int k2 = res_start ? 1 : 0;
     int bl = lane, bv = cand ? 1 : 0;
 #pragma unroll
@@ -371,7 +375,7 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
     }
   }
   if (lane == 0) {
-    T->clock = clock0 + (int64_t)P;
+    T->clock = clock1;
     T->lookups = token0 + a.T;
     if (a.trace && a.trace_cap) *a.trace_count = tbase + E;
     LayerStats *st = a.stats;

@@ -12,9 +12,11 @@
 // last-use tick and prefetched flag, and the K lookups of the token are
 // applied in rank order with wave-wide argmin reductions choosing the victim
 // (LRU, Sec. 3.1: smallest last-use tick; LFU, Sec. 4.2: smallest count, then
-// last-use tick; then lower slot).  Wave 0 serves the demand lookup of this
-// layer, wave 1 the speculative insertion into the next layer's table; the
-// tables are disjoint, so the two run concurrently.
+// last-use tick; aged LFU, after Sec. 6.1: the count halved once per fixed
+// number of ticks since the last use, then last-use tick; then lower slot).
+// Wave 0 serves the demand lookup of this layer, wave 1 the speculative
+// insertion into the next layer's table; the tables are disjoint, so the two
+// run concurrently.
 #include "common.hpp"
 
 #include <math.h>
@@ -97,9 +99,14 @@ __device__ void gate_logits(const RouterArgs &a, const float *hs, int r0, int r1
 }
 
 // Lane of the resident, unpinned expert with the smallest policy key
-// (LFU: count, last, slot; LRU: last, slot), or -1 if there is none.
-__device__ int wave_victim(bool cand, int policy, uint32_t count, int64_t last, int slot) {
-  uint32_t k1 = (cand && policy == 1) ? count : 0u;
+// (LFU: count, last, slot; aged LFU: count aged to `clock`, last, slot;
+// LRU: last, slot), or -1 if there is none.
+__device__ int wave_victim(bool cand, int policy, int aging, int64_t clock, uint32_t count, int64_t last,
+                           int slot) {
+  uint32_t k1 = !cand ? 0u
+              : policy == 1 ? count
+              : policy == 2 ? aged_count(count, last, clock, aging)
+              : 0u;
   int64_t k2 = last;
   int k3 = slot;
   int bl = threadIdx.x & (kWave - 1);
@@ -183,7 +190,7 @@ __device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t
       hits += 1;
     } else {
       const bool cand = in_range && my_slot >= 0 && !pinned;
-      const int v = wave_victim(cand, a.policy, my_count, my_last, my_slot);
+      const int v = wave_victim(cand, a.policy, a.aging, clock, my_count, my_last, my_slot);
       if (v < 0) {  // cannot happen with slots >= K; refuse rather than corrupt
         if (lane == 0) *a.err = ERR_BAD_LIST;
         break;
@@ -271,7 +278,7 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
     } else if (issued < a.pmax) {
       clock += 1;
       const bool cand = in_range && my_slot >= 0 && !pinned;
-      const int v = wave_victim(cand, a.policy, my_count, my_last, my_slot);
+      const int v = wave_victim(cand, a.policy, a.aging, clock, my_count, my_last, my_slot);
       if (v < 0) {
         if (lane == 0) *a.err = ERR_BAD_LIST;
         break;

@@ -153,7 +153,8 @@ class OffloadedMoE:
         torch = _torch()
         self.cfg, self.store, self.gates = cfg, store, gates
         self.L, self.E, self.S, self.K = cfg.layers, cfg.experts, slots, cfg.top_k
-        self.handle = b.moe_cache_create(cfg.layers, cfg.experts, slots, b.POLICIES[policy])
+        policy_id, aging = b.parse_policy(policy)
+        self.handle = b.moe_cache_create(cfg.layers, cfg.experts, slots, policy_id)
         try:
             self.compute = torch.cuda.Stream()
             self.copy = torch.cuda.Stream() if separate_copy_stream else self.compute
@@ -172,6 +173,7 @@ class OffloadedMoE:
             d.max_prefill_tokens = max_prefill_tokens
             d.host_format = b.MOE_HOST_PACKED if store.packed else b.MOE_HOST_PLAIN
             d.packed_exc_cap = store.exc_cap
+            d.aging_ticks = aging
             d.gate_w = gates.ptr
             d.host_experts = None
             d.host_layers = ctypes.cast(store.layer_ptrs, ctypes.POINTER(ctypes.c_void_p))

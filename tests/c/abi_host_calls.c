@@ -45,6 +45,16 @@ int main(void) {
   CHECK(moe_cache_sync(c) == MOE_ERR_STATE);
 
   moe_cache_destroy(c);
+
+  /* aged LFU needs a halving period of at least one tick */
+  c = NULL;
+  CHECK(moe_cache_create(2, 8, 4, MOE_POLICY_LFU_AGED, &c) == MOE_OK && c != NULL);
+  d.aging_ticks = 0;
+  CHECK(moe_cache_workspace_bytes(c, &d) == 0);
+  CHECK(moe_cache_bind(c, &d) == MOE_ERR_ARG);
+  d.aging_ticks = 16;
+  CHECK(moe_cache_workspace_bytes(c, &d) > 0);
+  moe_cache_destroy(c);
   moe_cache_destroy(NULL);
   if (fails == 0) printf("ok\n");
   return fails != 0;

@@ -38,7 +38,7 @@ def test_struct_sizes_match_the_header_layout():
 
 
 @pytest.mark.parametrize("args", [
-    (0, 8, 4, 0), (2, 0, 1, 0), (2, 65, 4, 0), (2, 8, 0, 0), (2, 8, 9, 0), (2, 8, 4, 2), (2, 8, 4, -1),
+    (0, 8, 4, 0), (2, 0, 1, 0), (2, 65, 4, 0), (2, 8, 0, 0), (2, 8, 9, 0), (2, 8, 4, 3), (2, 8, 4, -1),
 ])
 def test_create_rejects_bad_arguments(args):
     with pytest.raises(b.MoeError) as e:
@@ -96,3 +96,31 @@ def test_slots_below_top_k_rejected():
         assert b.moe_cache_workspace_bytes(h, _desc(top_k=3)) == 0
     finally:
         b.moe_cache_destroy(h)
+
+
+def test_aged_lfu_needs_a_period():
+    h = b.moe_cache_create(2, 8, 4, b.MOE_POLICY_LFU_AGED)
+    try:
+        for bad in (0, -3):
+            assert b.moe_cache_workspace_bytes(h, _desc(aging_ticks=bad)) == 0
+            with pytest.raises(b.MoeError) as e:
+                b.moe_cache_bind(h, _desc(aging_ticks=bad))
+            assert e.value.code == b.MOE_ERR_ARG
+        assert b.moe_cache_workspace_bytes(h, _desc(aging_ticks=1)) > 0
+    finally:
+        b.moe_cache_destroy(h)
+    # the other policies ignore the field
+    h = b.moe_cache_create(2, 8, 4, b.MOE_POLICY_LFU)
+    try:
+        assert b.moe_cache_workspace_bytes(h, _desc(aging_ticks=0)) > 0
+    finally:
+        b.moe_cache_destroy(h)
+
+
+def test_policy_names():
+    assert b.parse_policy("lru") == (b.MOE_POLICY_LRU, 0)
+    assert b.parse_policy("lfu") == (b.MOE_POLICY_LFU, 0)
+    assert b.parse_policy("lfu-aged:32") == (b.MOE_POLICY_LFU_AGED, 32)
+    for bad in ("lfu-aged", "lfu-aged:0", "lfu:3", "mru"):
+        with pytest.raises(ValueError):
+            b.parse_policy(bad)

@@ -27,7 +27,7 @@ def tiny():
     return Rig(cfg)
 
 
-@pytest.mark.parametrize("policy", ["lru", "lfu"])
+@pytest.mark.parametrize("policy", ["lru", "lfu", "lfu-aged:2"])
 def test_tiny_stack_decode_parity(tiny, policy):
     cfg = tiny.cfg
     _say("tiny decode", policy)
@@ -48,12 +48,13 @@ def test_tiny_stack_decode_parity(tiny, policy):
     moe.close()
 
 
-def test_tiny_stack_prefetch_parity(tiny):
+@pytest.mark.parametrize("policy", ["lfu", "lfu-aged:3"])
+def test_tiny_stack_prefetch_parity(tiny, policy):
     cfg = tiny.cfg
-    _say("tiny decode lfu + prefetch 2")
-    moe = tiny.cache(4, "lfu", prefetch_max=2)
+    _say("tiny decode + prefetch 2", policy)
+    moe = tiny.cache(4, policy, prefetch_max=2)
     hs, recs, _ = tiny.run(moe, cfg.tokens, flags=b.MOE_PREFETCH_NEXT)
-    worst, unc, caches = check_decode(cfg, tiny.model, hs, recs, 4, "lfu", prefetch=True, pmax=2,
+    worst, unc, caches = check_decode(cfg, tiny.model, hs, recs, 4, policy, prefetch=True, pmax=2,
                                       tol=_tol(cfg))
     st = moe.stats()
     o = caches[1].stats
@@ -115,11 +116,11 @@ def test_reset_replays_identically(tiny):
     moe.close()
 
 
-@pytest.mark.parametrize("policy", ["lru", "lfu"])
+@pytest.mark.parametrize("policy", ["lru", "lfu", "lfu-aged:1", "lfu-aged:4"])
 def test_injected_routing_traces_match_oracle(tiny, policy):
     cfg = tiny.cfg
     _say("injected routing", policy)
-    rng = np.random.default_rng(5 if policy == "lru" else 6)
+    rng = np.random.default_rng({"lru": 5, "lfu": 6}.get(policy, 7))
     moe = tiny.cache(4, policy, trace_cap=4096)
     T = 300
     p = rng.dirichlet(np.full(cfg.experts, 0.4))
@@ -134,6 +135,13 @@ def test_injected_routing_traces_match_oracle(tiny, policy):
             want += oracle[l].access(ids[t])
     recs, _ = moe.trace_records()
     assert recs == [w.astuple() for w in want]
+    if policy.startswith("lfu-aged"):
+        # the aged key really decided evictions: plain LFU takes other victims
+        plain = [LayerCache(cfg.experts, 4, "lfu", layer=l) for l in range(cfg.layers)]
+        lfu = []
+        for t in range(T):
+            lfu += plain[t % cfg.layers].access(ids[t])
+        assert sum(a != w.astuple() for a, w in zip(recs, lfu)) > 50
     # the copies really happened: slot contents equal the host store's experts
     arena = moe.arena.cpu().numpy().reshape(cfg.layers, 4, -1)
     for l in range(cfg.layers):

@@ -60,7 +60,7 @@ def prefill_and_check(rig, moe, policy, slots, T, sample_rows, tol=2e-2):
     return h, caches, worst, unc
 
 
-@pytest.mark.parametrize("policy", ["lfu", "lru"])
+@pytest.mark.parametrize("policy", ["lfu", "lru", "lfu-aged:128"])
 def test_prefill_fine_grained_two_layers(policy):
     cfg = wl.CONFIGS["fine-grained"].with_(layers=2, tokens=10, prefill_tokens=300)
     _say("prefill fine-grained", policy, cfg)
