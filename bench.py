@@ -272,9 +272,9 @@ def main():
     ap.add_argument("--tokens", type=int, default=0,
                     help="decode only the first N tokens of the workload (profiling passes)")
     ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
-    ap.add_argument("--host-store", choices=["plain", "packed"], default="plain",
-                    help="packed: bf16 experts packed losslessly (~12.25 bits a weight) in host memory and "
-                         "rebuilt on the GPU after each copy")
+    ap.add_argument("--host-store", choices=["plain", "packed", "entropy"], default="plain",
+                    help="packed / entropy: bf16 experts coded losslessly in host memory (~12.25 / ~10.9 bits a "
+                         "weight) and rebuilt on the GPU after each copy")
     ap.add_argument("--batch", type=int, default=1,
                     help="decode B tokens per step through the batch path (bf16 experts; no speculation)")
     args = ap.parse_args()
@@ -314,17 +314,17 @@ def main():
         elif args.workload == "fine-grained":
             runs.append(("lfu", 16, False))
     # store per run: the headline's, then (bf16 batch-1 decode on the plain
-    # store) the headline's policy once more on the packed host store
-    runs = [r + (args.host_store == "packed",) for r in runs]
+    # store) the headline's policy once more on each coded host store
+    runs = [r + (args.host_store,) for r in runs]
     if (args.host_store == "plain" and cfg.dtype == "bf16" and not cfg.prefill_tokens and args.batch == 1
             and not args.lfu_only):
-        runs.append(runs[0][:3] + (True,))
+        runs += [runs[0][:3] + ("packed",), runs[0][:3] + ("entropy",)]
 
     log("generating", cfg.name, "host store", cfg.layers * cfg.experts * cfg.expert_bytes / 1e9, "GB")
     t0 = time.perf_counter()
-    if args.host_store == "packed" and (cfg.dtype != "bf16" or cfg.prefill_tokens or args.batch > 1):
-        sys.exit("the packed host store serves bf16 experts in batch-1 decode")
-    store = offload.HostStore(cfg, packed=args.host_store == "packed")
+    if args.host_store != "plain" and (cfg.dtype != "bf16" or cfg.prefill_tokens or args.batch > 1):
+        sys.exit("a coded host store serves bf16 experts in batch-1 decode")
+    store = offload.HostStore(cfg, fmt=args.host_store)
     gates = offload.DeviceGates(cfg)
     h0 = wl.hidden_states(cfg)
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s")
@@ -344,12 +344,13 @@ def main():
         return cpu_baseline(cfg, store, gates.host, h0[cfg.prefill_tokens:], cap, primary_slots, "lfu",
                             args.cpu_seconds)
 
-    for i, (policy, slots, spec, packed) in enumerate(runs):
-        if packed and not store.packed:
-            cpu = time_oracle()  # on the plain store's bytes, before it is released
-            store.close()  # both stores at once could exceed the driver's pinning cap
-            log("generating the packed host store")
-            store = offload.HostStore(cfg, packed=True)
+    for i, (policy, slots, spec, fmt) in enumerate(runs):
+        if fmt != store.fmt:
+            if cpu is None:
+                cpu = time_oracle()  # on the plain store's bytes, before it is released
+            store.close()  # two stores at once could exceed the driver's pinning cap
+            log(f"generating the {fmt} host store")
+            store = offload.HostStore(cfg, fmt=fmt)
         flags = b.MOE_PREFETCH_NEXT if spec else 0
         moe = offload.OffloadedMoE(cfg, store, gates, slots, policy,
                                    prefetch_max=cfg.prefetch_max if spec else 0, fetch_mode=fetch_mode,
@@ -360,7 +361,7 @@ def main():
         dec, pre, tim, st, recs, pbytes = run_steps(torch, b, moe, H0, H, steps, True, flags,
                                                     cfg.prefill_tokens, args.batch)
         results.append(dict(policy=policy, slots=slots, flags=flags, steps=steps, dec=dec, pre=pre,
-                            prefill_bytes=pbytes, packed=packed, expert_stride=store.expert_stride,
+                            prefill_bytes=pbytes, fmt=fmt, expert_stride=store.expert_stride,
                             timing=tim, stats=st, recs=recs))
         log(policy, slots, "prefetch" if spec else "", f"{steps * cfg.tokens / dec:.2f} tok/s")
         moe.close()
@@ -386,7 +387,7 @@ def main():
     tokens_per_s = head["steps"] * cfg.tokens / head["dec"]
     traffic = pmc_traffic() if args.workload == "mixtral-layer" else None
     summary = {f"{r['policy']}-s{r['slots']}" + ("-prefetch" if r["flags"] else "")
-               + ("-packed" if r["packed"] and not head["packed"] else ""): summarize(cfg, r)
+               + (f"-{r['fmt']}" if r["fmt"] != head["fmt"] else ""): summarize(cfg, r)
                for r in results}
 
     out = {
@@ -411,8 +412,9 @@ def main():
             "decode_tokens_per_step": cfg.tokens,
             "prefill_tokens_per_step": cfg.prefill_tokens,
             "fetch": args.fetch,
-            "host_store": ("bf16 packed losslessly, %.2f bits a weight" % (8 * head["expert_stride"] / cfg.expert_elems)
-                           if head["packed"] else cfg.dtype),
+            "host_store": ("bf16 coded losslessly (%s), %.2f bits a weight"
+                           % (head["fmt"], 8 * head["expert_stride"] / cfg.expert_elems)
+                           if head["fmt"] != "plain" else cfg.dtype),
         },
         "hit_rate": next(iter(summary.values()))["hit_rate"],
         "runs": summary,
@@ -454,13 +456,17 @@ def main():
                             "achieved_ms_per_step": round(1e3 * head["dec"] / head["steps"], 3),
                             "frac": round(bound_s / (head["dec"] / head["steps"]), 4),
                             "terms": "link bytes / measured link + FFN weight bytes / 8 TB/s"}
-    pk = next((r for r in results if r["packed"]), None)
-    if pk is not None:
+    # the kernels that rebuild bf16 experts from a coded host store
+    rebuild = {"packed": "unpack_kernel", "entropy": "entropy_unpack_kernel"}
+    for pk in results:
+        if pk["fmt"] == "plain" or rebuild[pk["fmt"]] in out.get("unpack", {}):
+            continue
         t = pk["timing"]
-        out["unpack"] = {"kernel": "unpack_kernel", "run": "headline" if pk is head else "packed comparison run",
-                         "avg_launch_us": round(1e3 * t["unpack_ms"] / max(1, t["unpack_n"]), 2),
-                         "launches": t["unpack_n"], "bytes_per_expert_moved": pk["expert_stride"],
-                         "bytes_per_expert_rebuilt": cfg.expert_bytes}
+        out.setdefault("unpack", {})[rebuild[pk["fmt"]]] = {
+            "run": "headline" if pk is head else f"{pk['fmt']} comparison run",
+            "avg_launch_us": round(1e3 * t["unpack_ms"] / max(1, t["unpack_n"]), 2),
+            "launches": t["unpack_n"], "bytes_per_expert_moved": pk["expert_stride"],
+            "bytes_per_expert_rebuilt": cfg.expert_bytes}
     if cfg.prefill_tokens:
         mf = {"bound": "mfma", "unit": "TFLOP/s", "peak": MFMA_BF16_PEAK_TFLOPS,
               "gemm_launches": tim["gemm_up_n"] + tim["gemm_down_n"],

@@ -84,7 +84,7 @@ enum {
 /* Layout of the pinned host store (moe_model_desc.host_format). */
 enum {
   MOE_HOST_PLAIN = 0,  /* experts stored as dtype, exactly as in the HBM slots   */
-  MOE_HOST_PACKED = 1  /* bf16 experts packed losslessly to ~12.25 bits a weight:
+  MOE_HOST_PACKED = 1, /* bf16 experts packed losslessly to ~12.25 bits a weight:
                           each of W1, W3, W2 (n = d_model * d_ff weights) is cut
                           into blocks of 8192 weights of 12560 bytes each:
                             16-byte header: uint32 first exception of the
@@ -97,9 +97,33 @@ enum {
                           ((index in block) << 8) | exponent, for every weight
                           whose offset would be 15 or more (stored offset 15);
                           the matrix is padded to a capacity of
-                          blocks * 12560 + 4 * packed_exc_cap bytes rounded up
+                          blocks * 12560 + 4 * packed_cap bytes rounded up
                           to 16, and an expert is W1 | W3 | W2 at that stride.
                           Copies move the packed bytes; a kernel on the copy
+                          stream rebuilds the identical bf16 expert in its slot.
+                          Needs dtype bf16 and max_prefill_tokens = 0.       */
+  MOE_HOST_ENTROPY = 2 /* bf16 experts with entropy-coded exponents, ~10.9 bits
+                          a weight for N(0, sigma) weights: each of W1, W3, W2
+                          (n = d_model * d_ff weights, n a multiple of 512) is
+                            512 bytes: 256 uint16 decode entries
+                              (length << 8) | exponent, indexed by the next 8
+                              bits of a stream (0 where no code starts);
+                            one uint32 per span of 32768 weights (the last
+                              may be short), padded to 16 bytes: the span's
+                              first word in the stream area;
+                            n bytes (sign << 7) | mantissa, in weight order;
+                            packed_cap uint32 words of streams: the exponent
+                              of weight 32768 s + 512 j + 8 l + u (l < 64,
+                              u < 8) is code 8 j + u of lane stream l of span
+                              s; canonical prefix codes of at most 8 bits,
+                              first bit in the lowest free bit; word k of lane
+                              stream l sits at the span's first word + 64 k +
+                              l, over as many rows as the span's longest lane
+                              stream needs (shorter ones padded with zeros);
+                          the matrix occupies moe_entropy_matrix_bytes(n,
+                          packed_cap) bytes and an expert is W1 | W3 | W2 at
+                          that stride.  moe_entropy_pack writes this layout.
+                          Copies move the coded bytes; a kernel on the copy
                           stream rebuilds the identical bf16 expert in its slot.
                           Needs dtype bf16 and max_prefill_tokens = 0.       */
 };
@@ -133,7 +157,8 @@ typedef struct {
                                      [E][W1|W3|W2] at host_layers[l]; when non-NULL it
                                      replaces host_experts, so a store can span several
                                      allocations (entries may repeat); 16-byte aligned */
-  int packed_exc_cap;        /* MOE_HOST_PACKED: exception capacity per matrix       */
+  int packed_cap;            /* per matrix: MOE_HOST_PACKED exception entries,
+                                MOE_HOST_ENTROPY stream words                        */
   int aging_ticks;           /* MOE_POLICY_LFU_AGED: ticks per halving, >= 1;
                                 ignored by the other policies                     */
 } moe_model_desc;
@@ -258,6 +283,22 @@ void moe_cache_destroy(moe_cache_t *c);
  * from both host and device.  moe_host_free(NULL) is a no-op. */
 int moe_host_alloc(size_t bytes, void **out);
 int moe_host_free(void *p);
+
+/* Bytes one matrix of n weights occupies in a MOE_HOST_ENTROPY store whose
+ * lane streams have room for cap_words words (the layout is described at
+ * MOE_HOST_ENTROPY); 0 if n is 0 or not a multiple of 512. */
+size_t moe_entropy_matrix_bytes(size_t n, size_t cap_words);
+
+/* Encode one matrix of n bf16 weights (host memory, row-major bit patterns)
+ * into the MOE_HOST_ENTROPY layout at out (host memory of
+ * moe_entropy_matrix_bytes(n, cap_words) bytes, e.g. inside a pinned store),
+ * with prefix codes built from this matrix's exponent counts (optimal among
+ * codes of at most 8 bits).  *used receives the stream words the matrix
+ * needs.  MOE_ERR_ARG: NULL pointers, n not a positive multiple of 512, or
+ * the streams need more than cap_words words (out is then unspecified).
+ * Host-only, no GPU work; different matrices may be encoded from different
+ * threads at once. */
+int moe_entropy_pack(const uint16_t *w, size_t n, size_t cap_words, void *out, size_t *used);
 
 /* Thread-local message of the last failure on this thread ("" if none). */
 const char *moe_last_error(void);

@@ -20,7 +20,7 @@ MOE_DTYPE_F32, MOE_DTYPE_BF16, MOE_DTYPE_Q2G16 = 0, 1, 2
 MOE_OK, MOE_ERR_ARG, MOE_ERR_STATE, MOE_ERR_HIP, MOE_ERR_NOMEM = 0, -1, -2, -3, -4
 MOE_PREFETCH_NEXT = 1
 MOE_FETCH_KERNEL, MOE_FETCH_DMA, MOE_FETCH_SPLIT = 0, 1, 2
-MOE_HOST_PLAIN, MOE_HOST_PACKED = 0, 1
+MOE_HOST_PLAIN, MOE_HOST_PACKED, MOE_HOST_ENTROPY = 0, 1, 2
 MOE_MAX_EXPERTS, MOE_MAX_TOPK = 64, 16
 
 POLICIES = {"lru": MOE_POLICY_LRU, "lfu": MOE_POLICY_LFU, "lfu-aged": MOE_POLICY_LFU_AGED}
@@ -55,7 +55,7 @@ class moe_model_desc(ctypes.Structure):
         ("workspace_bytes", ctypes.c_size_t), ("trace", ctypes.c_void_p),
         ("trace_cap", ctypes.c_size_t), ("compute_stream", ctypes.c_void_p),
         ("copy_stream", ctypes.c_void_p), ("host_layers", ctypes.POINTER(ctypes.c_void_p)),
-        ("packed_exc_cap", ctypes.c_int), ("aging_ticks", ctypes.c_int),
+        ("packed_cap", ctypes.c_int), ("aging_ticks", ctypes.c_int),
     ]
 
 
@@ -108,6 +108,9 @@ _SIGNATURES = [
     ("moe_cache_destroy", None, [ctypes.c_void_p]),
     ("moe_host_alloc", ctypes.c_int, [ctypes.c_size_t, ctypes.POINTER(ctypes.c_void_p)]),
     ("moe_host_free", ctypes.c_int, [ctypes.c_void_p]),
+    ("moe_entropy_matrix_bytes", ctypes.c_size_t, [ctypes.c_size_t, ctypes.c_size_t]),
+    ("moe_entropy_pack", ctypes.c_int,
+     [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_void_p, ctypes.POINTER(ctypes.c_size_t)]),
     ("moe_last_error", ctypes.c_char_p, []),
 ]
 EXPORTED = [s[0] for s in _SIGNATURES]
@@ -237,3 +240,15 @@ def moe_host_alloc(nbytes: int) -> int:
 
 def moe_host_free(ptr: int) -> None:
     _check(lib().moe_host_free(ptr), "moe_host_free")
+
+
+def moe_entropy_matrix_bytes(n: int, cap_words: int) -> int:
+    return lib().moe_entropy_matrix_bytes(n, cap_words)
+
+
+def moe_entropy_pack(w_ptr: int, n: int, cap_words: int, out_ptr: int) -> int:
+    """Encode n bf16 weights at host address w_ptr into out_ptr; returns the
+    stream words used."""
+    used = ctypes.c_size_t()
+    _check(lib().moe_entropy_pack(w_ptr, n, cap_words, out_ptr, ctypes.byref(used)), "moe_entropy_pack")
+    return used.value

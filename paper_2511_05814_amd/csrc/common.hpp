@@ -162,6 +162,15 @@ hipError_t launch_fetch(const FetchList *list, const uint8_t *const *layers, uin
 // as bf16 into their slots; n = weights per matrix.
 hipError_t launch_unpack(const FetchList *list, const uint8_t *staging, uint8_t *arena, int L, int S, int K,
                          uint64_t mat_cap, uint64_t expert_bytes, uint64_t n, int32_t *err, const Launch &l);
+// Entropy-coded experts (host format 2): the same, from the entropy layout
+// with cap_words stream words per matrix.
+hipError_t launch_entropy_unpack(const FetchList *list, const uint8_t *staging, uint8_t *arena, int L, int S, int K,
+                                 uint64_t mat_cap, uint64_t expert_bytes, uint64_t n, uint64_t cap_words,
+                                 int32_t *err, const Launch &l);
+// Bytes of one entropy-coded matrix (0 unless n is a positive multiple of 512)
+// and the host encoder (0, or -1 with *why set).
+uint64_t entropy_matrix_bytes(uint64_t n, uint64_t cap_words);
+int entropy_pack(const uint16_t *w, uint64_t n, uint64_t cap_words, uint8_t *out, uint64_t *used, const char **why);
 hipError_t launch_ffn_up(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_down(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, const Launch &l);

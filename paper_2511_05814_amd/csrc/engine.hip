@@ -220,6 +220,16 @@ int prefill_routing(moe_cache *c, int32_t *ids, float *g, size_t cap, size_t *n)
     if (_e != hipSuccess) return fail(MOE_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(_e)); \
   } while (0)
 
+// The kernel that rebuilds the bf16 experts of a fetch list from a coded
+// host store's bytes in staging.
+static hipError_t launch_rebuild(const moe_cache *c, const FetchList *list, const Launch &l) {
+  uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
+  if (c->host_format == MOE_HOST_ENTROPY)
+    return launch_entropy_unpack(list, c->staging, arena, c->L, c->S, c->K, c->mat_cap, c->B, c->n_mat,
+                                 (uint64_t)c->desc.packed_cap, c->err, l);
+  return launch_unpack(list, c->staging, arena, c->L, c->S, c->K, c->mat_cap, c->B, c->n_mat, c->err, l);
+}
+
 static int check_ready(const moe_cache *c) {
   if (!c) return fail(MOE_ERR_ARG, "NULL handle");
   if (!c->bound) return fail(MOE_ERR_STATE, "handle is not bound (call moe_cache_bind)");
@@ -235,17 +245,23 @@ static uint64_t expert_bytes(const moe_model_desc *d) {
   return 3 * n * (d->dtype == MOE_DTYPE_BF16 ? 2 : 4);
 }
 
-// Packed host store (MOE_HOST_PACKED): blocks of 8192 weights in 12560 bytes,
-// then packed_exc_cap exception words, per matrix, rounded up to 16 bytes.
-static uint64_t packed_matrix_bytes(const moe_model_desc *d) {
+// Bytes of one matrix in a coded host store.  MOE_HOST_PACKED: blocks of 8192
+// weights in 12560 bytes, then packed_cap exception words, rounded up to 16
+// bytes; MOE_HOST_ENTROPY: see entropy_matrix_bytes.
+static uint64_t coded_matrix_bytes(const moe_model_desc *d) {
   const uint64_t n = (uint64_t)d->d_model * d->d_ff;
+  if (d->host_format == MOE_HOST_ENTROPY) return entropy_matrix_bytes(n, (uint64_t)d->packed_cap);
   const uint64_t nb = (n + 8191) / 8192;
-  return (nb * 12560 + 4ull * (uint64_t)d->packed_exc_cap + 15) / 16 * 16;
+  return (nb * 12560 + 4ull * (uint64_t)d->packed_cap + 15) / 16 * 16;
+}
+
+static bool coded_store(int host_format) {
+  return host_format == MOE_HOST_PACKED || host_format == MOE_HOST_ENTROPY;
 }
 
 // Stride of one expert in the host store: the bytes one miss moves.
 static uint64_t host_expert_bytes(const moe_model_desc *d) {
-  return d->host_format == MOE_HOST_PACKED ? 3 * packed_matrix_bytes(d) : expert_bytes(d);
+  return coded_store(d->host_format) ? 3 * coded_matrix_bytes(d) : expert_bytes(d);
 }
 
 // Element type of the gate: fp32 for fp32 models, bf16 otherwise (router dtype code).
@@ -268,13 +284,17 @@ static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
   if (d->fetch_mode != MOE_FETCH_KERNEL && d->fetch_mode != MOE_FETCH_DMA && d->fetch_mode != MOE_FETCH_SPLIT)
     return fail(MOE_ERR_ARG, "bad fetch_mode");
   if (d->max_prefill_tokens < 0) return fail(MOE_ERR_ARG, "max_prefill_tokens < 0");
-  if (d->host_format != MOE_HOST_PLAIN && d->host_format != MOE_HOST_PACKED)
+  if (d->host_format != MOE_HOST_PLAIN && !coded_store(d->host_format))
     return fail(MOE_ERR_ARG, "bad host_format");
-  if (d->host_format == MOE_HOST_PACKED) {
-    if (d->dtype != MOE_DTYPE_BF16) return fail(MOE_ERR_ARG, "a packed host store holds bf16 experts");
-    if (d->max_prefill_tokens > 0) return fail(MOE_ERR_ARG, "a packed host store serves decode only");
-    if (d->packed_exc_cap < 0 || (uint64_t)d->packed_exc_cap > (uint64_t)d->d_model * d->d_ff)
-      return fail(MOE_ERR_ARG, "packed_exc_cap out of range");
+  if (coded_store(d->host_format)) {
+    if (d->dtype != MOE_DTYPE_BF16) return fail(MOE_ERR_ARG, "a coded host store holds bf16 experts");
+    if (d->max_prefill_tokens > 0) return fail(MOE_ERR_ARG, "a coded host store serves decode only");
+    const uint64_t n = (uint64_t)d->d_model * d->d_ff;
+    if (d->host_format == MOE_HOST_PACKED && (d->packed_cap < 0 || (uint64_t)d->packed_cap > n))
+      return fail(MOE_ERR_ARG, "packed_cap out of range");
+    if (d->host_format == MOE_HOST_ENTROPY && (n % 512 || d->packed_cap < 1 || (uint64_t)d->packed_cap > n))
+      return fail(MOE_ERR_ARG, "an entropy-coded store needs d_model * d_ff a multiple of 512 and "
+                               "packed_cap in [1, d_model * d_ff]");
   }
   if (c->policy == MOE_POLICY_LFU_AGED && d->aging_ticks < 1)
     return fail(MOE_ERR_ARG, "aged LFU needs aging_ticks >= 1");
@@ -304,7 +324,7 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff, d->dtype) * d->d_model);
   const uint64_t B = expert_bytes(d);
   l.prefill = take(prefill_layout(d->top_k, d->d_model, d->d_ff, c->E, c->S, d->max_prefill_tokens, B).total);
-  l.staging = take(d->host_format == MOE_HOST_PACKED ? (size_t)d->top_k * host_expert_bytes(d) : 0);
+  l.staging = take(coded_store(d->host_format) ? (size_t)d->top_k * host_expert_bytes(d) : 0);
   l.total = off;
   return l;
 }
@@ -385,7 +405,7 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->B = expert_bytes(d);
   c->host_format = d->host_format;
   c->Bh = host_expert_bytes(d);
-  c->mat_cap = d->host_format == MOE_HOST_PACKED ? packed_matrix_bytes(d) : 0;
+  c->mat_cap = coded_store(d->host_format) ? coded_matrix_bytes(d) : 0;
   c->n_mat = (uint64_t)d->d_model * d->d_ff;
   c->cs = static_cast<hipStream_t>(d->compute_stream);
   c->xs = d->copy_stream ? static_cast<hipStream_t>(d->copy_stream) : c->cs;
@@ -402,7 +422,7 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->act = reinterpret_cast<float *>(c->ws + lay.act);
   c->part = reinterpret_cast<float *>(c->ws + lay.part);
   c->prefill_ws = c->ws + lay.prefill;
-  c->staging = d->host_format == MOE_HOST_PACKED ? c->ws + lay.staging : nullptr;
+  c->staging = coded_store(d->host_format) ? c->ws + lay.staging : nullptr;
   c->dev_layers = reinterpret_cast<const uint8_t *const *>(c->ws + lay.hostptrs);
   c->dev_layer_host = dl;
   HIP_TRY0(hipMemcpy(c->ws + lay.hostptrs, dl.data(), sizeof(void *) * c->L, hipMemcpyHostToDevice));
@@ -472,8 +492,8 @@ int moe_cache_reset(moe_cache_t *c) {
   }
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
-  if (c->host_format == MOE_HOST_PACKED) {
-    // copy each packed expert to staging and rebuild it in its slot, through
+  if (coded_store(c->host_format)) {
+    // copy each coded expert to staging and rebuild it in its slot, through
     // the layer's demand list (cleared again afterwards)
     for (int l = 0; l < c->L; ++l)
       for (int s = 0; s < c->S; ++s) {
@@ -484,8 +504,7 @@ int moe_cache_reset(moe_cache_t *c) {
         f.slot[0] = s;
         HIP_TRY(c, hipMemcpy(c->dl + l, &f, sizeof f, hipMemcpyHostToDevice));
         HIP_TRY(c, hipMemcpy(c->staging, c->host_layer[l] + (size_t)s * c->Bh, c->Bh, hipMemcpyHostToDevice));
-        HIP_TRY(c, launch_unpack(c->dl + l, c->staging, arena, c->L, c->S, c->K, c->mat_cap, c->B, c->n_mat,
-                                 c->err, Launch{c->xs}));
+        HIP_TRY(c, launch_rebuild(c, c->dl + l, Launch{c->xs}));
         HIP_TRY(c, hipStreamSynchronize(c->xs));
       }
     HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.dlists, 0, sizeof(FetchList) * c->L, c->xs));
@@ -494,7 +513,9 @@ int moe_cache_reset(moe_cache_t *c) {
     HIP_TRY(c, hipStreamSynchronize(c->xs));
     if (e != ERR_NONE) {
       c->sticky = MOE_ERR_ARG;
-      return fail(MOE_ERR_ARG, "packed host store is corrupt (an exception entry is missing)");
+      return fail(MOE_ERR_ARG, c->host_format == MOE_HOST_PACKED
+                                   ? "packed host store is corrupt (an exception entry is missing)"
+                                   : "entropy-coded host store is corrupt (a stream holds no valid code)");
     }
   } else {
     for (int l = 0; l < c->L; ++l)
@@ -519,15 +540,14 @@ int moe_cache_reset(moe_cache_t *c) {
 static int unpack_list(moe_cache *c, FetchList *list, hipStream_t q) {
   Launch l;
   HIP_TRY(c, kernel_span(c, q, &l));
-  HIP_TRY(c, launch_unpack(list, c->staging, static_cast<uint8_t *>(c->desc.arena), c->L, c->S, c->K, c->mat_cap,
-                           c->B, c->n_mat, c->err, l));
+  HIP_TRY(c, launch_rebuild(c, list, l));
   kernel_span_done(c, SPAN_UNPACK, l);
   return MOE_OK;
 }
 
 static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_t q) {
   const bool by_kernel = c->fetch_mode == MOE_FETCH_KERNEL || (c->fetch_mode == MOE_FETCH_SPLIT && mirror_idx == 0);
-  const bool packed = c->host_format == MOE_HOST_PACKED;
+  const bool packed = coded_store(c->host_format);
   if (by_kernel) {
     Launch l;
     HIP_TRY(c, kernel_span(c, q, &l));
@@ -1128,6 +1148,17 @@ int moe_host_free(void *p) {
   if (!p) return MOE_OK;
   hipError_t e = hipHostFree(p);
   if (e != hipSuccess) return fail(MOE_ERR_HIP, "hipHostFree failed: %s", hipGetErrorString(e));
+  return MOE_OK;
+}
+
+size_t moe_entropy_matrix_bytes(size_t n, size_t cap_words) { return entropy_matrix_bytes(n, cap_words); }
+
+int moe_entropy_pack(const uint16_t *w, size_t n, size_t cap_words, void *out, size_t *used) {
+  if (!w || !out || !used) return fail(MOE_ERR_ARG, "NULL pointer");
+  const char *why = "";
+  uint64_t u = 0;
+  if (entropy_pack(w, n, cap_words, static_cast<uint8_t *>(out), &u, &why) != 0) return fail(MOE_ERR_ARG, "%s", why);
+  *used = u;
   return MOE_OK;
 }
 

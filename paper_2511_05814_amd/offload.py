@@ -17,7 +17,7 @@ from typing import Optional
 import numpy as np
 
 from . import binding as b
-from . import pack
+from . import entropy, pack
 from . import workload as wl
 
 
@@ -39,25 +39,40 @@ class HostStore:
     of layer l mod distinct: every fetch still moves a whole expert over the
     host link, only the weight values repeat (gates stay per layer).
 
-    packed=True stores bf16 experts in the lossless packed format of
-    paper_2511_05814_amd.pack (about 12.25 bits a weight); exc_cap is the
-    exception capacity of every matrix (default n / 4096 + 64, about three
-    times what N(0, sigma) weights need)."""
+    fmt selects how bf16 experts are held (the GPU rebuilds identical bf16
+    weights after each copy, so fewer bytes cross the host link per miss):
+    "plain" (as stored in HBM), "packed" (paper_2511_05814_amd.pack, about
+    12.25 bits a weight; `cap` = exception entries per matrix, default
+    n / 4096 + 64, about three times what N(0, sigma) weights need) or
+    "entropy" (paper_2511_05814_amd.entropy, about 10.9 bits a weight; `cap`
+    = stream words per matrix, by default 1% above what the first matrix of
+    the store needs).
+    packed=True is the same as fmt="packed"."""
+
+    FORMATS = ("plain", "packed", "entropy")
 
     def __init__(self, cfg: wl.Config, fill: bool = True, workers: Optional[int] = None,
-                 max_pinned_bytes: int = 64 << 30, packed: bool = False, exc_cap: Optional[int] = None):
+                 max_pinned_bytes: int = 64 << 30, packed: bool = False, fmt: Optional[str] = None,
+                 cap: Optional[int] = None):
         self.cfg = cfg
-        self.packed = packed
-        if packed:
-            if cfg.dtype != "bf16":
-                raise ValueError("the packed host store holds bf16 experts")
-            n = cfg.matrix_elems
-            self.exc_cap = exc_cap if exc_cap is not None else n // 4096 + 64
-            self.matrix_stride = pack.matrix_capacity(n, self.exc_cap)
-            self.expert_stride = 3 * self.matrix_stride
+        fmt = fmt or ("packed" if packed else "plain")
+        if fmt not in self.FORMATS:
+            raise ValueError(f"unknown host store format {fmt!r}")
+        self.fmt = fmt
+        self.packed = fmt != "plain"   # a coded store: copies move coded bytes
+        n = cfg.matrix_elems
+        if self.packed and cfg.dtype != "bf16":
+            raise ValueError("a coded host store holds bf16 experts")
+        if fmt == "packed":
+            self.cap = cap if cap is not None else n // 4096 + 64
+            self.matrix_stride = pack.matrix_capacity(n, self.cap)
+        elif fmt == "entropy":
+            self.cap = cap if cap is not None else self._entropy_cap(cfg)
+            self.matrix_stride = entropy.matrix_capacity(n, self.cap)
         else:
-            self.exc_cap = 0
-            self.expert_stride = cfg.expert_bytes
+            self.cap = 0
+            self.matrix_stride = cfg.matrix_bytes
+        self.expert_stride = 3 * self.matrix_stride
         self.layer_bytes = cfg.experts * self.expert_stride
         self.distinct = int(max(1, min(cfg.layers, max_pinned_bytes // self.layer_bytes)))
         self.nbytes = self.distinct * self.layer_bytes
@@ -91,7 +106,10 @@ class HostStore:
                 row = self.arrays[l].reshape(cfg.experts, self.expert_stride)[e]
                 for m in range(3):
                     dst = row[m * self.matrix_stride:(m + 1) * self.matrix_stride]
-                    pack.pack_matrix(raw[m * n:(m + 1) * n], self.exc_cap, out=dst)
+                    if self.fmt == "entropy":
+                        entropy.pack_matrix(raw[m * n:(m + 1) * n], self.cap, dst)
+                    else:
+                        pack.pack_matrix(raw[m * n:(m + 1) * n], self.cap, out=dst)
                 return
             view = self.arrays[l].view(sdt).reshape(cfg.experts, cfg.expert_storage_len)
             wl.fill_expert(cfg, l, e, view[e])
@@ -99,6 +117,18 @@ class HostStore:
         workers = workers or max(1, min(16, os.cpu_count() or 1))
         with ThreadPoolExecutor(workers) as ex:
             list(ex.map(one, todo))
+
+    @staticmethod
+    def _entropy_cap(cfg: wl.Config) -> int:
+        """Stream words per matrix: what W1 of expert (0, 0) needs plus 2% and
+        one row (64 words) per span.  Every matrix of the generator has the
+        same distribution; what varies is mostly the padding of each span to
+        its longest lane stream, well within that margin."""
+        n = cfg.matrix_elems
+        probe = entropy.default_cap_words(n)
+        buf = np.empty(entropy.matrix_capacity(n, probe), dtype=np.uint8)
+        used = entropy.pack_matrix(wl.expert_matrix(cfg, 0, 0, 0), probe, buf)
+        return used + used // 50 + 64 * entropy.spans(n)
 
     @property
     def aliased(self) -> bool:
@@ -171,8 +201,9 @@ class OffloadedMoE:
             d.prefetch_max = prefetch_max
             d.fetch_mode = fetch_mode
             d.max_prefill_tokens = max_prefill_tokens
-            d.host_format = b.MOE_HOST_PACKED if store.packed else b.MOE_HOST_PLAIN
-            d.packed_exc_cap = store.exc_cap
+            d.host_format = {"plain": b.MOE_HOST_PLAIN, "packed": b.MOE_HOST_PACKED,
+                             "entropy": b.MOE_HOST_ENTROPY}[store.fmt]
+            d.packed_cap = store.cap
             d.aging_ticks = aging
             d.gate_w = gates.ptr
             d.host_experts = None

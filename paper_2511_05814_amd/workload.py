@@ -236,6 +236,16 @@ def fill_expert(cfg: Config, layer: int, expert: int, out: np.ndarray) -> None:
             _draw_into(_rng(cfg, tag, layer, expert), part, cfg.dtype)
 
 
+def expert_matrix(cfg: Config, layer: int, expert: int, j: int) -> np.ndarray:
+    """Matrix j (0 W1, 1 W3, 2 W2) of expert (layer, expert), flat, in the
+    storage dtype of a bf16 or fp32 model: the same values fill_expert writes."""
+    if cfg.dtype == "q2g16":
+        raise ValueError("quantised experts are drawn whole")
+    out = np.empty(cfg.matrix_elems, dtype=_storage_dtype(cfg))
+    _draw_into(_rng(cfg, (TAG_W1, TAG_W3, TAG_W2)[j], layer, expert), out, cfg.dtype)
+    return out
+
+
 def expert_weights(cfg: Config, layer: int, expert: int) -> np.ndarray:
     out = np.empty(cfg.expert_storage_len, dtype=_storage_dtype(cfg))
     fill_expert(cfg, layer, expert, out)

@@ -56,6 +56,21 @@ int main(void) {
   CHECK(moe_cache_workspace_bytes(c, &d) > 0);
   moe_cache_destroy(c);
   moe_cache_destroy(NULL);
+
+  /* entropy-coded matrices: sizes and argument errors (host-only calls) */
+  {
+    static uint16_t w[512];
+    static uint8_t out[8192 + 256 + 512 + 4 * 64 + 16];
+    size_t used = 0;
+    int i;
+    CHECK(moe_entropy_matrix_bytes(1000, 10) == 0);
+    CHECK(moe_entropy_matrix_bytes(512, 64) == 512 + 16 + 512 + 4 * 64);
+    for (i = 0; i < 512; ++i) w[i] = (uint16_t)(0x3F80 + (i % 3) * 0x80 + (i % 128));
+    CHECK(moe_entropy_pack(w, 512, 64, out, &used) == MOE_OK && used > 0 && used <= 64);
+    CHECK(moe_entropy_pack(w, 500, 64, out, &used) == MOE_ERR_ARG);
+    CHECK(moe_entropy_pack(w, 512, 1, out, &used) == MOE_ERR_ARG);
+    CHECK(moe_entropy_pack(NULL, 512, 64, out, &used) == MOE_ERR_ARG);
+  }
   if (fails == 0) printf("ok\n");
   return fails != 0;
 }

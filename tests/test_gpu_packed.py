@@ -1,6 +1,7 @@
-"""The packed host store (lossless ~12.25-bit bf16 experts rebuilt on the GPU
-after each copy) must give exactly what the plain bf16 store gives: the same
-outputs bit for bit and the same cache traces, with fewer bytes per miss."""
+"""The coded host stores (lossless bf16 experts rebuilt on the GPU after each
+copy: the ~12.25-bit packed format and the ~10.9-bit entropy-coded one) must
+give exactly what the plain bf16 store gives: the same outputs bit for bit
+and the same cache traces, with fewer bytes per miss."""
 import numpy as np
 import pytest
 
@@ -26,15 +27,15 @@ def run(cfg, store, gates, slots, policy, tokens, flags=0, **kw):
     return H.cpu().numpy(), recs, st
 
 
-def compare(cfg, slots, policy, tokens, modes, pmax):
+def compare(cfg, slots, policy, tokens, modes, pmax, fmt="packed"):
     gates = offload.DeviceGates(cfg)
     plain = offload.HostStore(cfg)
-    packed = offload.HostStore(cfg, packed=True)
+    packed = offload.HostStore(cfg, fmt=fmt)
     assert packed.expert_stride < cfg.expert_bytes
     flags = b.MOE_PREFETCH_NEXT if pmax else 0
     ref = run(cfg, plain, gates, slots, policy, tokens, flags, prefetch_max=pmax)
     for mode in modes:
-        _say("packed store, fetch mode", mode)
+        _say(fmt, "store, fetch mode", mode)
         H, recs, st = run(cfg, packed, gates, slots, policy, tokens, flags, prefetch_max=pmax, fetch_mode=mode)
         assert H.tobytes() == ref[0].tobytes()
         assert recs == ref[1]
@@ -46,9 +47,10 @@ def compare(cfg, slots, policy, tokens, modes, pmax):
     packed.close()
 
 
-def test_packed_store_matches_plain_all_fetch_modes():
+@pytest.mark.parametrize("fmt", ["packed", "entropy"])
+def test_packed_store_matches_plain_all_fetch_modes(fmt):
     cfg = wl.CONFIGS["tiny-stack"].with_(dtype="bf16", tokens=40)
-    compare(cfg, 4, "lfu", cfg.tokens, (b.MOE_FETCH_SPLIT, b.MOE_FETCH_KERNEL, b.MOE_FETCH_DMA), pmax=2)
+    compare(cfg, 4, "lfu", cfg.tokens, (b.MOE_FETCH_SPLIT, b.MOE_FETCH_KERNEL, b.MOE_FETCH_DMA), pmax=2, fmt=fmt)
 
 
 def test_packed_store_ragged_shape_partial_block():
@@ -58,9 +60,17 @@ def test_packed_store_ragged_shape_partial_block():
     compare(cfg, 3, "lru", cfg.tokens, (b.MOE_FETCH_SPLIT, b.MOE_FETCH_DMA), pmax=1)
 
 
-def test_packed_store_mixtral_layer():
+def test_entropy_store_ragged_shape_short_last_span():
+    # n = 192 * 320 = 61440 weights per matrix: the second span has 56 of 64 steps
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=3, experts=5, top_k=3, d_model=192, d_ff=320,
+                                         dtype="bf16", tokens=20)
+    compare(cfg, 3, "lru", cfg.tokens, (b.MOE_FETCH_SPLIT, b.MOE_FETCH_DMA), pmax=1, fmt="entropy")
+
+
+@pytest.mark.parametrize("fmt", ["packed", "entropy"])
+def test_packed_store_mixtral_layer(fmt):
     cfg = wl.CONFIGS["mixtral-layer"].with_(tokens=16)
-    compare(cfg, 4, "lfu", cfg.tokens, (b.MOE_FETCH_SPLIT,), pmax=0)
+    compare(cfg, 4, "lfu", cfg.tokens, (b.MOE_FETCH_SPLIT,), pmax=0, fmt=fmt)
 
 
 def test_corrupt_packed_store_is_reported():
@@ -74,6 +84,19 @@ def test_corrupt_packed_store_is_reported():
     first_block_hdr = row[:16].view("<u4")
     assert row[nb * 12560:store.matrix_stride].view("<u4").any() or first_block_hdr[1] > 0
     row[nb * 12560:store.matrix_stride] = 0xFF
+    with pytest.raises(b.MoeError) as e:
+        offload.OffloadedMoE(cfg, store, gates, 4, "lfu")
+    assert e.value.code == b.MOE_ERR_ARG and "corrupt" in str(e.value)
+    store.close()
+
+
+def test_corrupt_entropy_store_is_reported():
+    cfg = wl.CONFIGS["tiny-stack"].with_(dtype="bf16", layers=1, tokens=4)
+    gates = offload.DeviceGates(cfg)
+    store = offload.HostStore(cfg, fmt="entropy")
+    # expert 1, W3: a decode table with no codes
+    row = store.arrays[0].reshape(cfg.experts, store.expert_stride)[1]
+    row[store.matrix_stride:store.matrix_stride + 8192] = 0
     with pytest.raises(b.MoeError) as e:
         offload.OffloadedMoE(cfg, store, gates, 4, "lfu")
     assert e.value.code == b.MOE_ERR_ARG and "corrupt" in str(e.value)
