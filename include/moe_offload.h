@@ -101,7 +101,7 @@ enum {
                           to 16, and an expert is W1 | W3 | W2 at that stride.
                           Copies move the packed bytes; a kernel on the copy
                           stream rebuilds the identical bf16 expert in its slot.
-                          Needs dtype bf16 and max_prefill_tokens = 0.       */
+                          Needs dtype bf16.                                   */
   MOE_HOST_ENTROPY = 2 /* bf16 experts with entropy-coded exponents, ~10.9 bits
                           a weight for N(0, sigma) weights: each of W1, W3, W2
                           (n = d_model * d_ff weights, n a multiple of 512) is
@@ -125,7 +125,7 @@ enum {
                           that stride.  moe_entropy_pack writes this layout.
                           Copies move the coded bytes; a kernel on the copy
                           stream rebuilds the identical bf16 expert in its slot.
-                          Needs dtype bf16 and max_prefill_tokens = 0.       */
+                          Needs dtype bf16.                                   */
 };
 
 /* Limits of this build. */

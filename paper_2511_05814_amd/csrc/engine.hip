@@ -54,12 +54,16 @@ namespace moe {
 // Prefill workspace for batches of up to T tokens (offsets from its base).
 struct PrefillLayout {
   size_t ids = 0, g = 0, inv_r = 0, xn = 0, perm = 0, pos = 0, plan = 0, jobs = 0, tiles = 0, act = 0,
-         y = 0, staging = 0, total = 0;
+         y = 0, staging = 0, coded = 0, lists = 0, total = 0;
   int tile_cap = 0;  // GEMM tiles the schedule can hold
   int ring = 0;      // staging slots for experts streamed through the batch
 };
+// fetch lists one prefill layer can need with a coded host store
+constexpr int kPrefillLists = 2 * kMaxE + 2;
 
-static PrefillLayout prefill_layout(int K, int d, int d_ff, int E, int S, int T, uint64_t B) {
+// Bh > 0: a coded host store, whose experts are copied to `coded` (room for
+// half a ring) and rebuilt from there through device-side fetch lists.
+static PrefillLayout prefill_layout(int K, int d, int d_ff, int E, int S, int T, uint64_t B, uint64_t Bh) {
   PrefillLayout p;
   if (T <= 0) return p;
   size_t off = 0;
@@ -86,6 +90,8 @@ static PrefillLayout prefill_layout(int K, int d, int d_ff, int E, int S, int T,
   p.act = take(P * d_ff * 2);
   p.y = take(P * d * 4);
   p.staging = take((size_t)p.ring * B);
+  p.coded = take(Bh ? (size_t)(p.ring / 2) * Bh : 0);
+  p.lists = take(Bh ? sizeof(FetchList) * kPrefillLists : 0);
   p.total = off;
   return p;
 }
@@ -220,14 +226,20 @@ int prefill_routing(moe_cache *c, int32_t *ids, float *g, size_t cap, size_t *n)
     if (_e != hipSuccess) return fail(MOE_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(_e)); \
   } while (0)
 
-// The kernel that rebuilds the bf16 experts of a fetch list from a coded
-// host store's bytes in staging.
-static hipError_t launch_rebuild(const moe_cache *c, const FetchList *list, const Launch &l) {
-  uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
+// The kernel that rebuilds the bf16 experts of a fetch list (at most `max_n`
+// entries) from a coded host store's bytes at `coded` (entry i at
+// coded + i * Bh) into dst + (list layer * S + list slot) * B.
+static hipError_t launch_rebuild(const moe_cache *c, const FetchList *list, const uint8_t *coded, uint8_t *dst,
+                                 int L, int S, int max_n, const Launch &l) {
   if (c->host_format == MOE_HOST_ENTROPY)
-    return launch_entropy_unpack(list, c->staging, arena, c->L, c->S, c->K, c->mat_cap, c->B, c->n_mat,
+    return launch_entropy_unpack(list, coded, dst, L, S, max_n, c->mat_cap, c->B, c->n_mat,
                                  (uint64_t)c->desc.packed_cap, c->err, l);
-  return launch_unpack(list, c->staging, arena, c->L, c->S, c->K, c->mat_cap, c->B, c->n_mat, c->err, l);
+  return launch_unpack(list, coded, dst, L, S, max_n, c->mat_cap, c->B, c->n_mat, c->err, l);
+}
+
+// ... into the HBM slots of the list's layer, from the decode staging area
+static hipError_t launch_rebuild(const moe_cache *c, const FetchList *list, const Launch &l) {
+  return launch_rebuild(c, list, c->staging, static_cast<uint8_t *>(c->desc.arena), c->L, c->S, c->K, l);
 }
 
 static int check_ready(const moe_cache *c) {
@@ -288,7 +300,6 @@ static int validate_desc(const moe_cache *c, const moe_model_desc *d) {
     return fail(MOE_ERR_ARG, "bad host_format");
   if (coded_store(d->host_format)) {
     if (d->dtype != MOE_DTYPE_BF16) return fail(MOE_ERR_ARG, "a coded host store holds bf16 experts");
-    if (d->max_prefill_tokens > 0) return fail(MOE_ERR_ARG, "a coded host store serves decode only");
     const uint64_t n = (uint64_t)d->d_model * d->d_ff;
     if (d->host_format == MOE_HOST_PACKED && (d->packed_cap < 0 || (uint64_t)d->packed_cap > n))
       return fail(MOE_ERR_ARG, "packed_cap out of range");
@@ -323,7 +334,8 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff, d->dtype) * d->d_model);
   const uint64_t B = expert_bytes(d);
-  l.prefill = take(prefill_layout(d->top_k, d->d_model, d->d_ff, c->E, c->S, d->max_prefill_tokens, B).total);
+  const uint64_t Bh_coded = coded_store(d->host_format) ? host_expert_bytes(d) : 0;
+  l.prefill = take(prefill_layout(d->top_k, d->d_model, d->d_ff, c->E, c->S, d->max_prefill_tokens, B, Bh_coded).total);
   l.staging = take(coded_store(d->host_format) ? (size_t)d->top_k * host_expert_bytes(d) : 0);
   l.total = off;
   return l;
@@ -441,11 +453,12 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->mirror), 3 * sizeof(FetchList),
                                  hipHostMallocDefault));
   if (c->max_T > 0) {
-    c->play = prefill_layout(c->K, c->d, c->dff, c->E, c->S, c->max_T, c->B);
+    c->play = prefill_layout(c->K, c->d, c->dff, c->E, c->S, c->max_T, c->B, coded_store(c->host_format) ? c->Bh : 0);
     HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->h_plan), sizeof(PrefillPlan) * kMaxE,
                            hipHostMallocDefault));
     HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->h_sched),
-                           sizeof(GemmJob) * kMaxE + sizeof(GemmTile) * (size_t)c->play.tile_cap,
+                           sizeof(GemmJob) * kMaxE + sizeof(GemmTile) * (size_t)c->play.tile_cap +
+                               sizeof(FetchList) * kPrefillLists,
                            hipHostMallocDefault));
     c->pf_ev.assign(2 * kMaxE + 4, nullptr);
     for (auto &e : c->pf_ev) HIP_TRY0(hipEventCreateWithFlags(&e, hipEventDisableTiming));
@@ -760,7 +773,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   pa.trace_count = c->trace_count;
   pa.trace_cap = c->desc.trace ? c->desc.trace_cap : 0;
   pa.err = c->err;
-  pa.expert_bytes = c->B;
+  pa.expert_bytes = c->Bh;  // bytes one fetch moves (counters)
   pa.T = T;
   pa.K = c->K;
   pa.E = c->E;
@@ -849,8 +862,53 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     c->sticky = MOE_ERR_HIP;
     return fail(MOE_ERR_HIP, "prefill tile schedule overflow (%d > %d)", nt, p.tile_cap);
   }
+  // A coded host store's experts are copied to the coded staging area and
+  // rebuilt from there by a kernel that reads a device-side fetch list: per
+  // batch one list for experts bound to their new slots and one for experts
+  // bound to the ring, then the unrouted newcomers in lists of up to `half`.
+  const bool coded = coded_store(c->host_format);
+  struct Part {
+    int list = -1;
+    bool ring = false;
+    std::vector<int> experts;
+  };
+  std::vector<std::vector<Part>> batch_parts(batches.size());
+  std::vector<Part> unrouted_parts;
+  FetchList *hl = reinterpret_cast<FetchList *>(c->h_sched + sizeof(GemmJob) * kMaxE +
+                                                sizeof(GemmTile) * (size_t)p.tile_cap);
+  FetchList *dlists = reinterpret_cast<FetchList *>(base + p.lists);
+  int nl = 0;
+  auto add_part = [&](std::vector<Part> &parts, const std::vector<int> &ex, bool ring) {
+    if (ex.empty()) return;
+    Part pt;
+    pt.list = nl++;
+    pt.ring = ring;
+    pt.experts = ex;
+    FetchList &f = hl[pt.list];
+    std::memset(&f, 0, sizeof f);
+    f.n = (int)ex.size();
+    f.layer = ring ? 0 : layer;
+    for (size_t i = 0; i < ex.size(); ++i) {
+      f.expert[i] = ex[i];
+      f.slot[i] = ring ? ring_of[ex[i]] : pl[ex[i]].slot_after;
+    }
+    parts.push_back(pt);
+  };
+  if (coded) {
+    for (size_t bi = 0; bi < batches.size(); ++bi) {
+      std::vector<int> to_slot, to_ring;
+      for (int e : batches[bi]) (pl[e].slot_after >= 0 ? to_slot : to_ring).push_back(e);
+      add_part(batch_parts[bi], to_slot, false);
+      add_part(batch_parts[bi], to_ring, true);
+    }
+    for (size_t i = 0; i < unrouted_new.size(); i += half)
+      add_part(unrouted_parts,
+               std::vector<int>(unrouted_new.begin() + i, unrouted_new.begin() + std::min(unrouted_new.size(), i + half)),
+               false);
+  }
   HIP_TRY(c, hipMemcpyAsync(jobs, hj, sizeof(GemmJob) * kMaxE, hipMemcpyHostToDevice, c->cs));
   if (nt > 0) HIP_TRY(c, hipMemcpyAsync(tiles, ht, sizeof(GemmTile) * nt, hipMemcpyHostToDevice, c->cs));
+  if (nl > 0) HIP_TRY(c, hipMemcpyAsync(dlists, hl, sizeof(FetchList) * nl, hipMemcpyHostToDevice, c->cs));
 
   const double up_flop_per_row = 4.0 * c->d * c->dff, down_flop_per_row = 2.0 * c->d * c->dff;
   auto run_group = [&](size_t gi) -> int {
@@ -869,28 +927,48 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     int rc = run_group(0);
     if (rc != MOE_OK) return rc;
   }
-  HIP_TRY(c, hipEventRecord(evA, c->cs));
+  HIP_TRY(c, hipEventRecord(evA, c->cs));  // also orders the schedule uploads before any copy
   hipStream_t q = c->xs;
   bool waited_A = false;
+  uint8_t *coded_stage = base + p.coded;
+  // copies (and, for a coded store, the rebuild) of one part of a batch
+  auto stream_part = [&](const Part &pt) -> int {
+    for (size_t i = 0; i < pt.experts.size(); ++i) {
+      const int e = pt.experts[i];
+      HIP_TRY(c, hipMemcpyAsync(coded_stage + i * c->Bh, host + (size_t)e * c->Bh, c->Bh, hipMemcpyHostToDevice, q));
+    }
+    Launch lr;
+    HIP_TRY(c, kernel_span(c, q, &lr));
+    HIP_TRY(c, pt.ring ? launch_rebuild(c, dlists + pt.list, coded_stage, staging, 1, p.ring, half, lr)
+                       : launch_rebuild(c, dlists + pt.list, coded_stage, arena, c->L, c->S, half, lr));
+    kernel_span_done(c, SPAN_UNPACK, lr);
+    return MOE_OK;
+  };
   for (size_t bi = 0; bi < batches.size(); ++bi) {
     hipEvent_t evC = c->pf_ev[2 + 2 * (bi % kMaxE)], evG = c->pf_ev[3 + 2 * (bi % kMaxE)];
     bool waited_ring = false;
     for (int e : batches[bi]) {
-      uint8_t *dst;
       if (pl[e].slot_after >= 0) {
         if (!waited_A) {
           HIP_TRY(c, hipStreamWaitEvent(q, evA, 0));
           waited_A = true;
         }
-        dst = arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B;
-      } else {
-        if (!waited_ring && bi >= 2) {
-          HIP_TRY(c, hipStreamWaitEvent(q, c->pf_ev[3 + 2 * ((bi - 2) % kMaxE)], 0));
-          waited_ring = true;
-        }
-        dst = staging + (size_t)ring_of[e] * c->B;
+      } else if (!waited_ring && bi >= 2) {
+        HIP_TRY(c, hipStreamWaitEvent(q, c->pf_ev[3 + 2 * ((bi - 2) % kMaxE)], 0));
+        waited_ring = true;
       }
+      if (coded) continue;  // streamed part by part below
+      uint8_t *dst = pl[e].slot_after >= 0 ? arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B
+                                           : staging + (size_t)ring_of[e] * c->B;
       HIP_TRY(c, hipMemcpyAsync(dst, host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
+    }
+    if (coded && !waited_A) {  // the lists were uploaded before event A
+      HIP_TRY(c, hipStreamWaitEvent(q, evA, 0));
+      waited_A = true;
+    }
+    for (const Part &pt : batch_parts[bi]) {
+      int rc = stream_part(pt);
+      if (rc != MOE_OK) return rc;
     }
     HIP_TRY(c, hipEventRecord(evC, q));
     HIP_TRY(c, hipStreamWaitEvent(c->cs, evC, 0));
@@ -900,9 +978,16 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   }
   if (!unrouted_new.empty()) {
     if (!waited_A) HIP_TRY(c, hipStreamWaitEvent(q, evA, 0));
-    for (int e : unrouted_new)
-      HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B,
-                                host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
+    if (coded) {
+      for (const Part &pt : unrouted_parts) {
+        int rc = stream_part(pt);
+        if (rc != MOE_OK) return rc;
+      }
+    } else {
+      for (int e : unrouted_new)
+        HIP_TRY(c, hipMemcpyAsync(arena + ((size_t)layer * c->S + pl[e].slot_after) * c->B,
+                                  host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
+    }
   }
   HIP_TRY(c, hipEventRecord(evF, q));
   HIP_TRY(c, hipStreamWaitEvent(c->cs, evF, 0));
@@ -985,6 +1070,8 @@ int moe_cache_sync(moe_cache_t *c) {
   }
   if (e != ERR_NONE) {
     c->sticky = MOE_ERR_HIP;
+    if (e == ERR_BAD_PACK)
+      return fail(MOE_ERR_HIP, "coded host store is corrupt (an expert could not be rebuilt)");
     return fail(MOE_ERR_HIP, "device reported an inconsistent fetch list (code %d)", e);
   }
   return MOE_OK;

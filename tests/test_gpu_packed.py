@@ -101,3 +101,37 @@ def test_corrupt_entropy_store_is_reported():
         offload.OffloadedMoE(cfg, store, gates, 4, "lfu")
     assert e.value.code == b.MOE_ERR_ARG and "corrupt" in str(e.value)
     store.close()
+
+
+@pytest.mark.parametrize("fmt", ["packed", "entropy"])
+def test_coded_store_prefill_then_decode_matches_plain(fmt):
+    # the 64-expert shape: a 300-token batched prefill streams the experts it
+    # routes to (into their new slots or the staging ring), then decode with
+    # next-layer prefetch continues from the prefilled caches
+    cfg = wl.CONFIGS["fine-grained"].with_(layers=2, tokens=6, prefill_tokens=300)
+    gates = offload.DeviceGates(cfg)
+    h = np.ascontiguousarray(wl.hidden_states(cfg, 300 + cfg.tokens))
+
+    def go(store):
+        moe = offload.OffloadedMoE(cfg, store, gates, 16, "lfu", prefetch_max=2, max_prefill_tokens=300)
+        H = torch.from_numpy(h).to("cuda")
+        moe.prefill(H[:300])
+        moe.decode(H[300:], flags=b.MOE_PREFETCH_NEXT)
+        moe.sync()
+        recs, dropped = moe.trace_records()
+        assert dropped == 0
+        st = moe.stats()
+        moe.close()
+        return H.cpu().numpy(), recs, st
+
+    plain = offload.HostStore(cfg)
+    ref = go(plain)
+    plain.close()
+    _say(fmt, "store, prefill + decode")
+    coded = offload.HostStore(cfg, fmt=fmt)
+    H, recs, st = go(coded)
+    assert H.tobytes() == ref[0].tobytes()
+    assert recs == ref[1]
+    for a, c in zip(st, ref[2]):
+        assert a["bytes_fetched"] * cfg.expert_bytes == c["bytes_fetched"] * coded.expert_stride
+    coded.close()
