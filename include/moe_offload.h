@@ -72,13 +72,14 @@ enum {
   MOE_FETCH_KERNEL = 0, /* a copy kernel on the copy stream reads the host store
                            directly; no host round trip per layer            */
   MOE_FETCH_DMA = 1,    /* the host waits for the routing decision, then issues
-                           one DMA-engine copy per missed expert              */
+                           one runtime copy (hipMemcpyAsync) per missed expert */
   MOE_FETCH_SPLIT = 2   /* demand misses by the copy kernel (no host round
                            trip on the critical path); speculative prefetches
-                           by the DMA engines, which read host memory without
-                           slowing the FFN kernels that run meanwhile. The
-                           host reads each prefetch list back on a stream the
-                           library owns, after enqueueing the layer's FFN.   */
+                           by runtime copies (hipMemcpyAsync), which do not
+                           slow the FFN kernels that run meanwhile the way the
+                           copy kernel's host reads do.  The host reads each
+                           prefetch list back on a stream the library owns,
+                           after enqueueing the layer's FFN.                  */
 };
 
 /* Layout of the pinned host store (moe_model_desc.host_format). */

@@ -697,7 +697,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   }
   if (spec_layer >= 0 && split) {
     // The prefetch list comes back on the library's own stream, so neither the
-    // FFN just enqueued nor the demand copies wait for the host; the DMA copies
+    // FFN just enqueued nor the demand copies wait for the host; the runtime copies
     // then queue on the copy stream behind this layer's demand copies.
     hipStream_t m = c->ms ? c->ms : c->cs;
     int32_t *err_mirror = reinterpret_cast<int32_t *>(&c->mirror[2]);
