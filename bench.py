@@ -383,7 +383,8 @@ def main():
     up_gbps = up_bytes / (up_ms * 1e-3) / 1e9
     down_gbps = down_bytes / (down_ms * 1e-3) / 1e9
     fetched = sum(s["bytes_fetched"] for s in head["stats"]) - head["prefill_bytes"]  # decode only
-    fetch_gbps = fetched / (tim["fetch_ms"] * 1e-3) / 1e9 if tim["fetch_ms"] > 0 else None
+    copy_ms = tim["fetch_ms"] + tim["pf_fetch_ms"]  # demand and speculative copies
+    fetch_gbps = fetched / (copy_ms * 1e-3) / 1e9 if copy_ms > 0 else None
     tokens_per_s = head["steps"] * cfg.tokens / head["dec"]
     traffic = pmc_traffic() if args.workload == "mixtral-layer" else None
     summary = {f"{r['policy']}-s{r['slots']}" + ("-prefetch" if r["flags"] else "")
@@ -456,6 +457,19 @@ def main():
                             "achieved_ms_per_step": round(1e3 * head["dec"] / head["steps"], 3),
                             "frac": round(bound_s / (head["dec"] / head["steps"]), 4),
                             "terms": "link bytes / measured link + FFN weight bytes / 8 TB/s"}
+    # how the copies overlap the compute: the compute stream's wait between
+    # each router and its FFN against the copy time (demand + speculative)
+    steps = head["steps"]
+    dec_ms = 1e3 * head["dec"] / steps
+    out["copy_overlap"] = {
+        "demand_copy_ms_per_step": round(tim["fetch_ms"] / steps, 2),
+        "prefetch_copy_ms_per_step": round(tim["pf_fetch_ms"] / steps, 2),
+        "compute_wait_ms_per_step": round(tim["wait_ms"] / steps, 2),
+        "link_busy_frac": round(copy_ms / steps / dec_ms, 4) if not cfg.prefill_tokens else None,
+        "hidden_copy_frac": round(max(0.0, 1.0 - tim["wait_ms"] / copy_ms), 4) if copy_ms > 0 else None,
+        "definition": "hidden_copy_frac = 1 - compute wait / copy time: the share of the copy time "
+                      "(demand + speculative) during which the compute stream was not waiting",
+    }
     # the kernels that rebuild bf16 experts from a coded host store
     rebuild = {"packed": "unpack_kernel", "entropy": "entropy_unpack_kernel"}
     for pk in results:

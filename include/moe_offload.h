@@ -264,14 +264,20 @@ typedef struct {
       ffn_reduce_ms;
   uint64_t router_n, fetch_n, ffn_up_n, ffn_down_n, prefill_n, gemm_up_n, gemm_down_n, ffn_reduce_n;
   double gemm_up_flop, gemm_down_flop; /* algorithmic flops of the timed GEMM launches */
-  double unpack_ms;                    /* MOE_HOST_PACKED: rebuilding copied experts  */
+  double unpack_ms;                    /* coded host stores: rebuilding copied experts */
   uint64_t unpack_n;
+  double wait_ms;     /* decode: compute stream from each router's end to the FFN's start,
+                         i.e. waiting for the copies that fill the layer's slots        */
+  uint64_t wait_n;
+  double pf_fetch_ms; /* speculative (next-layer) copies; fetch_ms counts demand copies */
+  uint64_t pf_fetch_n;
 } moe_timing;
 
 /* Kernel timing with HIP events, off by default.  While enabled, every router,
  * fetch, decode FFN and prefill grouped-GEMM launch is bracketed by a pair of
  * events on the stream it runs on (prefill_ms spans a whole layer's prefill on
- * the compute stream, waits for streamed experts included).
+ * the compute stream, waits for streamed experts included; wait_ms spans the
+ * compute stream's wait for copies between a decode router and its FFN).
  * moe_cache_read_timing syncs, returns the summed durations (ms), launch
  * counts and GEMM flops since the previous read, and clears them. */
 int moe_cache_set_timing(moe_cache_t *c, int enable);

@@ -78,7 +78,8 @@ class moe_timing(ctypes.Structure):
                    ("router_n", "fetch_n", "ffn_up_n", "ffn_down_n", "prefill_n", "gemm_up_n",
                     "gemm_down_n", "ffn_reduce_n")]
                 + [(n, ctypes.c_double) for n in ("gemm_up_flop", "gemm_down_flop", "unpack_ms")]
-                + [("unpack_n", ctypes.c_uint64)])
+                + [("unpack_n", ctypes.c_uint64), ("wait_ms", ctypes.c_double), ("wait_n", ctypes.c_uint64),
+                   ("pf_fetch_ms", ctypes.c_double), ("pf_fetch_n", ctypes.c_uint64)])
 
 
 # (name, restype, argtypes) of every exported function, in header order

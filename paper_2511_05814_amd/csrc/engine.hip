@@ -150,7 +150,7 @@ struct moe_cache {
 namespace moe {
 enum SpanKind {
   SPAN_ROUTER = 0, SPAN_FETCH, SPAN_UP, SPAN_DOWN, SPAN_PREFILL, SPAN_GEMM_UP, SPAN_GEMM_DOWN, SPAN_REDUCE,
-  SPAN_UNPACK, SPAN_KINDS
+  SPAN_UNPACK, SPAN_WAIT, SPAN_PF_FETCH, SPAN_KINDS
 };
 
 // Start/stop a timed span on stream s (no-op unless timing is on).
@@ -561,12 +561,13 @@ static int unpack_list(moe_cache *c, FetchList *list, hipStream_t q) {
 static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_t q) {
   const bool by_kernel = c->fetch_mode == MOE_FETCH_KERNEL || (c->fetch_mode == MOE_FETCH_SPLIT && mirror_idx == 0);
   const bool packed = coded_store(c->host_format);
+  const int kind = mirror_idx == 1 ? SPAN_PF_FETCH : SPAN_FETCH;  // speculative or demand copies
   if (by_kernel) {
     Launch l;
     HIP_TRY(c, kernel_span(c, q, &l));
     HIP_TRY(c, launch_fetch(list, c->dev_layers, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
                             c->K, c->B, c->Bh, c->staging, c->err, l));
-    kernel_span_done(c, SPAN_FETCH, l);
+    kernel_span_done(c, kind, l);
     return packed ? unpack_list(c, list, q) : MOE_OK;
   }
   const FetchList &m = c->mirror[mirror_idx];
@@ -588,7 +589,7 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
     uint8_t *dst = packed ? c->staging + (size_t)i * c->Bh : arena + ((size_t)m.layer * c->S + s) * c->B;
     HIP_TRY(c, hipMemcpyAsync(dst, host + (size_t)e * c->Bh, c->Bh, hipMemcpyHostToDevice, q));
   }
-  HIP_TRY(c, span_end(c, q, SPAN_FETCH, t0));
+  HIP_TRY(c, span_end(c, q, kind, t0));
   return packed ? unpack_list(c, list, q) : MOE_OK;
 }
 
@@ -630,6 +631,10 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   HIP_TRY(c, kernel_span(c, c->cs, &lr));
   HIP_TRY(c, launch_router(a, lr));
   kernel_span_done(c, SPAN_ROUTER, lr);
+  // from the router's end to the FFN's start: the compute stream's wait for
+  // the copies that fill this layer's slots
+  hipEvent_t t_wait = nullptr;
+  if (ffn) HIP_TRY(c, span_begin(c, c->cs, &t_wait));
 
   hipStream_t q = c->xs;
   const bool split = c->fetch_mode == MOE_FETCH_SPLIT;
@@ -683,6 +688,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     f.d = c->d;
     f.d_ff = c->dff;
     f.phase = 0;
+    HIP_TRY(c, span_end(c, c->cs, SPAN_WAIT, t_wait));
     Launch lu, ld, lx;
     HIP_TRY(c, kernel_span(c, c->cs, &lu));
     HIP_TRY(c, launch_ffn_up(f, c->dtype, lu));
@@ -1172,10 +1178,12 @@ int moe_cache_read_timing(moe_cache_t *c, moe_timing *out) {
   if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
   double *ms[SPAN_KINDS] = {&out->router_ms,  &out->fetch_ms,     &out->ffn_up_ms,
                             &out->ffn_down_ms, &out->prefill_ms,   &out->gemm_up_ms,
-                            &out->gemm_down_ms, &out->ffn_reduce_ms, &out->unpack_ms};
+                            &out->gemm_down_ms, &out->ffn_reduce_ms, &out->unpack_ms,
+                            &out->wait_ms,     &out->pf_fetch_ms};
   uint64_t *n[SPAN_KINDS] = {&out->router_n,  &out->fetch_n,     &out->ffn_up_n,
                              &out->ffn_down_n, &out->prefill_n,   &out->gemm_up_n,
-                             &out->gemm_down_n, &out->ffn_reduce_n, &out->unpack_n};
+                             &out->gemm_down_n, &out->ffn_reduce_n, &out->unpack_n,
+                             &out->wait_n,     &out->pf_fetch_n};
   int rc = MOE_OK;
   for (const auto &sp : c->spans) {
     float t = 0.0f;
