@@ -338,11 +338,20 @@ def main():
     cpu = None
 
     def time_oracle():
+        """(all host threads, one thread) oracle timings; one thread only for
+        the one- and two-layer workloads, on a quarter of the time budget."""
         if args.no_cpu_baseline:
             return None
+        from threadpoolctl import threadpool_limits
         cap = min(args.cpu_tokens, cfg.tokens) if args.cpu_tokens > 0 else cfg.tokens
-        return cpu_baseline(cfg, store, gates.host, h0[cfg.prefill_tokens:], cap, primary_slots, "lfu",
+        full = cpu_baseline(cfg, store, gates.host, h0[cfg.prefill_tokens:], cap, primary_slots, "lfu",
                             args.cpu_seconds)
+        one = None
+        if cfg.layers <= 2:
+            with threadpool_limits(limits=1):
+                one = cpu_baseline(cfg, store, gates.host, h0[cfg.prefill_tokens:], cap, primary_slots, "lfu",
+                                   args.cpu_seconds / 4)
+        return full, one
 
     for i, (policy, slots, spec, fmt) in enumerate(runs):
         if fmt != store.fmt:
@@ -495,11 +504,15 @@ def main():
     if cpu is None:
         cpu = time_oracle()
     if cpu is not None:
-        tps, n, dt, thr = cpu
-        out["cpu_baseline"] = {"value": round(tps, 4), "unit": "tokens/s", "cores": thr, "kind": "oracle",
-                               "sample": f"first {n} of the {cfg.tokens} decode tokens (a {args.cpu_seconds:g} s "
-                                         f"budget), fp64 router + LFU cache + SwiGLU FFN through all {cfg.layers} "
-                                         f"layers from the warm start (bf16->fp64 widening included), {dt:.1f} s"}
+        for key, res, budget in (("cpu_baseline", cpu[0], args.cpu_seconds),
+                                 ("cpu_baseline_1thread", cpu[1], args.cpu_seconds / 4)):
+            if res is None:
+                continue
+            tps, n, dt, thr = res
+            out[key] = {"value": round(tps, 4), "unit": "tokens/s", "cores": thr, "kind": "oracle",
+                        "sample": f"first {n} of the {cfg.tokens} decode tokens (a {budget:g} s budget), fp64 "
+                                  f"router + LFU cache + SwiGLU FFN through all {cfg.layers} layers from the warm "
+                                  f"start (bf16->fp64 widening included), {dt:.1f} s"}
     store.close()
     print(json.dumps(out), flush=True)
 
