@@ -886,6 +886,10 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   int nl = 0;
   auto add_part = [&](std::vector<Part> &parts, const std::vector<int> &ex, bool ring) {
     if (ex.empty()) return;
+    if (nl >= kPrefillLists || (int)ex.size() > kMaxK) {  // cannot happen: at most 48 lists of <= 4 experts
+      nl = kPrefillLists + 1;
+      return;
+    }
     Part pt;
     pt.list = nl++;
     pt.ring = ring;
@@ -911,6 +915,10 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       add_part(unrouted_parts,
                std::vector<int>(unrouted_new.begin() + i, unrouted_new.begin() + std::min(unrouted_new.size(), i + half)),
                false);
+  }
+  if (nl > kPrefillLists) {
+    c->sticky = MOE_ERR_HIP;
+    return fail(MOE_ERR_HIP, "prefill fetch-list overflow");
   }
   HIP_TRY(c, hipMemcpyAsync(jobs, hj, sizeof(GemmJob) * kMaxE, hipMemcpyHostToDevice, c->cs));
   if (nt > 0) HIP_TRY(c, hipMemcpyAsync(tiles, ht, sizeof(GemmTile) * nt, hipMemcpyHostToDevice, c->cs));
