@@ -181,15 +181,15 @@ hipError_t launch_ffnq_down(const FfnArgs &a, const Launch &l);
 int ffnq_down_chunks(int K, int d_ff);
 hipError_t launch_prefill_gate(const PrefillArgs &a, const Launch &l);
 hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l);
+// grouped GEMMs over tiles of `rows` (64 or 128) sorted pairs by
+// prefill_tile_cols() output columns
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l);
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l);
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, const Launch &l);
+                               float *Y, int d, int d_ff, int rows, const Launch &l);
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
                                     int d, int K, const Launch &l);
-int prefill_tile_rows();       // GEMM output tile: rows (sorted pairs) ...
-int prefill_tile_cols_up();    // ... columns of act per up tile
-int prefill_tile_cols_down();  // ... columns of Y per down tile
+int prefill_tile_cols();  // GEMM output tile columns (act for up, Y for down)
 
 // ---------------------------------------------------------------------------
 // device helpers

@@ -844,9 +844,22 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       }
     }
   }
-  const int rows = prefill_tile_rows(), cols_up = prefill_tile_cols_up(), cols_down = prefill_tile_cols_down();
+  // Output tiles of 128 rows (sorted pairs) by 128 columns; a launch that
+  // would not give every CU two of them takes 64-row tiles instead.
+  const int cols = prefill_tile_cols();
+  int cus = 0;
+  {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    (void)hipGetLastError();
+  }
   int nt = 0;
-  auto add_tiles = [&](const std::vector<int> &group, int ncols, int cols, int &first, int &count) {
+  auto add_tiles = [&](const std::vector<int> &group, int ncols, int &first, int &count, int &rows) {
+    long big = 0;
+    for (int e : group) big += (long)((pl[e].n + 127) / 128) * ((ncols + cols - 1) / cols);
+    rows = big < 2L * cus ? 64 : 128;
     first = nt;
     for (int e : group)
       for (int m0 = 0; m0 < pl[e].n; m0 += rows)
@@ -854,14 +867,15 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     count = nt - first;
   };
   const size_t ngroups = batches.size() + 1;
-  std::vector<int> up_first(ngroups), up_n(ngroups), dn_first(ngroups), dn_n(ngroups);
+  std::vector<int> up_first(ngroups), up_n(ngroups), dn_first(ngroups), dn_n(ngroups), up_rows(ngroups),
+      dn_rows(ngroups);
   std::vector<double> group_rows(ngroups, 0.0);
-  add_tiles(resident, c->dff, cols_up, up_first[0], up_n[0]);
-  add_tiles(resident, c->d, cols_down, dn_first[0], dn_n[0]);
+  add_tiles(resident, c->dff, up_first[0], up_n[0], up_rows[0]);
+  add_tiles(resident, c->d, dn_first[0], dn_n[0], dn_rows[0]);
   for (int e : resident) group_rows[0] += pl[e].n;
   for (size_t bi = 0; bi < batches.size(); ++bi) {
-    add_tiles(batches[bi], c->dff, cols_up, up_first[bi + 1], up_n[bi + 1]);
-    add_tiles(batches[bi], c->d, cols_down, dn_first[bi + 1], dn_n[bi + 1]);
+    add_tiles(batches[bi], c->dff, up_first[bi + 1], up_n[bi + 1], up_rows[bi + 1]);
+    add_tiles(batches[bi], c->d, dn_first[bi + 1], dn_n[bi + 1], dn_rows[bi + 1]);
     for (int e : batches[bi]) group_rows[bi + 1] += pl[e].n;
   }
   if (nt > p.tile_cap) {
@@ -929,10 +943,10 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     if (up_n[gi] <= 0) return MOE_OK;
     Launch lu, ld;
     HIP_TRY(c, kernel_span(c, c->cs, &lu));
-    HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, lu));
+    HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, up_rows[gi], lu));
     kernel_span_done(c, SPAN_GEMM_UP, lu, group_rows[gi] * up_flop_per_row);
     HIP_TRY(c, kernel_span(c, c->cs, &ld));
-    HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, ld));
+    HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, dn_rows[gi], ld));
     kernel_span_done(c, SPAN_GEMM_DOWN, ld, group_rows[gi] * down_flop_per_row);
     return MOE_OK;
   };

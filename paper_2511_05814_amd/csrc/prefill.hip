@@ -402,29 +402,26 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row
   return r;
 }
 
-// A workgroup takes a 128 x 128 output tile, against both W1 and W3 in the
+// A workgroup takes a BM x 128 output tile (BM = 128, or 64 for launches too
+// small to fill the chip with 128-row tiles), against both W1 and W3 in the
 // up projection and against W2 in the down projection.  Four waves each own
-// 64 x 64 of it as 4 x 4 v_mfma_f32_16x16x32_bf16 tiles.  (A 128 x 256 down
-// tile streams W2 no faster in isolation and halves the workgroups of the
-// small per-batch launches.)  The next 32-deep K slice is loaded from global memory into
-// registers kGemmStages slices ahead of the one multiplied out of LDS; LDS
-// is double-buffered so one barrier per step suffices.  Every output
-// accumulates its K slices in ascending order.
-constexpr int kBM = 128, kBN = 128;
+// (BM / 2) x 64 of it as (BM / 32) x 4 v_mfma_f32_16x16x32_bf16 tiles.  (A
+// 128 x 256 down tile streams W2 no faster in isolation and halves the
+// workgroups of the small per-batch launches.)  The next 32-deep K slice is
+// loaded from global memory into registers kGemmStages slices ahead of the
+// one multiplied out of LDS; LDS is double-buffered so one barrier per step
+// suffices.  Every output accumulates its K slices in ascending order.
+constexpr int kBN = 128;
 constexpr int kGemmStages = 2;  // K slices loaded ahead of the one being multiplied
 
-struct TileRows {
-  const uint16_t *p[2];  // this thread's two rows of the 128-row tile (or nullptr)
-};
-
-template <bool UP, int P>
-__global__ __launch_bounds__(256, P <= 2 ? 2 : 1) void prefill_gemm_kernel(const GemmTile *tiles,
-                                                                           const GemmJob *jobs,
-                                                                           const uint16_t *a_src,
-                                                                           const int32_t *perm_tok, void *out,
-                                                                           int d, int d_ff) {
-  constexpr int NB = UP ? 2 : 1;  // B matrices: W1 and W3, or W2
-  __shared__ uint16_t As[2][kBM][kLdsK];
+template <bool UP, int P, int BM>
+__global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_gemm_kernel(
+    const GemmTile *tiles, const GemmJob *jobs, const uint16_t *a_src, const int32_t *perm_tok, void *out, int d,
+    int d_ff) {
+  constexpr int NB = UP ? 2 : 1;   // B matrices: W1 and W3, or W2
+  constexpr int HA = BM / 64;      // A rows each thread stages
+  constexpr int MX = BM / 32;      // 16-row MFMA blocks per wave
+  __shared__ uint16_t As[2][BM][kLdsK];
   __shared__ uint16_t Bs[2][NB][kBN][kLdsK];
   const GemmTile t = tiles[blockIdx.x];
   const GemmJob j = jobs[t.job];
@@ -433,51 +430,53 @@ __global__ __launch_bounds__(256, P <= 2 ? 2 : 1) void prefill_gemm_kernel(const
   const int K = UP ? d : d_ff;   // reduction length
   const int N = UP ? d_ff : d;   // output columns
   const int ldo = N;
-  // staging: thread -> rows (tid / 4) and (tid / 4 + 64), 16-byte quarter tid % 4
+  // staging: thread -> rows (tid / 4) + 64 h, 16-byte quarter tid % 4
   const int r0 = tid / 4, q = tid % 4;
-  TileRows ar, br[NB];
+  const uint16_t *ap[HA];
+  const uint16_t *bp[NB][2];
+#pragma unroll
+  for (int h = 0; h < HA; ++h) {
+    const int m = t.m0 + r0 + 64 * h;
+    ap[h] = m < j.nrows ? (UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff)
+                        : nullptr;
+  }
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    const int m = t.m0 + r0 + 64 * h;
-    if (m < j.nrows)
-      ar.p[h] = UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff;
-    else
-      ar.p[h] = nullptr;
     const int n = t.n0 + r0 + 64 * h;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const uint16_t *w = j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d);
-      br[b].p[h] = n < N ? w + (size_t)n * K : nullptr;
+      bp[b][h] = n < N ? w + (size_t)n * K : nullptr;
     }
   }
   // K slices loaded ahead live in a ring of P register slots: slice t >= 1
   // sits in slot (t - 1) % P until it is stored to LDS.
-  uint4 ra[P][2], rb[P][NB][2];
+  uint4 ra[P][HA], rb[P][NB][2];
   auto gload = [&](int slot, int k0) {
     const int k = k0 + q * 8;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      ra[slot][h] = (ar.p[h] && k < K) ? *reinterpret_cast<const uint4 *>(ar.p[h] + k) : make_uint4(0, 0, 0, 0);
+    for (int h = 0; h < HA; ++h)
+      ra[slot][h] = (ap[h] && k < K) ? *reinterpret_cast<const uint4 *>(ap[h] + k) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int b = 0; b < NB; ++b)
-        rb[slot][b][h] = (br[b].p[h] && k < K) ? *reinterpret_cast<const uint4 *>(br[b].p[h] + k)
-                                               : make_uint4(0, 0, 0, 0);
-    }
+        rb[slot][b][h] = (bp[b][h] && k < K) ? *reinterpret_cast<const uint4 *>(bp[b][h] + k)
+                                             : make_uint4(0, 0, 0, 0);
   };
   auto lstore = [&](int slot, int buf) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][q * 8]) = ra[slot][h];
+    for (int h = 0; h < HA; ++h) *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][q * 8]) = ra[slot][h];
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
-        *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][q * 8]) = rb[slot][b][h];
-    }
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][q * 8]) = rb[slot][b][h];
   };
-  floatx4 c[NB][4][4];
+  floatx4 c[NB][MX][4];
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int x = 0; x < MX; ++x)
 #pragma unroll
       for (int y = 0; y < 4; ++y)
 #pragma unroll
@@ -496,16 +495,16 @@ __global__ __launch_bounds__(256, P <= 2 ? 2 : 1) void prefill_gemm_kernel(const
       const int s = i + u;  // slice multiplied now, out of LDS buffer s & 1
       if (s < nk) {
         const int buf = s & 1;
-        bf16x8 af[4];
+        bf16x8 af[MX];
 #pragma unroll
-        for (int x = 0; x < 4; ++x) af[x] = lds_frag(As[buf], wm * 64 + x * 16 + lane % 16, lane);
+        for (int x = 0; x < MX; ++x) af[x] = lds_frag(As[buf], wm * (BM / 2) + x * 16 + lane % 16, lane);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
           bf16x8 bf[4];
 #pragma unroll
           for (int y = 0; y < 4; ++y) bf[y] = lds_frag(Bs[buf][b], wn * 64 + y * 16 + lane % 16, lane);
 #pragma unroll
-          for (int x = 0; x < 4; ++x)
+          for (int x = 0; x < MX; ++x)
 #pragma unroll
             for (int y = 0; y < 4; ++y)
               c[b][x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
@@ -519,12 +518,12 @@ __global__ __launch_bounds__(256, P <= 2 ? 2 : 1) void prefill_gemm_kernel(const
     }
   }
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int x = 0; x < MX; ++x)
 #pragma unroll
     for (int y = 0; y < 4; ++y)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int m = t.m0 + wm * 64 + x * 16 + (lane / 16) * 4 + i;
+        const int m = t.m0 + wm * (BM / 2) + x * 16 + (lane / 16) * 4 + i;
         if (m >= j.nrows) continue;
         const int n = t.n0 + wn * 64 + y * 16 + lane % 16;
         if (n < N) {
@@ -565,18 +564,26 @@ hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l) {
 }
 
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l) {
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, perm_tok,
-             (void *)act, d, d_ff);
+  if (rows == 64)
+    MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, 64>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn,
+               perm_tok, (void *)act, d, d_ff);
+  else
+    MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, 128>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn,
+               perm_tok, (void *)act, d, d_ff);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, const Launch &l) {
+                               float *Y, int d, int d_ff, int rows, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
-             (const int32_t *)nullptr, (void *)Y, d, d_ff);
+  if (rows == 64)
+    MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, 64>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
+               (const int32_t *)nullptr, (void *)Y, d, d_ff);
+  else
+    MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, 128>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
+               (const int32_t *)nullptr, (void *)Y, d, d_ff);
   return hipGetLastError();
 }
 
@@ -586,8 +593,6 @@ hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, co
   return hipGetLastError();
 }
 
-int prefill_tile_rows() { return kBM; }
-int prefill_tile_cols_up() { return kBN; }
-int prefill_tile_cols_down() { return kBN; }
+int prefill_tile_cols() { return kBN; }
 
 }  // namespace moe
