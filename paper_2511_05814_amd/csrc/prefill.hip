@@ -39,7 +39,7 @@ typedef double double4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kGateTok = 16;     // tokens per gate workgroup
 constexpr int kKStep = 32;       // GEMM reduction step (one MFMA depth)
-constexpr int kLdsK = kKStep + 8;  // padded LDS row (bf16 elements)
+constexpr int kLdsK = kKStep;  // LDS row of one K slice (bf16 elements), 16-byte chunks swizzled
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -393,10 +393,15 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
 // 3. grouped GEMMs.  A rows come from the sorted pair order; B = expert
 // weights stored out x in (K contiguous), so both operands are K-major.
 
+// 16-byte chunk c of LDS row r sits at chunk c ^ ((r / 2) % 4) of the row:
+// rows are 64 bytes, so without the swizzle rows r and r + 2 would put the
+// same chunk in the same banks.
+__device__ __forceinline__ int lds_chunk(int row, int c) { return c ^ ((row >> 1) & 3); }
+
 // One MFMA 16x16x32 operand fragment from a K-major LDS tile: lane i holds
 // row (i % 16), elements (i / 16) * 8 .. + 8 of the 32-deep slice.
 __device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row, int lane) {
-  const uint4 v = *reinterpret_cast<const uint4 *>(&src[row][(lane / 16) * 8]);
+  const uint4 v = *reinterpret_cast<const uint4 *>(&src[row][lds_chunk(row, lane / 16) * 8]);
   bf16x8 r;
   __builtin_memcpy(&r, &v, sizeof v);
   return r;
@@ -466,11 +471,13 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
   };
   auto lstore = [&](int slot, int buf) {
 #pragma unroll
-    for (int h = 0; h < HA; ++h) *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][q * 8]) = ra[slot][h];
+    for (int h = 0; h < HA; ++h)
+      *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) = ra[slot][h];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][q * 8]) = rb[slot][b][h];
+      for (int b = 0; b < NB; ++b)
+        *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) = rb[slot][b][h];
   };
   floatx4 c[NB][MX][4];
 #pragma unroll
