@@ -275,6 +275,9 @@ def main():
     ap.add_argument("--host-store", choices=["plain", "packed", "entropy"], default="plain",
                     help="packed / entropy: bf16 experts coded losslessly in host memory (~12.25 / ~10.9 bits a "
                          "weight) and rebuilt on the GPU after each copy")
+    ap.add_argument("--prefetch-max", type=int, default=-1,
+                    help="override the workload's cap on next-layer experts prefetched per layer (0 turns "
+                         "speculation off)")
     ap.add_argument("--batch", type=int, default=1,
                     help="decode B tokens per step through the batch path (bf16 experts; no speculation)")
     args = ap.parse_args()
@@ -289,6 +292,8 @@ def main():
     from paper_2511_05814_amd import offload, workload as wl
 
     cfg = wl.CONFIGS[args.workload]
+    if args.prefetch_max >= 0:
+        cfg = cfg.with_(prefetch_max=min(args.prefetch_max, cfg.top_k))
     if args.tokens:
         cfg = cfg.with_(tokens=min(args.tokens, cfg.tokens))
     fetch_mode = {"kernel": b.MOE_FETCH_KERNEL, "dma": b.MOE_FETCH_DMA, "split": b.MOE_FETCH_SPLIT}[args.fetch]
