@@ -80,6 +80,16 @@ def measure_link(torch, nbytes=1 << 30, reps=3):
     return best
 
 
+def measure_hbm_read(torch, b, nbytes=1 << 30, reps=20):
+    """Streaming read rate (GB/s) of the library's HBM read probe over 1 GiB:
+    what a kernel with nothing to do but read reaches on this device."""
+    buf = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    gbps = b.moe_probe_hbm_read(buf.data_ptr(), nbytes, reps, torch.cuda.current_stream().cuda_stream)
+    del buf
+    return gbps
+
+
 def calibrate_counters(torch, nbytes=512 << 20):
     """One plain device-to-device copy of known size (512 MiB read, 512 MiB
     written), so that hardware byte counters collected on this program can be
@@ -335,6 +345,8 @@ def main():
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s")
     link = measure_link(torch)
     log(f"measured pinned H2D link: {link:.2f} GB/s")
+    hbm_probe = measure_hbm_read(torch, b)
+    log(f"HBM read probe: {hbm_probe:.1f} GB/s")
     calibrate_counters(torch)
 
     H0 = torch.from_numpy(h0[:cfg.prefill_tokens + cfg.tokens]).to("cuda")
@@ -450,6 +462,13 @@ def main():
                      "achieved_gbps": round(down_gbps, 1), "frac": round(down_gbps / HBM_PEAK_GBPS, 4),
                      "bytes_per_launch": down_bytes, "avg_launch_us": round(down_ms * 1e3, 2),
                      "reduce_avg_us": round(1e3 * tim["ffn_reduce_ms"] / max(1, tim["ffn_reduce_n"]), 2)},
+        "hbm_read_probe": {
+            "kernel": "hbm_read_probe_kernel",
+            "gbps": round(hbm_probe, 1),
+            "bytes": 1 << 30,
+            "roofline_kernel_frac_of_probe": round(up_gbps / hbm_probe, 4) if hbm_probe else None,
+            "is": "a streaming read with nothing else to do (one workgroup per CU, 8 16-byte loads in flight a lane)",
+        },
         "link_roofline": {
             "kernel": "fetch_kernel",
             "bound": "host-link",

@@ -307,6 +307,18 @@ size_t moe_entropy_matrix_bytes(size_t n, size_t cap_words);
  * threads at once. */
 int moe_entropy_pack(const uint16_t *w, size_t n, size_t cap_words, void *out, size_t *used);
 
+/* Calibration, not part of the decode path: the read bandwidth (GB/s) a
+ * plain streaming kernel reaches on the current device, a practical ceiling
+ * for the HBM-bound kernels above (the published peak is not reachable).
+ * Reads `bytes` (a positive multiple of 16) of device memory at buf (16-byte
+ * aligned, not written) `reps` times (1..1000) on `stream` (a hipStream_t,
+ * NULL = the default stream) after one untimed pass, with one workgroup per
+ * compute unit streaming 16-byte non-temporal loads; *gbps = bytes * reps
+ * over the time between events recorded around the timed passes.
+ * Synchronous.  MOE_ERR_ARG for bad arguments, MOE_ERR_HIP for runtime
+ * failures.  Use a buffer well above the 256 MB last-level cache. */
+int moe_probe_hbm_read(const void *buf, size_t bytes, int reps, void *stream, double *gbps);
+
 /* Thread-local message of the last failure on this thread ("" if none). */
 const char *moe_last_error(void);
 

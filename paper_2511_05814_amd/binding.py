@@ -112,6 +112,8 @@ _SIGNATURES = [
     ("moe_entropy_matrix_bytes", ctypes.c_size_t, [ctypes.c_size_t, ctypes.c_size_t]),
     ("moe_entropy_pack", ctypes.c_int,
      [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_void_p, ctypes.POINTER(ctypes.c_size_t)]),
+    ("moe_probe_hbm_read", ctypes.c_int,
+     [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
     ("moe_last_error", ctypes.c_char_p, []),
 ]
 EXPORTED = [s[0] for s in _SIGNATURES]
@@ -245,6 +247,13 @@ def moe_host_free(ptr: int) -> None:
 
 def moe_entropy_matrix_bytes(n: int, cap_words: int) -> int:
     return lib().moe_entropy_matrix_bytes(n, cap_words)
+
+
+def moe_probe_hbm_read(buf_ptr: int, nbytes: int, reps: int, stream: int) -> float:
+    """Streaming read rate (GB/s) of nbytes of device memory at buf_ptr."""
+    out = ctypes.c_double()
+    _check(lib().moe_probe_hbm_read(buf_ptr, nbytes, reps, stream, ctypes.byref(out)), "moe_probe_hbm_read")
+    return out.value
 
 
 def moe_entropy_pack(w_ptr: int, n: int, cap_words: int, out_ptr: int) -> int:

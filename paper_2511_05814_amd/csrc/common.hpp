@@ -151,6 +151,9 @@ struct Launch {
   hipExtLaunchKernelGGL(kernel, grid, block, shmem, (L).s, (L).start, (L).stop, 0, __VA_ARGS__)
 
 // launchers (one per translation unit that owns the kernel)
+// Streaming read of bytes (a multiple of 16) at buf with the given number of
+// workgroups; reads only.
+hipError_t launch_hbm_read_probe(const void *buf, size_t bytes, int workgroups, hipStream_t s);
 hipError_t launch_router(const RouterArgs &a, const Launch &l);
 // Copies of a fetch list: expert e of the list's layer from its host store
 // (stride src_stride) into its HBM slot (stride expert_bytes), or, when

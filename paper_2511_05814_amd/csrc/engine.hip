@@ -856,6 +856,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     (void)hipGetLastError();
   }
   int nt = 0;
+  bool overflow = false;  // checked before each write: ht is a fixed-size pinned buffer
   auto add_tiles = [&](const std::vector<int> &group, int ncols, int &first, int &count, int &rows) {
     long big = 0;
     for (int e : group) big += (long)((pl[e].n + 127) / 128) * ((ncols + cols - 1) / cols);
@@ -863,7 +864,13 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     first = nt;
     for (int e : group)
       for (int m0 = 0; m0 < pl[e].n; m0 += rows)
-        for (int n0 = 0; n0 < ncols; n0 += cols) ht[nt++] = GemmTile{e, m0, n0, 0};
+        for (int n0 = 0; n0 < ncols; n0 += cols) {
+          if (nt >= p.tile_cap) {
+            overflow = true;
+            continue;
+          }
+          ht[nt++] = GemmTile{e, m0, n0, 0};
+        }
     count = nt - first;
   };
   const size_t ngroups = batches.size() + 1;
@@ -878,9 +885,9 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     add_tiles(batches[bi], c->d, dn_first[bi + 1], dn_n[bi + 1], dn_rows[bi + 1]);
     for (int e : batches[bi]) group_rows[bi + 1] += pl[e].n;
   }
-  if (nt > p.tile_cap) {
+  if (overflow) {  // cannot happen: the capacity counts 64 x 64 tiles
     c->sticky = MOE_ERR_HIP;
-    return fail(MOE_ERR_HIP, "prefill tile schedule overflow (%d > %d)", nt, p.tile_cap);
+    return fail(MOE_ERR_HIP, "prefill tile schedule overflow (capacity %d)", p.tile_cap);
   }
   // A coded host store's experts are copied to the coded staging area and
   // rebuilt from there by a kernel that reads a device-side fetch list: per
@@ -1276,6 +1283,35 @@ int moe_entropy_pack(const uint16_t *w, size_t n, size_t cap_words, void *out, s
   uint64_t u = 0;
   if (entropy_pack(w, n, cap_words, static_cast<uint8_t *>(out), &u, &why) != 0) return fail(MOE_ERR_ARG, "%s", why);
   *used = u;
+  return MOE_OK;
+}
+
+int moe_probe_hbm_read(const void *buf, size_t bytes, int reps, void *stream, double *gbps) {
+  if (!buf || !gbps) return fail(MOE_ERR_ARG, "NULL pointer");
+  if (misaligned(buf, 16) || bytes < 16 || bytes % 16)
+    return fail(MOE_ERR_ARG, "buf must be 16-byte aligned and bytes a positive multiple of 16");
+  if (reps < 1 || reps > 1000) return fail(MOE_ERR_ARG, "reps must be in [1, 1000]");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0, cus = 0;
+  HIP_TRY0(hipGetDevice(&dev));
+  HIP_TRY0(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  hipEvent_t a = nullptr, b = nullptr;
+  HIP_TRY0(hipEventCreate(&a));
+  hipError_t e = hipEventCreate(&b);
+  if (e == hipSuccess) e = launch_hbm_read_probe(buf, bytes, cus, s);  // warm-up
+  if (e == hipSuccess) e = hipEventRecord(a, s);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) e = launch_hbm_read_probe(buf, bytes, cus, s);
+  if (e == hipSuccess) e = hipEventRecord(b, s);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.0f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(MOE_ERR_HIP, "HBM read probe failed: %s", hipGetErrorString(e));
+  }
+  *gbps = ms > 0.0f ? (double)bytes * reps / (ms * 1e-3) / 1e9 : 0.0;
   return MOE_OK;
 }
 

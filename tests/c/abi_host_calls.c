@@ -71,6 +71,16 @@ int main(void) {
     CHECK(moe_entropy_pack(w, 512, 1, out, &used) == MOE_ERR_ARG);
     CHECK(moe_entropy_pack(NULL, 512, 64, out, &used) == MOE_ERR_ARG);
   }
+  /* HBM read probe: argument errors are found before any GPU call */
+  {
+    static uint8_t buf[64] __attribute__((aligned(16)));
+    double g = 0.0;
+    CHECK(moe_probe_hbm_read(NULL, 64, 1, NULL, &g) == MOE_ERR_ARG);
+    CHECK(moe_probe_hbm_read(buf, 64, 1, NULL, NULL) == MOE_ERR_ARG);
+    CHECK(moe_probe_hbm_read(buf + 4, 48, 1, NULL, &g) == MOE_ERR_ARG); /* misaligned */
+    CHECK(moe_probe_hbm_read(buf, 40, 1, NULL, &g) == MOE_ERR_ARG);     /* not a multiple of 16 */
+    CHECK(moe_probe_hbm_read(buf, 64, 0, NULL, &g) == MOE_ERR_ARG);     /* reps */
+  }
   if (fails == 0) printf("ok\n");
   return fails != 0;
 }

@@ -100,3 +100,20 @@ def test_batch_of_one_and_of_full_capacity(T):
     _say("worst", worst)
     moe.close()
     rig.store.close()
+
+
+def test_hbm_read_probe():
+    # calibration call beside the path: a plausible rate on 512 MiB, and its
+    # argument errors (a misaligned pointer, a size that is not a multiple of 16)
+    _say("hbm read probe, 512 MiB, 3 reps")
+    nbytes = 512 << 20
+    buf = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream().cuda_stream
+    gbps = b.moe_probe_hbm_read(buf.data_ptr(), nbytes, 3, stream)
+    assert 1000.0 < gbps < 10000.0
+    assert int(buf.sum().item()) == 0  # read only
+    for ptr, n in ((buf.data_ptr() + 4, 1024), (buf.data_ptr(), 1000)):
+        with pytest.raises(b.MoeError) as e:
+            b.moe_probe_hbm_read(ptr, n, 1, stream)
+        assert e.value.code == b.MOE_ERR_ARG
