@@ -14,10 +14,13 @@ prefetch, the 64-expert stack with a 4096-token prefill); those print the
 same JSON schema.
 
 Prints one JSON line: decode tokens/s (LFU) and, alongside, LRU tokens/s,
-hit rates, cache and speculation precision/recall, the decode FFN kernels'
-HBM roofline (HIP-event timed inside the timed region), the fetch kernel's
-host-link roofline against the H2D rate measured here, and the fp64 oracle
-timed on a bounded sample on the host cores.
+hit rates, cache and speculation precision/recall, the decode FFN up
+kernel's HBM roofline (HIP events stamped by its dispatches inside the timed
+region; the other kernels' durations, the copy/compute overlap and the
+prefill GEMM rates come from one more pass of the same work with every launch
+timed, since events on every launch cost GPU time), the fetch kernel's
+host-link roofline against the H2D rate measured here, a streaming HBM read
+probe, and the fp64 oracle timed on a bounded sample on the host cores.
 """
 from __future__ import annotations
 
@@ -117,15 +120,16 @@ def pmc_traffic():
 
 def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0, batch=1):
     """n passes (reset, [prefill], decode all tokens, one at a time or
-    `batch` at a time); returns seconds of decode, seconds of prefill, summed
-    timing, summed per-layer statistics, the trace of the last pass and the
-    prefill's share of the fetched bytes."""
+    `batch` at a time) at a MOE_TIMING_* level; returns seconds of decode,
+    seconds of prefill, summed timing (None when off), summed per-layer
+    statistics, the trace of the last pass and the prefill's share of the
+    fetched bytes."""
     dec = pre = 0.0
     tim = None
     stats = None
     recs = None
     prefill_bytes = 0
-    b.moe_cache_set_timing(moe.handle, bool(timing))
+    b.moe_cache_set_timing(moe.handle, timing)
     for _ in range(n):
         moe.reset()
         H.copy_(H0)
@@ -153,7 +157,7 @@ def run_steps(torch, b, moe, H0, H, n, timing, flags=0, prefill_tokens=0, batch=
         st = moe.stats()
         stats = st if stats is None else [{k: a[k] + c[k] for k in a} for a, c in zip(stats, st)]
         recs, _ = moe.trace_records()
-    b.moe_cache_set_timing(moe.handle, False)
+    b.moe_cache_set_timing(moe.handle, b.MOE_TIMING_OFF)
     return dec, pre, tim, stats, recs, prefill_bytes
 
 
@@ -211,7 +215,7 @@ def batch_report(args, cfg, results, link):
     and the grouped GEMMs (which stream each routed expert's weights once per
     batch: HBM-bound at small batches)."""
     head = results[0]
-    tim, steps = head["timing"], head["steps"]
+    tim, steps = head["timing"], head["timing_steps"]
     mb = cfg.matrix_bytes
 
     def rates(r):
@@ -282,6 +286,9 @@ def main():
     ap.add_argument("--tokens", type=int, default=0,
                     help="decode only the first N tokens of the workload (profiling passes)")
     ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
+    ap.add_argument("--slots", type=int, default=0,
+                    help="HBM slots per layer (default 4, 16 for the 64-expert workload; "
+                         "slots = experts keeps every expert resident)")
     ap.add_argument("--host-store", choices=["plain", "packed", "entropy"], default="plain",
                     help="packed / entropy: bf16 experts coded losslessly in host memory (~12.25 / ~10.9 bits a "
                          "weight) and rebuilt on the GPU after each copy")
@@ -307,7 +314,9 @@ def main():
     if args.tokens:
         cfg = cfg.with_(tokens=min(args.tokens, cfg.tokens))
     fetch_mode = {"kernel": b.MOE_FETCH_KERNEL, "dma": b.MOE_FETCH_DMA, "split": b.MOE_FETCH_SPLIT}[args.fetch]
-    primary_slots = 16 if cfg.experts == 64 else 4
+    primary_slots = args.slots or (16 if cfg.experts == 64 else 4)
+    if not cfg.top_k <= primary_slots <= cfg.experts:
+        sys.exit(f"--slots must lie in [top_k, experts] = [{cfg.top_k}, {cfg.experts}]")
     if args.batch > 1 and cfg.dtype != "bf16":
         sys.exit("batched decode runs on bf16 experts (the grouped GEMMs use bf16 matrix cores)")
     if args.batch > 1 and cfg.prefill_tokens:
@@ -383,12 +392,21 @@ def main():
                                    max_prefill_tokens=max(cfg.prefill_tokens, args.batch if args.batch > 1 else 0))
         steps = args.steps if i == 0 else 1
         if i == 0 and args.warmup:
-            run_steps(torch, b, moe, H0, H, args.warmup, False, flags, cfg.prefill_tokens, args.batch)
-        dec, pre, tim, st, recs, pbytes = run_steps(torch, b, moe, H0, H, steps, True, flags,
-                                                    cfg.prefill_tokens, args.batch)
+            run_steps(torch, b, moe, H0, H, args.warmup, b.MOE_TIMING_OFF, flags, cfg.prefill_tokens, args.batch)
+        # timed passes: events on the decode FFN up launches only (the roofline
+        # kernel); every other kernel's events cost GPU time that would show in
+        # tokens/s, so the full breakdown comes from one more pass of the same
+        # work (the headline run, and the coded-store runs for their rebuilds)
+        dec, pre, up_tim, st, recs, pbytes = run_steps(torch, b, moe, H0, H, steps, b.MOE_TIMING_FFN_UP, flags,
+                                                       cfg.prefill_tokens, args.batch)
+        tim = up_tim
+        if i == 0 or fmt != "plain":
+            _, _, tim, _, _, _ = run_steps(torch, b, moe, H0, H, 1, b.MOE_TIMING_ALL, flags,
+                                           cfg.prefill_tokens, args.batch)
+            tim["ffn_up_ms"], tim["ffn_up_n"] = up_tim["ffn_up_ms"], up_tim["ffn_up_n"]
         results.append(dict(policy=policy, slots=slots, flags=flags, steps=steps, dec=dec, pre=pre,
                             prefill_bytes=pbytes, fmt=fmt, expert_stride=store.expert_stride,
-                            timing=tim, stats=st, recs=recs))
+                            timing=tim, timing_steps=1 if tim is not up_tim else steps, stats=st, recs=recs))
         log(policy, slots, "prefetch" if spec else "", f"{steps * cfg.tokens / dec:.2f} tok/s")
         moe.close()
 
@@ -409,8 +427,9 @@ def main():
     up_gbps = up_bytes / (up_ms * 1e-3) / 1e9
     down_gbps = down_bytes / (down_ms * 1e-3) / 1e9
     fetched = sum(s["bytes_fetched"] for s in head["stats"]) - head["prefill_bytes"]  # decode only
-    copy_ms = tim["fetch_ms"] + tim["pf_fetch_ms"]  # demand and speculative copies
-    fetch_gbps = fetched / (copy_ms * 1e-3) / 1e9 if copy_ms > 0 else None
+    tsteps = head["timing_steps"]  # passes the breakdown spans cover
+    copy_ms = (tim["fetch_ms"] + tim["pf_fetch_ms"]) / tsteps  # demand and speculative copies, per pass
+    fetch_gbps = fetched / head["steps"] / (copy_ms * 1e-3) / 1e9 if copy_ms > 0 else None
     tokens_per_s = head["steps"] * cfg.tokens / head["dec"]
     traffic = pmc_traffic() if args.workload == "mixtral-layer" else None
     summary = {f"{r['policy']}-s{r['slots']}" + ("-prefetch" if r["flags"] else "")
@@ -431,7 +450,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": DESCRIPTIONS[args.workload] + (f" (first {cfg.tokens} tokens)" if args.tokens else ""),
+            "workload": DESCRIPTIONS[args.workload] + (f" (first {cfg.tokens} tokens)" if args.tokens else "")
+                        + (f"; run with {head['slots']} slots per layer" if args.slots else ""),
             "weights_dtype": cfg.dtype,
             "policy": head["policy"],
             "slots": head["slots"],
@@ -492,14 +512,13 @@ def main():
                             "terms": "link bytes / measured link + FFN weight bytes / 8 TB/s"}
     # how the copies overlap the compute: the compute stream's wait between
     # each router and its FFN against the copy time (demand + speculative)
-    steps = head["steps"]
-    dec_ms = 1e3 * head["dec"] / steps
+    dec_ms = 1e3 * head["dec"] / head["steps"]
     out["copy_overlap"] = {
-        "demand_copy_ms_per_step": round(tim["fetch_ms"] / steps, 2),
-        "prefetch_copy_ms_per_step": round(tim["pf_fetch_ms"] / steps, 2),
-        "compute_wait_ms_per_step": round(tim["wait_ms"] / steps, 2),
-        "link_busy_frac": round(copy_ms / steps / dec_ms, 4) if not cfg.prefill_tokens else None,
-        "hidden_copy_frac": round(max(0.0, 1.0 - tim["wait_ms"] / copy_ms), 4) if copy_ms > 0 else None,
+        "demand_copy_ms_per_step": round(tim["fetch_ms"] / tsteps, 2),
+        "prefetch_copy_ms_per_step": round(tim["pf_fetch_ms"] / tsteps, 2),
+        "compute_wait_ms_per_step": round(tim["wait_ms"] / tsteps, 2),
+        "link_busy_frac": round(copy_ms / dec_ms, 4) if not cfg.prefill_tokens else None,
+        "hidden_copy_frac": round(max(0.0, 1.0 - tim["wait_ms"] / tsteps / copy_ms), 4) if copy_ms > 0 else None,
         "definition": "hidden_copy_frac = 1 - compute wait / copy time: the share of the copy time "
                       "(demand + speculative) during which the compute stream was not waiting",
     }

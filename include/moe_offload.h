@@ -273,13 +273,19 @@ typedef struct {
   uint64_t pf_fetch_n;
 } moe_timing;
 
-/* Kernel timing with HIP events, off by default.  While enabled, every router,
- * fetch, decode FFN and prefill grouped-GEMM launch is bracketed by a pair of
- * events on the stream it runs on (prefill_ms spans a whole layer's prefill on
- * the compute stream, waits for streamed experts included; wait_ms spans the
- * compute stream's wait for copies between a decode router and its FFN).
+/* Kernel timing with HIP events, off by default.  At MOE_TIMING_ALL every
+ * router, fetch, decode FFN and prefill grouped-GEMM launch is bracketed by a
+ * pair of events on the stream it runs on (prefill_ms spans a whole layer's
+ * prefill on the compute stream, waits for streamed experts included; wait_ms
+ * spans the compute stream's work between a decode router and its FFN: the
+ * demand copies, or the wait for them).  The events cost GPU time as well
+ * (about a third of the kernel time of a layer whose experts are all
+ * resident), so MOE_TIMING_FFN_UP times only the decode FFN up launches and
+ * leaves every other count at zero.  enable: one of the MOE_TIMING_* levels
+ * (0 and 1 keep their boolean meaning); MOE_ERR_ARG otherwise.
  * moe_cache_read_timing syncs, returns the summed durations (ms), launch
  * counts and GEMM flops since the previous read, and clears them. */
+enum { MOE_TIMING_OFF = 0, MOE_TIMING_ALL = 1, MOE_TIMING_FFN_UP = 2 };
 int moe_cache_set_timing(moe_cache_t *c, int enable);
 int moe_cache_read_timing(moe_cache_t *c, moe_timing *out);
 

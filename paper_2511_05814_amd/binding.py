@@ -21,6 +21,7 @@ MOE_OK, MOE_ERR_ARG, MOE_ERR_STATE, MOE_ERR_HIP, MOE_ERR_NOMEM = 0, -1, -2, -3, 
 MOE_PREFETCH_NEXT = 1
 MOE_FETCH_KERNEL, MOE_FETCH_DMA, MOE_FETCH_SPLIT = 0, 1, 2
 MOE_HOST_PLAIN, MOE_HOST_PACKED, MOE_HOST_ENTROPY = 0, 1, 2
+MOE_TIMING_OFF, MOE_TIMING_ALL, MOE_TIMING_FFN_UP = 0, 1, 2
 MOE_MAX_EXPERTS, MOE_MAX_TOPK = 64, 16
 
 POLICIES = {"lru": MOE_POLICY_LRU, "lfu": MOE_POLICY_LFU, "lfu-aged": MOE_POLICY_LFU_AGED}
@@ -220,8 +221,9 @@ def moe_cache_last_routing(cache: int, cap: int):
     return list(ids[:m]), list(g[:m]), n.value
 
 
-def moe_cache_set_timing(cache: int, enable: bool) -> None:
-    _check(lib().moe_cache_set_timing(cache, int(bool(enable))), "moe_cache_set_timing")
+def moe_cache_set_timing(cache: int, level) -> None:
+    """level: a MOE_TIMING_* value (False/True are OFF/ALL)."""
+    _check(lib().moe_cache_set_timing(cache, int(level)), "moe_cache_set_timing")
 
 
 def moe_cache_read_timing(cache: int) -> dict:

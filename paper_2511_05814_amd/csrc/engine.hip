@@ -3,15 +3,18 @@
 //
 // Per decoded token and layer the engine only enqueues work:
 //   compute stream: router (routing + table update + fetch lists)
-//   copy stream:    wait(router) -> fetch demand misses -> event D[l]
-//                   -> fetch next-layer prefetches -> event P[l+1]
-//   compute stream: wait(D[l]) [, wait(P[l]) if layer l had prefetches]
-//                   -> FFN up -> FFN down (h += y)
-// Every copy waits for the router that chose it, and that router runs after
-// all compute that read the victim slot earlier (stream order), so a slot is
-// never overwritten while an FFN still reads it.  Every FFN waits for the
-// copies that filled its slots (Sec. 6.1 asks for transfers overlapped with
-// compute; here copies of one layer run while other work is queued behind).
+//                   [-> wait(P[l]) if layer l has speculative copies in flight]
+//                   -> fetch demand misses -> FFN up -> FFN down -> reduce (h += y)
+//   copy stream:    wait(router, demand fetch) -> fetch next-layer
+//                   prefetches -> event P[l+1]
+// (A coded host store's demand copies share the staging area with the
+// speculative ones, so they run on the copy stream instead, ending in event
+// D[l] that the FFN waits for.)  Every copy waits for the router that chose
+// it, and that router runs after all compute that read the victim slot
+// earlier (stream order), so a slot is never overwritten while an FFN still
+// reads it.  Every FFN waits for the copies that filled its slots (Sec. 6.1
+// asks for transfers overlapped with compute; here the next layer's
+// speculative copies run while this layer's FFN computes).
 #include "common.hpp"
 #include "moe_offload.h"
 
@@ -137,7 +140,7 @@ struct moe_cache {
   uint8_t *h_sched = nullptr;      // pinned: GEMM jobs + tiles uploaded per layer
   std::vector<hipEvent_t> pf_ev;   // prefill ordering events
   // kernel timing (moe_cache_set_timing)
-  bool timing = false;
+  int timing = MOE_TIMING_OFF;
   std::vector<hipEvent_t> ev_pool;
   struct Span {
     int kind;
@@ -153,10 +156,15 @@ enum SpanKind {
   SPAN_UNPACK, SPAN_WAIT, SPAN_PF_FETCH, SPAN_KINDS
 };
 
-// Start/stop a timed span on stream s (no-op unless timing is on).
-hipError_t span_begin(moe_cache *c, hipStream_t s, hipEvent_t *out) {
+// Whether spans of this kind are recorded at the handle's timing level.
+bool timed(const moe_cache *c, int kind) {
+  return c->timing == MOE_TIMING_ALL || (c->timing == MOE_TIMING_FFN_UP && kind == SPAN_UP);
+}
+
+// Start/stop a timed span on stream s (no-op unless its kind is timed).
+hipError_t span_begin(moe_cache *c, hipStream_t s, hipEvent_t *out, int kind) {
   *out = nullptr;
-  if (!c->timing) return hipSuccess;
+  if (!timed(c, kind)) return hipSuccess;
   hipEvent_t e;
   if (!c->ev_pool.empty()) {
     e = c->ev_pool.back();
@@ -170,7 +178,7 @@ hipError_t span_begin(moe_cache *c, hipStream_t s, hipEvent_t *out) {
 }
 
 hipError_t span_end(moe_cache *c, hipStream_t s, int kind, hipEvent_t begin, double flop = 0.0) {
-  if (!c->timing || !begin) return hipSuccess;
+  if (!begin) return hipSuccess;
   hipEvent_t e;
   if (!c->ev_pool.empty()) {
     e = c->ev_pool.back();
@@ -185,10 +193,10 @@ hipError_t span_end(moe_cache *c, hipStream_t s, int kind, hipEvent_t begin, dou
 
 // A kernel launch on stream s; with timing on it carries two pooled events
 // that the dispatch itself stamps at the kernel's start and end.
-hipError_t kernel_span(moe_cache *c, hipStream_t s, Launch *l) {
+hipError_t kernel_span(moe_cache *c, hipStream_t s, Launch *l, int kind) {
   l->s = s;
   l->start = l->stop = nullptr;
-  if (!c->timing) return hipSuccess;
+  if (!timed(c, kind)) return hipSuccess;
   for (hipEvent_t *e : {&l->start, &l->stop}) {
     if (!c->ev_pool.empty()) {
       *e = c->ev_pool.back();
@@ -552,7 +560,7 @@ int moe_cache_reset(moe_cache_t *c) {
 // by an unpack kernel behind the copies on the same stream.
 static int unpack_list(moe_cache *c, FetchList *list, hipStream_t q) {
   Launch l;
-  HIP_TRY(c, kernel_span(c, q, &l));
+  HIP_TRY(c, kernel_span(c, q, &l, SPAN_UNPACK));
   HIP_TRY(c, launch_rebuild(c, list, l));
   kernel_span_done(c, SPAN_UNPACK, l);
   return MOE_OK;
@@ -564,7 +572,7 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
   const int kind = mirror_idx == 1 ? SPAN_PF_FETCH : SPAN_FETCH;  // speculative or demand copies
   if (by_kernel) {
     Launch l;
-    HIP_TRY(c, kernel_span(c, q, &l));
+    HIP_TRY(c, kernel_span(c, q, &l, kind));
     HIP_TRY(c, launch_fetch(list, c->dev_layers, static_cast<uint8_t *>(c->desc.arena), c->L, c->E, c->S,
                             c->K, c->B, c->Bh, c->staging, c->err, l));
     kernel_span_done(c, kind, l);
@@ -579,7 +587,7 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
   uint8_t *arena = static_cast<uint8_t *>(c->desc.arena);
   if (m.n == 0) return MOE_OK;
   hipEvent_t t0;
-  HIP_TRY(c, span_begin(c, q, &t0));
+  HIP_TRY(c, span_begin(c, q, &t0, kind));
   for (int i = 0; i < m.n; ++i) {
     const int e = m.expert[i], s = m.slot[i];
     if (e < 0 || e >= c->E || s < 0 || s >= c->S) {
@@ -628,18 +636,26 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.spec_layer = spec_layer;
   a.pmax = pmax;
   Launch lr;
-  HIP_TRY(c, kernel_span(c, c->cs, &lr));
+  HIP_TRY(c, kernel_span(c, c->cs, &lr, SPAN_ROUTER));
   HIP_TRY(c, launch_router(a, lr));
   kernel_span_done(c, SPAN_ROUTER, lr);
   // from the router's end to the FFN's start: the compute stream's wait for
   // the copies that fill this layer's slots
   hipEvent_t t_wait = nullptr;
-  if (ffn) HIP_TRY(c, span_begin(c, c->cs, &t_wait));
+  if (ffn) HIP_TRY(c, span_begin(c, c->cs, &t_wait, SPAN_WAIT));
 
   hipStream_t q = c->xs;
   const bool split = c->fetch_mode == MOE_FETCH_SPLIT;
+  // A plain store's demand copies (kernel and split modes) go on the compute
+  // stream: the FFN waits for them anyway, and stream order then replaces the
+  // two cross-stream waits (router -> copy stream -> FFN) that cost tens of
+  // microseconds a layer even when nothing misses.  Coded stores keep them on
+  // the copy stream, where they share the staging area with speculative copies.
+  const bool demand_on_cs =
+      !c->one_stream && c->fetch_mode != MOE_FETCH_DMA && !coded_store(c->host_format);
+  hipStream_t qd = demand_on_cs ? c->cs : q;
   if (c->fetch_mode != MOE_FETCH_DMA) {
-    if (!c->one_stream) {
+    if (!c->one_stream && ((demand && !demand_on_cs) || spec_layer >= 0)) {
       HIP_TRY(c, hipEventRecord(c->ev_router, c->cs));
       HIP_TRY(c, hipStreamWaitEvent(q, c->ev_router, 0));
     }
@@ -653,11 +669,21 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     if (e != ERR_NONE) return MOE_OK;  // reported at the next synchronising call
   }
   if (demand) {
-    int rc = issue_fetch(c, c->dl + layer, 0, q);
+    // a slot the router just took may still be receiving a speculative copy
+    if (demand_on_cs && c->pf_pending[layer]) {
+      HIP_TRY(c, hipStreamWaitEvent(c->cs, c->ev_pf[layer], 0));
+      c->pf_pending[layer] = 0;
+    }
+    int rc = issue_fetch(c, c->dl + layer, 0, qd);
     if (rc != MOE_OK) return rc;
     if (!c->one_stream) {
-      HIP_TRY(c, hipEventRecord(c->ev_demand[layer], q));
-      c->demand_pending[layer] = 1;
+      HIP_TRY(c, hipEventRecord(c->ev_demand[layer], qd));
+      if (demand_on_cs) {
+        // speculative copies queue behind this layer's demand copies
+        if (spec_layer >= 0) HIP_TRY(c, hipStreamWaitEvent(q, c->ev_demand[layer], 0));
+      } else {
+        c->demand_pending[layer] = 1;
+      }
     }
   }
   if (spec_layer >= 0 && !split) {
@@ -690,13 +716,13 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     f.phase = 0;
     HIP_TRY(c, span_end(c, c->cs, SPAN_WAIT, t_wait));
     Launch lu, ld, lx;
-    HIP_TRY(c, kernel_span(c, c->cs, &lu));
+    HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_UP));
     HIP_TRY(c, launch_ffn_up(f, c->dtype, lu));
     kernel_span_done(c, SPAN_UP, lu);
-    HIP_TRY(c, kernel_span(c, c->cs, &ld));
+    HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_DOWN));
     HIP_TRY(c, launch_ffn_down(f, c->dtype, ld));
     kernel_span_done(c, SPAN_DOWN, ld);
-    HIP_TRY(c, kernel_span(c, c->cs, &lx));
+    HIP_TRY(c, kernel_span(c, c->cs, &lx, SPAN_REDUCE));
     HIP_TRY(c, launch_ffn_reduce(f, c->dtype, lx));
     kernel_span_done(c, SPAN_REDUCE, lx);
     c->last_route_kind = 1;
@@ -754,7 +780,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   const int gate_elem = c->dtype == MOE_DTYPE_BF16 ? 2 : 4;
 
   hipEvent_t tp;
-  HIP_TRY(c, span_begin(c, c->cs, &tp));
+  HIP_TRY(c, span_begin(c, c->cs, &tp, SPAN_PREFILL));
   PrefillArgs ga{};
   ga.gate = static_cast<const uint8_t *>(c->desc.gate_w) + (size_t)layer * c->E * c->d * gate_elem;
   ga.H = H;
@@ -949,10 +975,10 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   auto run_group = [&](size_t gi) -> int {
     if (up_n[gi] <= 0) return MOE_OK;
     Launch lu, ld;
-    HIP_TRY(c, kernel_span(c, c->cs, &lu));
+    HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_GEMM_UP));
     HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, up_rows[gi], lu));
     kernel_span_done(c, SPAN_GEMM_UP, lu, group_rows[gi] * up_flop_per_row);
-    HIP_TRY(c, kernel_span(c, c->cs, &ld));
+    HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
     HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, dn_rows[gi], ld));
     kernel_span_done(c, SPAN_GEMM_DOWN, ld, group_rows[gi] * down_flop_per_row);
     return MOE_OK;
@@ -973,7 +999,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       HIP_TRY(c, hipMemcpyAsync(coded_stage + i * c->Bh, host + (size_t)e * c->Bh, c->Bh, hipMemcpyHostToDevice, q));
     }
     Launch lr;
-    HIP_TRY(c, kernel_span(c, q, &lr));
+    HIP_TRY(c, kernel_span(c, q, &lr, SPAN_UNPACK));
     HIP_TRY(c, pt.ring ? launch_rebuild(c, dlists + pt.list, coded_stage, staging, 1, p.ring, half, lr)
                        : launch_rebuild(c, dlists + pt.list, coded_stage, arena, c->L, c->S, half, lr));
     kernel_span_done(c, SPAN_UNPACK, lr);
@@ -1195,7 +1221,9 @@ int moe_cache_last_routing(moe_cache_t *c, int32_t *ids, float *g, size_t cap, s
 
 int moe_cache_set_timing(moe_cache_t *c, int enable) {
   if (!c) return fail(MOE_ERR_ARG, "NULL handle");
-  c->timing = enable != 0;
+  if (enable < MOE_TIMING_OFF || enable > MOE_TIMING_FFN_UP)
+    return fail(MOE_ERR_ARG, "timing level must be MOE_TIMING_OFF, MOE_TIMING_ALL or MOE_TIMING_FFN_UP");
+  c->timing = enable;
   return MOE_OK;
 }
 

@@ -40,6 +40,11 @@ int main(void) {
   d.fetch_mode = MOE_FETCH_SPLIT;
   CHECK(moe_cache_bind(c, &d) == MOE_ERR_ARG); /* NULL buffers */
 
+  CHECK(moe_cache_set_timing(c, MOE_TIMING_FFN_UP) == MOE_OK);
+  CHECK(moe_cache_set_timing(c, 3) == MOE_ERR_ARG);
+  CHECK(moe_cache_set_timing(c, -1) == MOE_ERR_ARG);
+  CHECK(moe_cache_set_timing(c, MOE_TIMING_OFF) == MOE_OK);
+
   memset(h, 0, sizeof h);
   CHECK(moe_decode_layer(c, 0, h, 0) == MOE_ERR_STATE); /* not bound */
   CHECK(moe_cache_sync(c) == MOE_ERR_STATE);

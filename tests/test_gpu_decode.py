@@ -259,3 +259,35 @@ def test_aliased_host_layers():
         check_decode(cfg, rig.model, hs, recs, 4, "lru", prefetch=True, pmax=1, tol=_tol(cfg))
         moe.close()
     rig.store.close()
+
+
+def test_timing_levels(tiny):
+    # MOE_TIMING_ALL times every decode launch, MOE_TIMING_FFN_UP only the FFN
+    # up launches, OFF nothing; the events change no result
+    cfg = tiny.cfg
+    T = 8
+    calls = T * cfg.layers
+    out = {}
+    for level in (b.MOE_TIMING_OFF, b.MOE_TIMING_ALL, b.MOE_TIMING_FFN_UP):
+        _say("timing level", level)
+        moe = tiny.cache(4, "lfu", prefetch_max=2)
+        b.moe_cache_set_timing(moe.handle, level)
+        _, recs, H = tiny.run(moe, T, flags=b.MOE_PREFETCH_NEXT)
+        issued = sum(s["pf_issued"] for s in moe.stats())
+        out[level] = ([tuple(r) for r in recs], H, b.moe_cache_read_timing(moe.handle), issued)
+        with pytest.raises(b.MoeError) as e:
+            b.moe_cache_set_timing(moe.handle, 3)
+        assert e.value.code == b.MOE_ERR_ARG
+        moe.close()
+    t_all = out[b.MOE_TIMING_ALL][2]
+    for k in ("router", "fetch", "ffn_up", "ffn_down", "ffn_reduce", "wait"):
+        assert t_all[k + "_n"] == calls, k
+        assert t_all[k + "_ms"] > 0, k
+    assert (t_all["pf_fetch_n"] > 0) == (out[b.MOE_TIMING_ALL][3] > 0)
+    t_up = out[b.MOE_TIMING_FFN_UP][2]
+    assert t_up["ffn_up_n"] == calls and t_up["ffn_up_ms"] > 0
+    assert all(v == 0 for k, v in t_up.items() if not k.startswith("ffn_up")), t_up
+    assert all(v == 0 for v in out[b.MOE_TIMING_OFF][2].values())
+    for level in (b.MOE_TIMING_ALL, b.MOE_TIMING_FFN_UP):
+        assert out[level][0] == out[b.MOE_TIMING_OFF][0]
+        assert np.array_equal(out[level][1], out[b.MOE_TIMING_OFF][1])
