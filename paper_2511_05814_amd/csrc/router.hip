@@ -36,31 +36,51 @@ constexpr int kWaves = kThreads / kWave;
 // together, from addresses clamped into the gate array so that no load sits
 // behind a branch (a load under a condition is waited for on the spot), and
 // only then used.
-constexpr int kBatch = 16;
+constexpr int kBatch = 8;
 constexpr int kMaxD = 16384;
 
+struct GateWork {
+  int n = 0, cpr = 1;  // (row, chunk) items of this wave; chunks per row
+};
+
 template <int DT>
-__device__ void gate_logits(const RouterArgs &a, const float *hs, int r0, int r1, int wave, int lane,
-                            double *zs) {
+__device__ __forceinline__ GateWork gate_work(const RouterArgs &a, int r0, int r1, int wave) {
   constexpr int EPL = DT == 1 ? 8 : 4;  // elements per 16-byte load
+  GateWork g;
+  g.cpr = (a.d + kWave * EPL - 1) / (kWave * EPL);
+  const int M = r0 + wave < r1 ? (r1 - r0 - wave + kWaves - 1) / kWaves : 0;
+  g.n = M * g.cpr;
+  return g;
+}
+
+// Issue the weight loads of items j0 .. j0 + kBatch - 1 (n > 0).
+template <int DT>
+__device__ __forceinline__ void gate_load(const RouterArgs &a, int r0, int wave, int lane, const GateWork &g,
+                                          int j0, uint4 *v) {
+  constexpr int EPL = DT == 1 ? 8 : 4;
   constexpr int ESZ = DT == 1 ? 2 : 4;
   const int E = a.E, d = a.d;
-  const int cpr = (d + kWave * EPL - 1) / (kWave * EPL);
-  const int M = r0 + wave < r1 ? (r1 - r0 - wave + kWaves - 1) / kWaves : 0;
-  const int n = M * cpr;
   const uint8_t *gate = static_cast<const uint8_t *>(a.gate);
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) {
+    const int j = min(j0 + u, g.n - 1);
+    const int row = r0 + wave + kWaves * (j / g.cpr);
+    const int gl = row < E ? a.layer : a.spec_layer;
+    const int e = row < E ? row : row - E;
+    const int col = min((j % g.cpr) * kWave * EPL + lane * EPL, d - EPL);
+    v[u] = *reinterpret_cast<const uint4 *>(gate + (((size_t)gl * E + e) * d + col) * ESZ);
+  }
+}
+
+// v holds the first batch, loaded by gate_load(.., 0, v) before h was staged.
+template <int DT>
+__device__ void gate_logits(const RouterArgs &a, const float *hs, int r0, int wave, int lane,
+                            const GateWork &g, uint4 *v, double *zs) {
+  constexpr int EPL = DT == 1 ? 8 : 4;
+  const int d = a.d, n = g.n, cpr = g.cpr;
   double acc = 0.0;
   for (int j0 = 0; j0 < n; j0 += kBatch) {
-    uint4 v[kBatch];
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int j = min(j0 + u, n - 1);
-      const int row = r0 + wave + kWaves * (j / cpr);
-      const int gl = row < E ? a.layer : a.spec_layer;
-      const int e = row < E ? row : row - E;
-      const int col = min((j % cpr) * kWave * EPL + lane * EPL, d - EPL);
-      v[u] = *reinterpret_cast<const uint4 *>(gate + (((size_t)gl * E + e) * d + col) * ESZ);
-    }
+    if (j0 > 0) gate_load<DT>(a, r0, wave, lane, g, j0, v);
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int j = j0 + u;
@@ -96,6 +116,33 @@ __device__ void gate_logits(const RouterArgs &a, const float *hs, int r0, int r1
       }
     }
   }
+}
+
+// One wave's view of a layer's table (lane e = expert e, for lanes < E) and
+// of its statistics counter (lane i = counter i), read at kernel start so the
+// reads overlap the gate GEMV.  Indices are clamped instead of guarded (a
+// guarded load is waited for on the spot); lanes past E are masked where the
+// values are used.
+struct TableView {
+  int32_t slot;
+  uint32_t count;
+  int64_t last;
+  int32_t pf;
+  int64_t clock, lookups;
+  uint64_t stat;
+};
+
+__device__ __forceinline__ TableView load_table(const LayerTable *T, const LayerStats *st, int lane, int E) {
+  const int e = min(lane, E - 1);
+  TableView t;
+  t.slot = T->expert_slot[e];
+  t.count = T->count[e];
+  t.last = T->last[e];
+  t.pf = T->pf[e];
+  t.clock = T->clock;
+  t.lookups = T->lookups;
+  t.stat = st->v[lane & 15];
+  return t;
 }
 
 // Lane of the resident, unpinned expert with the smallest policy key
@@ -152,18 +199,18 @@ __device__ void put_rec(const RouterArgs &a, uint64_t idx, int kind, int64_t tok
 
 // Wave 0: the token's K lookups in layer a.layer, in rank order.
 // `idreg` on lane r < K holds the expert of rank r.
-__device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t rec_base) {
+__device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t rec_base, const TableView &tv) {
   LayerTable *T = a.tables + a.layer;
   LayerStats *st = a.stats + a.layer;
   FetchList *fl = a.dlists + a.layer;
   const int E = a.E, K = a.K;
   const bool in_range = lane < E;
-  int my_slot = in_range ? T->expert_slot[lane] : -1;
-  uint32_t my_count = in_range ? T->count[lane] : 0u;
-  int64_t my_last = in_range ? T->last[lane] : 0;
-  int my_pf = in_range ? T->pf[lane] : 0;
-  int64_t clock = T->clock;
-  const int64_t token = T->lookups;
+  int my_slot = in_range ? tv.slot : -1;
+  uint32_t my_count = in_range ? tv.count : 0u;
+  int64_t my_last = in_range ? tv.last : 0;
+  int my_pf = in_range ? tv.pf : 0;
+  int64_t clock = tv.clock;
+  const int64_t token = tv.lookups;
 
   bool pinned = false;
   for (int r = 0; r < K; ++r) pinned |= (__shfl(idreg, r, kWave) == lane);
@@ -245,24 +292,24 @@ __device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t
                      : lane == ST_PF_WASTED ? (uint64_t)wasted
                      : lane == ST_LOOKUPS ? 1ull
                      : lane == ST_BYTES ? (uint64_t)n_miss * a.expert_bytes : 0ull;
-  if (add) st->v[lane] += add;
+  if (add) st->v[lane] = tv.stat + add;
 }
 
 // Wave 1: insert up to pmax of the K guesses (lane r holds rank r's guess)
 // into the table of a.spec_layer, all guesses pinned.
-__device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_t rec_base) {
+__device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_t rec_base, const TableView &tv) {
   const int L2 = a.spec_layer;
   LayerTable *T = a.tables + L2;
   LayerStats *st = a.stats + L2;
   FetchList *fl = a.plists + L2;
   const int E = a.E, K = a.K;
   const bool in_range = lane < E;
-  int my_slot = in_range ? T->expert_slot[lane] : -1;
-  uint32_t my_count = in_range ? T->count[lane] : 0u;
-  int64_t my_last = in_range ? T->last[lane] : 0;
-  int my_pf = in_range ? T->pf[lane] : 0;
-  int64_t clock = T->clock;
-  const int64_t token = T->lookups;
+  int my_slot = in_range ? tv.slot : -1;
+  uint32_t my_count = in_range ? tv.count : 0u;
+  int64_t my_last = in_range ? tv.last : 0;
+  int my_pf = in_range ? tv.pf : 0;
+  int64_t clock = tv.clock;
+  const int64_t token = tv.lookups;
 
   bool pinned = false;
   for (int r = 0; r < K; ++r) pinned |= (__shfl(greg, r, kWave) == lane);
@@ -321,7 +368,7 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
                      : lane == ST_PF_ISSUED ? (uint64_t)issued
                      : lane == ST_PF_WASTED ? (uint64_t)wasted
                      : lane == ST_BYTES ? (uint64_t)issued * a.expert_bytes : 0ull;
-  if (add) st->v[lane] += add;
+  if (add) st->v[lane] = tv.stat + add;
 }
 
 __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
@@ -337,6 +384,23 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   const bool route_here = a.demand && a.inj_ids == nullptr;
   const bool spec = a.spec_layer >= 0;
 
+  // Every global read that does not depend on another is issued first: the
+  // tables and counters of waves 0 and 1, the first batch of gate rows, then h.
+  TableView tv{};
+  if (wave == 0 && a.demand) tv = load_table(a.tables + a.layer, a.stats + a.layer, lane, E);
+  if (wave == 1 && spec) tv = load_table(a.tables + a.spec_layer, a.stats + a.spec_layer, lane, E);
+  const int r0 = route_here ? 0 : E, r1 = spec ? 2 * E : E;
+  uint4 gv[kBatch];
+  GateWork gw;
+  if (route_here || spec) {
+    gw = a.dtype == 1 ? gate_work<1>(a, r0, r1, wave) : gate_work<0>(a, r0, r1, wave);
+    if (gw.n > 0) {
+      if (a.dtype == 1)
+        gate_load<1>(a, r0, wave, lane, gw, 0, gv);
+      else
+        gate_load<0>(a, r0, wave, lane, gw, 0, gv);
+    }
+  }
   if (tid == 0) {
     s_tbase = a.trace ? *a.trace_count : 0;
     s_demand_ok = 0;
@@ -355,11 +419,10 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     ss = wave_sum_d(ss);
     if (lane == 0) red[wave] = ss;
     __syncthreads();
-    const int r0 = route_here ? 0 : E, r1 = spec ? 2 * E : E;
     if (a.dtype == 1)
-      gate_logits<1>(a, hs, r0, r1, wave, lane, zs);
+      gate_logits<1>(a, hs, r0, wave, lane, gw, gv, zs);
     else
-      gate_logits<0>(a, hs, r0, r1, wave, lane, zs);
+      gate_logits<0>(a, hs, r0, wave, lane, gw, gv, zs);
   }
   __syncthreads();
   if (route_here && tid == 0) {
@@ -403,13 +466,13 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
       }
     }
     if (__shfl(idreg, 0, kWave) >= 0) {
-      demand_lookup(a, idreg, lane, s_tbase);
+      demand_lookup(a, idreg, lane, s_tbase, tv);
       if (lane == 0) s_demand_ok = 1;
     }
   }
   if (wave == 1 && spec) {
     const int greg = wave_topk_lds(zs + E, E, a.K, lane, s_top[1]);
-    prefetch_insert(a, greg, lane, s_tbase + (a.demand ? (uint64_t)a.K : 0));
+    prefetch_insert(a, greg, lane, s_tbase + (a.demand ? (uint64_t)a.K : 0), tv);
   }
   __syncthreads();
   if (tid == 0 && a.trace)
