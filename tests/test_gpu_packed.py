@@ -135,3 +135,32 @@ def test_coded_store_prefill_then_decode_matches_plain(fmt):
     for a, c in zip(st, ref[2]):
         assert a["bytes_fetched"] * cfg.expert_bytes == c["bytes_fetched"] * coded.expert_stride
     coded.close()
+
+
+@pytest.mark.parametrize("pmax", [0, 2])
+def test_coded_store_delayed_copy_stream(pmax):
+    # A coded store's demand copies and rebuilds run on the copy stream (they
+    # share its staging area with the speculative copies); a long spin there
+    # ahead of every layer must not let an FFN read a slot before its rebuild.
+    cfg = wl.CONFIGS["tiny-stack"].with_(dtype="bf16", tokens=16)
+    gates = offload.DeviceGates(cfg)
+    plain = offload.HostStore(cfg)
+    coded = offload.HostStore(cfg, fmt="entropy")
+    flags = b.MOE_PREFETCH_NEXT if pmax else 0
+    ref = run(cfg, plain, gates, 4, "lru", cfg.tokens, flags, prefetch_max=pmax)
+    _say("entropy store, delayed copy stream, prefetch", pmax)
+    moe = offload.OffloadedMoE(cfg, coded, gates, 4, "lru", prefetch_max=pmax)
+    H = torch.from_numpy(np.ascontiguousarray(wl.hidden_states(cfg, cfg.tokens))).to("cuda")
+    with torch.cuda.stream(moe.compute):
+        for t in range(cfg.tokens):
+            for l in range(cfg.layers):
+                with torch.cuda.stream(moe.copy):
+                    torch.cuda._sleep(200000)
+                b.moe_decode_layer(moe.handle, l, H[t].data_ptr(), flags)
+    moe.sync()
+    recs, _ = moe.trace_records()
+    moe.close()
+    assert recs == ref[1]
+    assert H.cpu().numpy().tobytes() == ref[0].tobytes()
+    plain.close()
+    coded.close()
