@@ -253,7 +253,8 @@ def batch_report(args, cfg, results, link):
                    "batch": args.batch, "decode_tokens_per_step": cfg.tokens},
         "runs": {f"{r['policy']}-s{r['slots']}": rates(r) for r in results},
         "roofline": {
-            "kernel": "prefill_gemm_kernel<true>", "bound": "hbm",
+            "kernel": "prefill_skinny_kernel<true>" if args.batch <= 32 else "prefill_gemm_kernel<true>",
+            "bound": "hbm",
             "achieved": round(up_gbps, 1) if up_gbps else None, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(up_gbps / HBM_PEAK_GBPS, 4) if up_gbps else None, "traffic": None,
             "bytes_per_launch": up_bytes // max(1, tim["gemm_up_n"] // steps),
@@ -261,7 +262,8 @@ def batch_report(args, cfg, results, link):
             "launches": tim["gemm_up_n"],
             "note": "weights of every routed expert (W1, W3) streamed once per batch",
         },
-        "gemm_down": {"achieved_gbps": round(down_bytes / down_s / 1e9, 1) if down_s > 0 else None,
+        "gemm_down": {"kernel": "prefill_skinny_kernel<false>" if args.batch <= 32 else "prefill_gemm_kernel<false>",
+                      "achieved_gbps": round(down_bytes / down_s / 1e9, 1) if down_s > 0 else None,
                       "avg_launch_us": round(1e3 * tim["gemm_down_ms"] / max(1, tim["gemm_down_n"]), 2)},
         "experts_per_batch_layer": round(used / max(1, (cfg.tokens // args.batch) * cfg.layers), 3),
         "link": {"bytes_per_step": fetched, "achieved_over_decode_gbps": round(link_gbps, 2),

@@ -901,16 +901,34 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   };
   const size_t ngroups = batches.size() + 1;
   std::vector<int> up_first(ngroups), up_n(ngroups), dn_first(ngroups), dn_n(ngroups), up_rows(ngroups),
-      dn_rows(ngroups);
+      dn_rows(ngroups), skinny(ngroups, 0);
   std::vector<double> group_rows(ngroups, 0.0);
-  add_tiles(resident, c->dff, up_first[0], up_n[0], up_rows[0]);
-  add_tiles(resident, c->d, dn_first[0], dn_n[0], dn_rows[0]);
-  for (int e : resident) group_rows[0] += pl[e].n;
-  for (size_t bi = 0; bi < batches.size(); ++bi) {
-    add_tiles(batches[bi], c->dff, up_first[bi + 1], up_n[bi + 1], up_rows[bi + 1]);
-    add_tiles(batches[bi], c->d, dn_first[bi + 1], dn_n[bi + 1], dn_rows[bi + 1]);
-    for (int e : batches[bi]) group_rows[bi + 1] += pl[e].n;
-  }
+  // a group whose experts all have few rows (batched decode) goes to the
+  // small-M kernels: one tile per expert, shared by the up and down launches
+  auto add_group = [&](const std::vector<int> &group, size_t gi) {
+    int most = 0;
+    for (int e : group) {
+      most = std::max(most, pl[e].n);
+      group_rows[gi] += pl[e].n;
+    }
+    if (most <= kSkinnyRows) {
+      skinny[gi] = 1;
+      up_first[gi] = dn_first[gi] = nt;
+      for (int e : group) {
+        if (nt >= p.tile_cap) {
+          overflow = true;
+          continue;
+        }
+        ht[nt++] = GemmTile{e, 0, 0, 0};
+      }
+      up_n[gi] = dn_n[gi] = nt - up_first[gi];
+    } else {
+      add_tiles(group, c->dff, up_first[gi], up_n[gi], up_rows[gi]);
+      add_tiles(group, c->d, dn_first[gi], dn_n[gi], dn_rows[gi]);
+    }
+  };
+  add_group(resident, 0);
+  for (size_t bi = 0; bi < batches.size(); ++bi) add_group(batches[bi], bi + 1);
   if (overflow) {  // cannot happen: the capacity counts 64 x 64 tiles
     c->sticky = MOE_ERR_HIP;
     return fail(MOE_ERR_HIP, "prefill tile schedule overflow (capacity %d)", p.tile_cap);
@@ -976,10 +994,16 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     if (up_n[gi] <= 0) return MOE_OK;
     Launch lu, ld;
     HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_GEMM_UP));
-    HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, up_rows[gi], lu));
+    if (skinny[gi])
+      HIP_TRY(c, launch_prefill_skinny_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, lu));
+    else
+      HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, up_rows[gi], lu));
     kernel_span_done(c, SPAN_GEMM_UP, lu, group_rows[gi] * up_flop_per_row);
     HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
-    HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, dn_rows[gi], ld));
+    if (skinny[gi])
+      HIP_TRY(c, launch_prefill_skinny_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, ld));
+    else
+      HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, dn_rows[gi], ld));
     kernel_span_done(c, SPAN_GEMM_DOWN, ld, group_rows[gi] * down_flop_per_row);
     return MOE_OK;
   };

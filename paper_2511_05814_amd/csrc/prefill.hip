@@ -543,6 +543,142 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
       }
 }
 
+// Small-M grouped GEMM: groups whose experts have at most kSkinnyRows rows
+// (batched decode).  The tiled kernel above stages 128-row slices through LDS
+// and, with a handful of rows per expert, streams the weights at a few TB/s
+// on too few resident waves.  Here a workgroup owns 16 output features of one
+// expert for all of its rows (up to 32: two 16-row MFMA blocks).  Its four
+// waves split K in four; each streams its quarter of the 16 weight rows (of W1
+// and W3 in the up projection) from global memory straight into
+// v_mfma_f32_16x16x32_bf16 fragments, several 32-deep steps ahead, with
+// the rows' activations read alongside (from L2: every workgroup of the expert
+// reads them).  A row or feature past the end reads a valid row instead (its
+// outputs are not written); only a K tail that is not a multiple of 32 is
+// zeroed.  The four partial products meet in LDS and are added in wave order.
+constexpr int kSkinnyAheadUp = 8, kSkinnyAheadDown = 8;  // steps in flight per wave
+
+__device__ __forceinline__ bf16x8 load_frag(const uint16_t *p) {
+  const uint4 v = *reinterpret_cast<const uint4 *>(p);
+  bf16x8 r;
+  __builtin_memcpy(&r, &v, sizeof v);
+  return r;
+}
+
+template <bool UP, int AHEAD>
+__global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *tiles, const GemmJob *jobs,
+                                                             const uint16_t *a_src, const int32_t *perm_tok,
+                                                             void *out, int d, int d_ff) {
+  constexpr int NB = UP ? 2 : 1;  // B matrices: W1 and W3, or W2
+  __shared__ floatx4 red[4][NB][2][kWave];
+  const int K = UP ? d : d_ff;  // reduction length
+  const int N = UP ? d_ff : d;  // output features
+  const int nfb = (N + 15) / 16;
+  const int ti = blockIdx.x / nfb, fb = blockIdx.x - ti * nfb;
+  const GemmJob j = jobs[tiles[ti].job];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int M = min(j.nrows, kSkinnyRows);
+  if (M <= 0) return;       // the host makes tiles only for experts with rows
+  const bool two = M > 16;  // second 16-row block
+  const int kg = (lane / 16) * 8;  // this lane's 8 elements of a 32-deep step
+  // A rows (tokens of the expert) and B rows (features) of this lane, clamped
+  const uint16_t *ap[2];
+#pragma unroll
+  for (int tb = 0; tb < 2; ++tb) {
+    const int m = min(tb * 16 + lane % 16, M - 1);
+    ap[tb] = (UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff) + kg;
+  }
+  const int f = min(fb * 16 + lane % 16, N - 1);
+  const uint16_t *bp[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    bp[b] = j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)f * K + kg;
+
+  floatx4 c[NB][2];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) c[b][tb] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  // this wave's full 32-deep steps
+  const int full = K / 32;
+  const int q = (full + 3) / 4;
+  const int s0 = min(wave * q, full), s1 = min(s0 + q, full);
+  const int n = s1 - s0;
+  bf16x8 wa[AHEAD][NB], xa[AHEAD][2];
+  auto load = [&](int slot, int step) {
+    const int k = step * 32;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) wa[slot][b] = load_frag(bp[b] + k);
+    xa[slot][0] = load_frag(ap[0] + k);
+    if (two) xa[slot][1] = load_frag(ap[1] + k);
+  };
+  auto mma = [&](int slot) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      c[b][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[slot][0], wa[slot][b], c[b][0], 0, 0, 0);
+      if (two) c[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[slot][1], wa[slot][b], c[b][1], 0, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int u = 0; u < AHEAD; ++u)
+    if (u < n) load(u, s0 + u);
+  for (int i = 0; i < n; i += AHEAD) {
+#pragma unroll
+    for (int u = 0; u < AHEAD; ++u) {
+      if (i + u < n) {
+        mma(u);
+        if (i + u + AHEAD < n) load(u, s0 + i + u + AHEAD);
+      }
+    }
+  }
+  // K tail (K not a multiple of 32): the last wave adds it, zeroing past K
+  if (K % 32 && wave == 3) {
+    const bool in = full * 32 + kg < K;
+    const int k = in ? full * 32 : 0;  // lanes past K read their row's start, then take zeros
+    const bf16x8 z = {};
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const bf16x8 v = load_frag(bp[b] + k);
+      wa[0][b] = in ? v : z;
+    }
+    const bf16x8 x0 = load_frag(ap[0] + k), x1 = load_frag(ap[1] + k);
+    xa[0][0] = in ? x0 : z;
+    xa[0][1] = in ? x1 : z;
+    mma(0);
+  }
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) red[wave][b][tb][lane] = c[b][tb];
+  __syncthreads();
+  if (wave == 0) {
+    floatx4 r[NB][2];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) {
+        r[b][tb] = red[0][b][tb][lane];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) r[b][tb] += red[w][b][tb][lane];
+      }
+    const int n_out = fb * 16 + lane % 16;
+    if (n_out < N) {
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = tb * 16 + (lane / 16) * 4 + i;
+          if (m >= M) continue;
+          if (UP)
+            static_cast<uint16_t *>(out)[(size_t)(j.row0 + m) * N + n_out] =
+                f32_to_bf16_rne(silu(r[0][tb][i]) * r[NB - 1][tb][i]);
+          else
+            static_cast<float *>(out)[(size_t)(j.row0 + m) * N + n_out] = r[0][tb][i];
+        }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // 4. h_t += sum_r g_tr Y[pos(t, r)], ranks in order
 __global__ __launch_bounds__(256) void prefill_unpermute_kernel(float *H, const float *Y, const float *g,
@@ -579,6 +715,22 @@ hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *j
   else
     MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, 128>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn,
                perm_tok, (void *)act, d, d_ff);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_skinny_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
+                                    const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l) {
+  if (ntiles <= 0) return hipSuccess;
+  MOE_LAUNCH((prefill_skinny_kernel<true, kSkinnyAheadUp>), dim3(ntiles * ((d_ff + 15) / 16)), dim3(256), 0, l, tiles, jobs, xn,
+             perm_tok, (void *)act, d, d_ff);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
+                                      float *Y, int d, int d_ff, const Launch &l) {
+  if (ntiles <= 0) return hipSuccess;
+  MOE_LAUNCH((prefill_skinny_kernel<false, kSkinnyAheadDown>), dim3(ntiles * ((d + 15) / 16)), dim3(256), 0, l, tiles, jobs, act,
+             nullptr, (void *)Y, d, d_ff);
   return hipGetLastError();
 }
 
