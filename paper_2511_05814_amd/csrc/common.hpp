@@ -82,6 +82,8 @@ struct RouterArgs {
   int demand;              // 1: route + look up `layer`
   int spec_layer;          // >= 0: guess that layer's experts from h and prefetch
   int pmax;                // prefetch at most this many guesses
+  double *zbuf;            // [2 * kMaxE] gate logits when the GEMV is a launch of its own
+  int phase;               // 0: one launch; 1: GEMV over several workgroups; 2: the rest
 };
 
 struct FfnArgs {

@@ -45,7 +45,7 @@ int fail(int code, const char *fmt, ...) {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
-  size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, act = 0, part = 0,
+  size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, rz = 0, act = 0, part = 0,
          hostptrs = 0, prefill = 0, staging = 0, total = 0;
 };
 
@@ -339,6 +339,7 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.route = take(sizeof(RouteOut));
   l.hostptrs = take(sizeof(void *) * c->L);
   l.err = take(256);
+  l.rz = take(sizeof(double) * 2 * kMaxE);  // router logits of a separate GEMV launch
   l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff, d->dtype) * d->d_model);
   const uint64_t B = expert_bytes(d);
@@ -500,6 +501,7 @@ int moe_cache_reset(moe_cache_t *c) {
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.plists, 0, sizeof(FetchList) * c->L, c->cs));
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.route, 0, sizeof(RouteOut), c->cs));
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.err, 0, 256, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.rz, 0, sizeof(double) * 2 * kMaxE, c->cs));
   {
     // the copy kernel dereferences this table: check it survived
     std::vector<const uint8_t *> got(c->L);
@@ -635,6 +637,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.demand = demand;
   a.spec_layer = spec_layer;
   a.pmax = pmax;
+  a.zbuf = reinterpret_cast<double *>(c->ws + c->lay.rz);
   Launch lr;
   HIP_TRY(c, kernel_span(c, c->cs, &lr, SPAN_ROUTER));
   HIP_TRY(c, launch_router(a, lr));

@@ -1,6 +1,8 @@
 // Router and cache-table kernel for batch-1 decode.
 //
-// One workgroup per call.  All 16 waves first compute the gate logits
+// One workgroup per call; beyond 32 gate rows a first launch spreads the GEMV
+// over several workgroups (one row per wave) and the single workgroup of a
+// second launch reads the logits back.  All 16 waves first compute the gate logits
 // z = W_g h (Sec. 4.3: the gate is a linear map [len_hidden, num_experts]) for
 // the layer being decoded and, when speculating, for the next layer (Sec. 3.2:
 // the next layer's gate applied to the current hidden state).  Each product
@@ -40,23 +42,26 @@ constexpr int kBatch = 8;
 constexpr int kMaxD = 16384;
 
 struct GateWork {
-  int n = 0, cpr = 1;  // (row, chunk) items of this wave; chunks per row
+  int n = 0, cpr = 1;        // (row, chunk) items of this wave; chunks per row
+  int first = 0, stride = 1;  // this wave's rows: first, first + stride, ...
 };
 
+// Rows r0 .. r1-1 are dealt out one per wave across the grid's workgroups.
 template <int DT>
 __device__ __forceinline__ GateWork gate_work(const RouterArgs &a, int r0, int r1, int wave) {
   constexpr int EPL = DT == 1 ? 8 : 4;  // elements per 16-byte load
   GateWork g;
   g.cpr = (a.d + kWave * EPL - 1) / (kWave * EPL);
-  const int M = r0 + wave < r1 ? (r1 - r0 - wave + kWaves - 1) / kWaves : 0;
+  g.first = r0 + (int)blockIdx.x * kWaves + wave;
+  g.stride = (int)gridDim.x * kWaves;
+  const int M = g.first < r1 ? (r1 - g.first + g.stride - 1) / g.stride : 0;
   g.n = M * g.cpr;
   return g;
 }
 
 // Issue the weight loads of items j0 .. j0 + kBatch - 1 (n > 0).
 template <int DT>
-__device__ __forceinline__ void gate_load(const RouterArgs &a, int r0, int wave, int lane, const GateWork &g,
-                                          int j0, uint4 *v) {
+__device__ __forceinline__ void gate_load(const RouterArgs &a, int lane, const GateWork &g, int j0, uint4 *v) {
   constexpr int EPL = DT == 1 ? 8 : 4;
   constexpr int ESZ = DT == 1 ? 2 : 4;
   const int E = a.E, d = a.d;
@@ -64,7 +69,7 @@ __device__ __forceinline__ void gate_load(const RouterArgs &a, int r0, int wave,
 #pragma unroll
   for (int u = 0; u < kBatch; ++u) {
     const int j = min(j0 + u, g.n - 1);
-    const int row = r0 + wave + kWaves * (j / g.cpr);
+    const int row = g.first + g.stride * (j / g.cpr);
     const int gl = row < E ? a.layer : a.spec_layer;
     const int e = row < E ? row : row - E;
     const int col = min((j % g.cpr) * kWave * EPL + lane * EPL, d - EPL);
@@ -72,15 +77,16 @@ __device__ __forceinline__ void gate_load(const RouterArgs &a, int r0, int wave,
   }
 }
 
-// v holds the first batch, loaded by gate_load(.., 0, v) before h was staged.
+// v holds the first batch, loaded by gate_load(.., 0, v) before h was staged;
+// logit `row` goes to zs[row].
 template <int DT>
-__device__ void gate_logits(const RouterArgs &a, const float *hs, int r0, int wave, int lane,
-                            const GateWork &g, uint4 *v, double *zs) {
+__device__ void gate_logits(const RouterArgs &a, const float *hs, int lane, const GateWork &g, uint4 *v,
+                            double *zs) {
   constexpr int EPL = DT == 1 ? 8 : 4;
   const int d = a.d, n = g.n, cpr = g.cpr;
   double acc = 0.0;
   for (int j0 = 0; j0 < n; j0 += kBatch) {
-    if (j0 > 0) gate_load<DT>(a, r0, wave, lane, g, j0, v);
+    if (j0 > 0) gate_load<DT>(a, lane, g, j0, v);
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int j = j0 + u;
@@ -110,7 +116,7 @@ __device__ void gate_logits(const RouterArgs &a, const float *hs, int r0, int wa
         }
         if (c == cpr - 1) {
           const double z = wave_sum_d(acc);
-          if (lane == 0) zs[r0 + wave + kWaves * (j / cpr)] = z;
+          if (lane == 0) zs[g.first + g.stride * (j / cpr)] = z;
           acc = 0.0;
         }
       }
@@ -182,7 +188,18 @@ __device__ int wave_victim(bool cand, int policy, int aging, int64_t clock, uint
   return bv ? bl : -1;
 }
 
-__device__ void put_rec(const RouterArgs &a, uint64_t idx, int kind, int64_t token, int layer,
+// Value of x on lane src, for a src the whole wave agrees on (a scalar read,
+// not an LDS round trip like a general shuffle).
+__device__ __forceinline__ int lane_value(int x, int src) { return __builtin_amdgcn_readlane(x, src); }
+
+// Ring position of record base + r, from base % cap computed once.
+__device__ __forceinline__ uint64_t ring_pos(uint64_t base_pos, int r, uint64_t cap, int K) {
+  uint64_t pos = base_pos + (uint64_t)r;
+  if (pos >= cap) pos = cap >= (uint64_t)K ? pos - cap : pos % cap;
+  return pos;
+}
+
+__device__ void put_rec(const RouterArgs &a, uint64_t pos, int kind, int64_t token, int layer,
                         int rank, int expert, int flags, int slot, int victim) {
   if (a.trace == nullptr || a.trace_cap == 0) return;
   TraceRec r;
@@ -194,7 +211,7 @@ __device__ void put_rec(const RouterArgs &a, uint64_t idx, int kind, int64_t tok
   r.flags = flags;
   r.slot = slot;
   r.victim = victim;
-  a.trace[idx % a.trace_cap] = r;
+  a.trace[pos] = r;
 }
 
 // Wave 0: the token's K lookups in layer a.layer, in rank order.
@@ -213,14 +230,15 @@ __device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t
   const int64_t token = tv.lookups;
 
   bool pinned = false;
-  for (int r = 0; r < K; ++r) pinned |= (__shfl(idreg, r, kWave) == lane);
+  for (int r = 0; r < K; ++r) pinned |= (lane_value(idreg, r) == lane);
+  const uint64_t base_pos = a.trace_cap ? rec_base % a.trace_cap : 0;
 
   int n_miss = 0, hits = 0, useful = 0, wasted = 0;
   for (int r = 0; r < K; ++r) {
-    const int j = __shfl(idreg, r, kWave);
+    const int j = lane_value(idreg, r);
     clock += 1;
-    const int slot_j = __shfl(my_slot, j, kWave);
-    const int pf_j = __shfl(my_pf, j, kWave);
+    const int slot_j = lane_value(my_slot, j);
+    const int pf_j = lane_value(my_pf, j);
     if (lane == j) {
       my_count += 1;
       my_last = clock;
@@ -242,8 +260,8 @@ __device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t
         if (lane == 0) *a.err = ERR_BAD_LIST;
         break;
       }
-      const int s = __shfl(my_slot, v, kWave);
-      const int pf_v = __shfl(my_pf, v, kWave);
+      const int s = lane_value(my_slot, v);
+      const int pf_v = lane_value(my_pf, v);
       if (pf_v) wasted += 1;
       if (lane == v) {
         my_slot = -1;
@@ -264,7 +282,7 @@ __device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t
       a.route->ids[r] = j;
       a.route->slot[r] = slot;
       a.route->hit[r] = flags & 1;
-      put_rec(a, rec_base + r, REC_ACCESS, token, a.layer, r, j, flags, slot, victim);
+      put_rec(a, ring_pos(base_pos, r, a.trace_cap, K), REC_ACCESS, token, a.layer, r, j, flags, slot, victim);
     }
   }
   // prefetched experts this token did not use are wasted
@@ -312,12 +330,13 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
   const int64_t token = tv.lookups;
 
   bool pinned = false;
-  for (int r = 0; r < K; ++r) pinned |= (__shfl(greg, r, kWave) == lane);
+  for (int r = 0; r < K; ++r) pinned |= (lane_value(greg, r) == lane);
+  const uint64_t base_pos = a.trace_cap ? rec_base % a.trace_cap : 0;
 
   int issued = 0, wasted = 0;
   for (int r = 0; r < K; ++r) {
-    const int j = __shfl(greg, r, kWave);
-    const int slot_j = __shfl(my_slot, j, kWave);
+    const int j = lane_value(greg, r);
+    const int slot_j = lane_value(my_slot, j);
     int flags = 0, slot = -1, victim = -1;
     if (slot_j >= 0) {
       flags = 1;
@@ -330,8 +349,8 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
         if (lane == 0) *a.err = ERR_BAD_LIST;
         break;
       }
-      const int s = __shfl(my_slot, v, kWave);
-      const int pf_v = __shfl(my_pf, v, kWave);
+      const int s = lane_value(my_slot, v);
+      const int pf_v = lane_value(my_pf, v);
       if (pf_v) wasted += 1;
       if (lane == v) {
         my_slot = -1;
@@ -352,7 +371,7 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
       slot = s;
       victim = v;
     }
-    if (lane == 0) put_rec(a, rec_base + r, REC_PREFETCH, token, L2, r, j, flags, slot, victim);
+    if (lane == 0) put_rec(a, ring_pos(base_pos, r, a.trace_cap, K), REC_PREFETCH, token, L2, r, j, flags, slot, victim);
   }
   if (in_range) {
     T->expert_slot[lane] = my_slot;
@@ -385,20 +404,26 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   const bool spec = a.spec_layer >= 0;
 
   // Every global read that does not depend on another is issued first: the
-  // tables and counters of waves 0 and 1, the first batch of gate rows, then h.
+  // tables and counters of waves 0 and 1, the first batch of gate rows (or,
+  // after a separate GEMV launch, its logits), then h.
+  const int phase = a.phase;
   TableView tv{};
-  if (wave == 0 && a.demand) tv = load_table(a.tables + a.layer, a.stats + a.layer, lane, E);
-  if (wave == 1 && spec) tv = load_table(a.tables + a.spec_layer, a.stats + a.spec_layer, lane, E);
+  if (phase != 1) {
+    if (wave == 0 && a.demand) tv = load_table(a.tables + a.layer, a.stats + a.layer, lane, E);
+    if (wave == 1 && spec) tv = load_table(a.tables + a.spec_layer, a.stats + a.spec_layer, lane, E);
+  }
   const int r0 = route_here ? 0 : E, r1 = spec ? 2 * E : E;
+  double zv = 0.0;  // clamped index, not a guarded load (one would be waited for on the spot)
+  if (phase == 2) zv = a.zbuf[min(r0 + tid, 2 * kMaxE - 1)];
   uint4 gv[kBatch];
   GateWork gw;
-  if (route_here || spec) {
+  if (phase != 2 && (route_here || spec)) {
     gw = a.dtype == 1 ? gate_work<1>(a, r0, r1, wave) : gate_work<0>(a, r0, r1, wave);
     if (gw.n > 0) {
       if (a.dtype == 1)
-        gate_load<1>(a, r0, wave, lane, gw, 0, gv);
+        gate_load<1>(a, lane, gw, 0, gv);
       else
-        gate_load<0>(a, r0, wave, lane, gw, 0, gv);
+        gate_load<0>(a, lane, gw, 0, gv);
     }
   }
   if (tid == 0) {
@@ -418,12 +443,17 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     }
     ss = wave_sum_d(ss);
     if (lane == 0) red[wave] = ss;
+    if (phase == 2 && r0 + tid < r1) zs[r0 + tid] = zv;
     __syncthreads();
-    if (a.dtype == 1)
-      gate_logits<1>(a, hs, r0, wave, lane, gw, gv, zs);
-    else
-      gate_logits<0>(a, hs, r0, wave, lane, gw, gv, zs);
+    if (phase != 2) {
+      double *zout = phase == 1 ? a.zbuf : zs;
+      if (a.dtype == 1)
+        gate_logits<1>(a, hs, lane, gw, gv, zout);
+      else
+        gate_logits<0>(a, hs, lane, gw, gv, zout);
+    }
   }
+  if (phase == 1) return;  // the GEMV launch is done; the next launch reads zbuf
   __syncthreads();
   if (route_here && tid == 0) {
     double t = 0.0;
@@ -448,7 +478,7 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
       idreg = (lane < a.K) ? a.inj_ids[lane] : -1;
       bool ok = true;
       for (int r = 0; r < a.K; ++r) {
-        const int j = __shfl(idreg, r, kWave);
+        const int j = lane_value(idreg, r);
         const unsigned long long same = __ballot(lane < a.K && idreg == j);
         ok = ok && j >= 0 && j < E && __popcll(same) == 1;
       }
@@ -465,7 +495,7 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
         if (lane == 0) a.route->inv_r = 0.0f;
       }
     }
-    if (__shfl(idreg, 0, kWave) >= 0) {
+    if (lane_value(idreg, 0) >= 0) {
       demand_lookup(a, idreg, lane, s_tbase, tv);
       if (lane == 0) s_demand_ok = 1;
     }
@@ -482,7 +512,22 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
 }  // namespace
 
 hipError_t launch_router(const RouterArgs &a, const Launch &l) {
-  MOE_LAUNCH(router_kernel, dim3(1), dim3(kThreads), 0, l, a);
+  // One workgroup converts and multiplies in fp64 at about 1 us per 16 gate
+  // rows on MI355X; beyond 32 rows (32 or 64 experts) the GEMV runs as its
+  // own launch, one row per wave, and the table work as a second one.  (A
+  // single launch whose last workgroup took over cost about 7 us in fences.)
+  const int rows = (a.demand && a.inj_ids == nullptr ? a.E : 0) + (a.spec_layer >= 0 ? a.E : 0);
+  if (rows <= 32) {
+    RouterArgs one = a;
+    one.phase = 0;
+    MOE_LAUNCH(router_kernel, dim3(1), dim3(kThreads), 0, l, one);
+    return hipGetLastError();
+  }
+  RouterArgs g = a, t = a;
+  g.phase = 1;
+  t.phase = 2;
+  MOE_LAUNCH(router_kernel, dim3((rows + kWaves - 1) / kWaves), dim3(kThreads), 0, (Launch{l.s, l.start, nullptr}), g);
+  MOE_LAUNCH(router_kernel, dim3(1), dim3(kThreads), 0, (Launch{l.s, nullptr, l.stop}), t);
   return hipGetLastError();
 }
 
