@@ -288,6 +288,9 @@ def main():
     ap.add_argument("--tokens", type=int, default=0,
                     help="decode only the first N tokens of the workload (profiling passes)")
     ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
+    ap.add_argument("--layers", type=int, default=0, help="run only the first N layers of the workload")
+    ap.add_argument("--prefill-tokens", type=int, default=-1,
+                    help="prefill at most this many tokens (0: decode only)")
     ap.add_argument("--slots", type=int, default=0,
                     help="HBM slots per layer (default 4, 16 for the 64-expert workload; "
                          "slots = experts keeps every expert resident)")
@@ -315,6 +318,10 @@ def main():
         cfg = cfg.with_(prefetch_max=min(args.prefetch_max, cfg.top_k))
     if args.tokens:
         cfg = cfg.with_(tokens=min(args.tokens, cfg.tokens))
+    if args.layers:
+        cfg = cfg.with_(layers=min(args.layers, cfg.layers))
+    if args.prefill_tokens >= 0:
+        cfg = cfg.with_(prefill_tokens=min(args.prefill_tokens, cfg.prefill_tokens))
     fetch_mode = {"kernel": b.MOE_FETCH_KERNEL, "dma": b.MOE_FETCH_DMA, "split": b.MOE_FETCH_SPLIT}[args.fetch]
     primary_slots = args.slots or (16 if cfg.experts == 64 else 4)
     if not cfg.top_k <= primary_slots <= cfg.experts:
@@ -453,7 +460,9 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": DESCRIPTIONS[args.workload] + (f" (first {cfg.tokens} tokens)" if args.tokens else "")
-                        + (f"; run with {head['slots']} slots per layer" if args.slots else ""),
+                        + (f"; run with {head['slots']} slots per layer" if args.slots else "")
+                        + (f"; first {cfg.layers} layers" if args.layers else "")
+                        + (f"; {cfg.prefill_tokens}-token prefill" if args.prefill_tokens >= 0 else ""),
             "weights_dtype": cfg.dtype,
             "policy": head["policy"],
             "slots": head["slots"],
