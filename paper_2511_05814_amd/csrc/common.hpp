@@ -141,6 +141,12 @@ struct PlanArgs {
   uint64_t expert_bytes;
   int T, K, E, S, layer, policy;
   int aging;  // aged LFU: lookup-clock ticks per halving of a count
+  // Batches planned on the device (every expert resident, small-M GEMMs):
+  // the kernel also writes one GEMM job and tile per expert; nullptr otherwise.
+  GemmJob *jobs;
+  GemmTile *tiles;
+  const uint8_t *arena_layer;  // this layer's slots
+  uint64_t slot_bytes;
 };
 
 // Where a kernel goes: its stream and, when kernel timing is on, two events

@@ -816,7 +816,30 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   pa.layer = layer;
   pa.policy = c->policy;
   pa.aging = c->policy == MOE_POLICY_LFU_AGED ? c->desc.aging_ticks : 0;
+  // With a slot for every expert nothing is ever streamed, and with at most
+  // kSkinnyRows tokens every expert's rows fit the small-M GEMMs: the plan
+  // kernel then writes the GEMM jobs itself and the host does not wait for it.
+  const bool device_plan = c->S == c->E && T <= kSkinnyRows;
+  pa.jobs = device_plan ? jobs : nullptr;
+  pa.tiles = device_plan ? tiles : nullptr;
+  pa.arena_layer = arena + (size_t)layer * c->S * c->B;
+  pa.slot_bytes = c->B;
   HIP_TRY(c, launch_prefill_plan(pa, Launch{c->cs}));
+  if (device_plan) {
+    const double rows = (double)T * c->K;
+    Launch lu, ld;
+    HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_GEMM_UP));
+    HIP_TRY(c, launch_prefill_skinny_up(tiles, c->E, jobs, xn, perm, act, c->d, c->dff, lu));
+    kernel_span_done(c, SPAN_GEMM_UP, lu, rows * 4.0 * c->d * c->dff);
+    HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
+    HIP_TRY(c, launch_prefill_skinny_down(tiles, c->E, jobs, act, Y, c->d, c->dff, ld));
+    kernel_span_done(c, SPAN_GEMM_DOWN, ld, rows * 2.0 * c->d * c->dff);
+    HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, Launch{c->cs}));
+    HIP_TRY(c, span_end(c, c->cs, SPAN_PREFILL, tp));
+    c->last_route_kind = 2;
+    c->last_prefill_T = T;
+    return MOE_OK;  // routing errors surface at the next synchronising call
+  }
   HIP_TRY(c, hipMemcpyAsync(c->h_plan, plan, sizeof(PrefillPlan) * c->E, hipMemcpyDeviceToHost, c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   {

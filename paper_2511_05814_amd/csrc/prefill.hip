@@ -227,6 +227,10 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
     lastp[tid] = 0;
   }
   if (tid == 0) bad = 0;
+  if (a.jobs && tid < E) {  // empty until the table step below fills them in
+    a.jobs[tid] = GemmJob{nullptr, 0, 0};
+    a.tiles[tid] = GemmTile{tid, 0, 0, 0};
+  }
   __syncthreads();
   for (int p = tid; p < P; p += 1024) {
     const int e = a.ids[p];
@@ -361,6 +365,11 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
     pl.newcomer = newcomer ? 1 : 0;
     pl.pad[0] = pl.pad[1] = pl.pad[2] = 0;
     a.plan[lane] = pl;
+    if (a.jobs) {
+      // every expert with rows is resident after the batch on this path
+      if (n > 0 && slot1 < 0) *a.err = ERR_BAD_LIST;
+      if (slot1 >= 0) a.jobs[lane] = GemmJob{reinterpret_cast<const uint16_t *>(a.arena_layer + (size_t)slot1 * a.slot_bytes), offs[lane], n};
+    }
     if (a.trace && a.trace_cap) {
       TraceRec r;
       r.kind = REC_PREFILL;

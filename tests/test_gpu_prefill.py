@@ -98,6 +98,22 @@ def test_prefill_ragged_shapes():
     rig.store.close()
 
 
+@pytest.mark.parametrize("T", [1, 13, 32])
+def test_device_planned_batches(T):
+    # a slot for every expert and at most 32 tokens: the plan kernel writes the
+    # GEMM jobs and the host does not read the plan back; ragged d and d_ff
+    # (K tails of the small-M GEMMs), 5 experts, top-3 (32 tokens can give an
+    # expert 32 rows: two 16-row MFMA blocks)
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=2, experts=5, top_k=3, d_model=136, d_ff=200,
+                                         dtype="bf16", tokens=4, prefill_tokens=32)
+    _say("device-planned batch", T)
+    rig = Rig(cfg)
+    moe = rig.cache(5, "lfu", max_prefill_tokens=32)
+    prefill_and_check(rig, moe, "lfu", 5, T, list(range(T)))
+    moe.close()
+    rig.store.close()
+
+
 def test_prefill_rejects_bad_token_counts():
     cfg = wl.CONFIGS["tiny-stack"].with_(layers=1, dtype="bf16", d_model=64, d_ff=64)
     rig = Rig(cfg)
@@ -111,18 +127,20 @@ def test_prefill_rejects_bad_token_counts():
     rig.store.close()
 
 
-def test_batched_decode_mixtral_shape():
+@pytest.mark.parametrize("slots", [4, 8])
+def test_batched_decode_mixtral_shape(slots):
     # batched decode through the batch path: three batches of 8 tokens through
-    # the Mixtral-shaped layer (d 4096, d_ff 14336), LRU, 4 slots; each batch
-    # must continue from the state the previous one left
+    # the Mixtral-shaped layer (d 4096, d_ff 14336), LRU; each batch must
+    # continue from the state the previous one left.  With 8 slots (every
+    # expert resident) the batches are planned on the device.
     cfg = wl.CONFIGS["mixtral-layer"].with_(tokens=24)
-    _say("batched decode mixtral-layer", cfg)
+    _say("batched decode mixtral-layer, slots", slots)
     rig = Rig(cfg)
     B, K = 8, cfg.top_k
-    moe = rig.cache(4, "lru", max_prefill_tokens=B)
+    moe = rig.cache(slots, "lru", max_prefill_tokens=B)
     h = wl.hidden_states(cfg, cfg.tokens)
     H = torch.from_numpy(np.ascontiguousarray(h)).to("cuda")
-    caches = make_caches(1, cfg.experts, 4, "lru")
+    caches = make_caches(1, cfg.experts, slots, "lru")
     worst = 0.0
     for g in range(0, cfg.tokens, B):
         rows = H[g:g + B]
