@@ -227,7 +227,11 @@ int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts
  * largest key stay resident: LFU the count, aged LFU the aged count at the
  * batch's last tick, LRU the last use; ties: resident first, lower id).  Kept
  * experts keep their slots; newcomers take the freed slots.  tokens must be
- * in 1..max_prefill_tokens. Enqueue only. */
+ * in 1..max_prefill_tokens.  The host waits for the device's plan of the batch
+ * (a few hundred bytes) before it issues the copies of streamed experts and
+ * sizes the GEMMs; when every expert has a slot (slots == experts) and tokens
+ * <= 32 the plan stays on the device and the call only enqueues, and a bad
+ * routing then surfaces at the next synchronising call. */
 int moe_prefill_layer(moe_cache_t *c, int layer, float *H, int tokens);
 
 /* Injected routing (test hook): run layer `layer`'s cache lookup, fetches and
