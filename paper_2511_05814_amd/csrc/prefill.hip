@@ -66,7 +66,7 @@ __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v));
 // B always pair the same column.  The waves' partial sums meet in LDS and
 // are added in wave order.
 constexpr int kGateWaves = 4;
-constexpr int kGateAhead = 2;  // blocks in flight per wave
+constexpr int kGateAhead = 8;  // blocks in flight per wave (the loop is latency-bound)
 
 struct GateBlock {
   float4 h;              // 4 columns of this lane's token row
@@ -74,9 +74,28 @@ struct GateBlock {
   float4 wf[kMaxE / 16]; // fp32 gate weights instead (dtype 0)
 };
 
-template <int DT>
+// FAST (d a multiple of 16 * kGateWaves * kGateAhead): every block the loop
+// multiplies lies inside d, so loads are unconditional; the look-ahead past
+// the end reads the row's last columns and is never used, and rows past T or
+// experts past E (clamped to the last valid one) only feed logits nobody reads.
+// A guarded load would be waited for on the spot.
+template <int DT, bool FAST>
 __device__ __forceinline__ void gate_load(GateBlock &b, const float *hrow, const uint8_t *wbase, int ng, int k,
                                           int d, int E, int i) {
+  if (FAST) {
+    const int kk = min(k, d - 4);
+    b.h = *reinterpret_cast<const float4 *>(hrow + kk);
+#pragma unroll
+    for (int g = 0; g < kMaxE / 16; ++g) {
+      if (g >= ng) break;
+      const int e = min(16 * g + i, E - 1);
+      if (DT == 1)
+        b.w[g] = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(wbase) + (size_t)e * d + kk);
+      else
+        b.wf[g] = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(wbase) + (size_t)e * d + kk);
+    }
+    return;
+  }
   b.h = make_float4(0.f, 0.f, 0.f, 0.f);
   if (hrow && k < d) b.h = *reinterpret_cast<const float4 *>(hrow + k);
 #pragma unroll
@@ -119,13 +138,14 @@ __device__ __forceinline__ void gate_mfma(const GateBlock &b, int ng, double4_t 
   }
 }
 
-template <int DT>
+template <int DT, bool FAST>
 __device__ __forceinline__ void gate_partial(const PrefillArgs &a, int t0, int wave, int lane,
                                              double (*zp)[kGateTok][kMaxE], double (*rp)[kGateTok]) {
   const int d = a.d, E = a.E;
   const int i = lane % 16, kq = lane / 16;
   const int ng = (E + 15) / 16;
-  const float *hrow = t0 + i < a.T ? a.H + (size_t)(t0 + i) * d : nullptr;
+  const float *hrow = FAST ? a.H + (size_t)min(t0 + i, a.T - 1) * d
+                           : (t0 + i < a.T ? a.H + (size_t)(t0 + i) * d : nullptr);
   const uint8_t *wbase = static_cast<const uint8_t *>(a.gate);
   double4_t acc[kMaxE / 16];
 #pragma unroll
@@ -134,12 +154,12 @@ __device__ __forceinline__ void gate_partial(const PrefillArgs &a, int t0, int w
   const int stride = 16 * kGateWaves;
   GateBlock buf[kGateAhead];
 #pragma unroll
-  for (int j = 0; j < kGateAhead; ++j) gate_load<DT>(buf[j], hrow, wbase, ng, (wave + j * kGateWaves) * 16 + 4 * kq, d, E, i);
+  for (int j = 0; j < kGateAhead; ++j) gate_load<DT, FAST>(buf[j], hrow, wbase, ng, (wave + j * kGateWaves) * 16 + 4 * kq, d, E, i);
   for (int k0 = wave * 16; k0 < d; k0 += stride * kGateAhead) {
 #pragma unroll
     for (int j = 0; j < kGateAhead; ++j) {
       const GateBlock cur = buf[j];
-      gate_load<DT>(buf[j], hrow, wbase, ng, k0 + (j + kGateAhead) * stride + 4 * kq, d, E, i);
+      gate_load<DT, FAST>(buf[j], hrow, wbase, ng, k0 + (j + kGateAhead) * stride + 4 * kq, d, E, i);
       gate_mfma<DT>(cur, ng, acc, sq);
     }
   }
@@ -160,10 +180,18 @@ __global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int t0 = blockIdx.x * kGateTok;
   const int E = a.E, d = a.d;
-  if (a.dtype == 1)
-    gate_partial<1>(a, t0, wave, lane, zp, rp);
-  else
-    gate_partial<0>(a, t0, wave, lane, zp, rp);
+  const bool fast = d % (16 * kGateWaves * kGateAhead) == 0;
+  if (a.dtype == 1) {
+    if (fast)
+      gate_partial<1, true>(a, t0, wave, lane, zp, rp);
+    else
+      gate_partial<1, false>(a, t0, wave, lane, zp, rp);
+  } else {
+    if (fast)
+      gate_partial<0, true>(a, t0, wave, lane, zp, rp);
+    else
+      gate_partial<0, false>(a, t0, wave, lane, zp, rp);
+  }
   __syncthreads();
   // zs = zp[0] + zp[1] + zp[2] + zp[3] in that order, kept in zp[0]
   for (int x = tid; x < kGateTok * kMaxE; x += 256) {
@@ -204,12 +232,23 @@ __global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
     }
     const float inv = (float)(1.0 / rr);
     if (lane == 0) a.inv_r[t] = inv;
-    for (int c = lane * 4; c < d; c += kWave * 4) {
-      const float4 v = *reinterpret_cast<const float4 *>(a.H + (size_t)t * d + c);
-      uint2 o;
-      o.x = (uint32_t)f32_to_bf16_rne(v.x * inv) | ((uint32_t)f32_to_bf16_rne(v.y * inv) << 16);
-      o.y = (uint32_t)f32_to_bf16_rne(v.z * inv) | ((uint32_t)f32_to_bf16_rne(v.w * inv) << 16);
-      *reinterpret_cast<uint2 *>(a.xn + (size_t)t * d + c) = o;
+    // the row's loads eight at a time (clamped, so none waits behind a branch)
+    constexpr int kRowAhead = 8;
+    for (int c0 = lane * 4; c0 < d; c0 += kRowAhead * kWave * 4) {
+      float4 v[kRowAhead];
+#pragma unroll
+      for (int u = 0; u < kRowAhead; ++u)
+        v[u] = *reinterpret_cast<const float4 *>(a.H + (size_t)t * d + min(c0 + u * kWave * 4, d - 4));
+#pragma unroll
+      for (int u = 0; u < kRowAhead; ++u) {
+        const int c = c0 + u * kWave * 4;
+        if (c < d) {
+          uint2 o;
+          o.x = (uint32_t)f32_to_bf16_rne(v[u].x * inv) | ((uint32_t)f32_to_bf16_rne(v[u].y * inv) << 16);
+          o.y = (uint32_t)f32_to_bf16_rne(v[u].z * inv) | ((uint32_t)f32_to_bf16_rne(v[u].w * inv) << 16);
+          *reinterpret_cast<uint2 *>(a.xn + (size_t)t * d + c) = o;
+        }
+      }
     }
   }
 }
