@@ -733,10 +733,42 @@ __global__ __launch_bounds__(256) void prefill_unpermute_kernel(float *H, const 
                                                                 const int32_t *pos_of, int T, int d, int K) {
   const int t = blockIdx.x;
   if (t >= T) return;
-  for (int c = threadIdx.x; c < d; c += 256) {
-    float y = 0.0f;
-    for (int r = 0; r < K; ++r) y = fmaf(g[(size_t)t * K + r], Y[(size_t)pos_of[(size_t)t * K + r] * d + c], y);
-    H[(size_t)t * d + c] += y;
+  // four columns per lane per step, the steps' loads issued together (clamped
+  // to the row, so none waits behind a branch); ranks added in order
+  constexpr int kAhead = 4;
+  for (int c0 = threadIdx.x * 4; c0 < d; c0 += kAhead * 256 * 4) {
+    float4 y[kAhead], h[kAhead];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) {
+      y[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      h[u] = *reinterpret_cast<const float4 *>(H + (size_t)t * d + min(c0 + u * 1024, d - 4));
+    }
+    for (int r = 0; r < K; ++r) {
+      const float gr = g[(size_t)t * K + r];
+      const float *yr = Y + (size_t)pos_of[(size_t)t * K + r] * d;
+      float4 v[kAhead];
+#pragma unroll
+      for (int u = 0; u < kAhead; ++u) v[u] = *reinterpret_cast<const float4 *>(yr + min(c0 + u * 1024, d - 4));
+#pragma unroll
+      for (int u = 0; u < kAhead; ++u) {
+        y[u].x = fmaf(gr, v[u].x, y[u].x);
+        y[u].y = fmaf(gr, v[u].y, y[u].y);
+        y[u].z = fmaf(gr, v[u].z, y[u].z);
+        y[u].w = fmaf(gr, v[u].w, y[u].w);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u) {
+      const int c = c0 + u * 1024;
+      if (c < d) {
+        float4 o = h[u];
+        o.x += y[u].x;
+        o.y += y[u].y;
+        o.z += y[u].z;
+        o.w += y[u].w;
+        *reinterpret_cast<float4 *>(H + (size_t)t * d + c) = o;
+      }
+    }
   }
 }
 
