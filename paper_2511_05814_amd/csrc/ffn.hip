@@ -311,7 +311,8 @@ struct DownShape {
 };
 DownShape down_shape(int d_ff, int dtype) {
   const int cols = kWave * (dtype == 1 ? 8 : 4);
-  if (d_ff <= 4 * cols) return {4, 2};
+  // narrow experts: one chunk per rank, as few padding columns as possible
+  if (d_ff <= 4 * cols) return {(d_ff + cols - 1) / cols, 2};
   return {2, 2};
 }
 
@@ -359,10 +360,12 @@ hipError_t launch_down_t(const FfnArgs &a, const Launch &l) {
   const int rows = kWavesPerBlock * sh.rows;
   const int ch = sh.steps * kWave * Elem<DT>::kVec;
   const dim3 grid(((a.d + rows - 1) / rows) * ffn_down_chunks(a.K, a.d_ff, DT));
-  if (sh.steps == 4)
-    launch_down_shape<DT, 4, 2>(grid, a.d_ff % ch != 0, a, l);
-  else
-    launch_down_shape<DT, 2, 2>(grid, a.d_ff % ch != 0, a, l);
+  switch (sh.steps) {
+    case 1: launch_down_shape<DT, 1, 2>(grid, a.d_ff % ch != 0, a, l); break;
+    case 2: launch_down_shape<DT, 2, 2>(grid, a.d_ff % ch != 0, a, l); break;
+    case 3: launch_down_shape<DT, 3, 2>(grid, a.d_ff % ch != 0, a, l); break;
+    default: launch_down_shape<DT, 4, 2>(grid, a.d_ff % ch != 0, a, l); break;
+  }
   return hipGetLastError();
 }
 
