@@ -177,6 +177,7 @@ __global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
   __shared__ double zp[kGateWaves][kGateTok][kMaxE];
   __shared__ double rp[kGateWaves][kGateTok];
   __shared__ int s_top[kGateWaves][kMaxK];
+  __shared__ float s_inv[kGateTok];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int t0 = blockIdx.x * kGateTok;
   const int E = a.E, d = a.d;
@@ -231,23 +232,36 @@ __global__ __launch_bounds__(256) void prefill_gate_kernel(PrefillArgs a) {
       a.g[(size_t)t * a.K + lane] = (float)(ex / den);
     }
     const float inv = (float)(1.0 / rr);
-    if (lane == 0) a.inv_r[t] = inv;
-    // the row's loads eight at a time (clamped, so none waits behind a branch)
-    constexpr int kRowAhead = 8;
-    for (int c0 = lane * 4; c0 < d; c0 += kRowAhead * kWave * 4) {
-      float4 v[kRowAhead];
+    if (lane == 0) {
+      a.inv_r[t] = inv;
+      s_inv[r] = inv;
+    }
+  }
+  __syncthreads();
+  // normalised bf16 rows of all the workgroup's tokens, every thread taking
+  // part, eight loads in flight (clamped, so none waits behind a branch)
+  constexpr int kRowAhead = 8;
+  const int nt = min(kGateTok, a.T - t0);
+  const int q4 = d / 4;  // float4 per row
+  const int total = nt * q4;
+  for (int i0 = tid; i0 < total; i0 += kRowAhead * 256) {
+    float4 v[kRowAhead];
 #pragma unroll
-      for (int u = 0; u < kRowAhead; ++u)
-        v[u] = *reinterpret_cast<const float4 *>(a.H + (size_t)t * d + min(c0 + u * kWave * 4, d - 4));
+    for (int u = 0; u < kRowAhead; ++u) {
+      const int i = min(i0 + u * 256, total - 1);
+      const int r = i / q4, c = (i - r * q4) * 4;
+      v[u] = *reinterpret_cast<const float4 *>(a.H + (size_t)(t0 + r) * d + c);
+    }
 #pragma unroll
-      for (int u = 0; u < kRowAhead; ++u) {
-        const int c = c0 + u * kWave * 4;
-        if (c < d) {
-          uint2 o;
-          o.x = (uint32_t)f32_to_bf16_rne(v[u].x * inv) | ((uint32_t)f32_to_bf16_rne(v[u].y * inv) << 16);
-          o.y = (uint32_t)f32_to_bf16_rne(v[u].z * inv) | ((uint32_t)f32_to_bf16_rne(v[u].w * inv) << 16);
-          *reinterpret_cast<uint2 *>(a.xn + (size_t)t * d + c) = o;
-        }
+    for (int u = 0; u < kRowAhead; ++u) {
+      const int i = i0 + u * 256;
+      if (i < total) {
+        const int r = i / q4, c = (i - r * q4) * 4;
+        const float inv = s_inv[r];
+        uint2 o;
+        o.x = (uint32_t)f32_to_bf16_rne(v[u].x * inv) | ((uint32_t)f32_to_bf16_rne(v[u].y * inv) << 16);
+        o.y = (uint32_t)f32_to_bf16_rne(v[u].z * inv) | ((uint32_t)f32_to_bf16_rne(v[u].w * inv) << 16);
+        *reinterpret_cast<uint2 *>(a.xn + (size_t)(t0 + r) * d + c) = o;
       }
     }
   }
