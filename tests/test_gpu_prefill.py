@@ -98,6 +98,20 @@ def test_prefill_ragged_shapes():
     rig.store.close()
 
 
+@pytest.mark.parametrize("T", [5, 64])
+def test_small_prefill_fine_grained(T):
+    # small prefills at the 64-expert shape (d = 2048): a partial and a full
+    # gate tile; 16 of 64 slots, so the batch is planned on the host and
+    # streams experts
+    cfg = wl.CONFIGS["fine-grained"].with_(layers=2, tokens=4, prefill_tokens=64)
+    _say("small prefill, 64-expert shape", T)
+    rig = Rig(cfg)
+    moe = rig.cache(16, "lfu", max_prefill_tokens=64)
+    prefill_and_check(rig, moe, "lfu", 16, T, list(range(0, T, 3)))
+    moe.close()
+    rig.store.close()
+
+
 @pytest.mark.parametrize("T", [1, 13, 32])
 def test_device_planned_batches(T):
     # a slot for every expert and at most 32 tokens: the plan kernel writes the
