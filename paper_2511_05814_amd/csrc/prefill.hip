@@ -478,10 +478,33 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row
 // loaded from global memory into registers kGemmStages slices ahead of the
 // one multiplied out of LDS; LDS is double-buffered so one barrier per step
 // suffices.  Every output accumulates its K slices in ascending order.
+//
+// The loads ahead must stay in flight across steps, so none of them is
+// conditional: a row past the group's end or a column past N reads the last
+// valid row instead (its outputs are not written), and a K tail (K not a
+// multiple of 32; RAGGED) reads the row's last 8 elements and is zeroed when
+// stored to LDS, where the wait for it happens anyway.  Loads under a branch
+// leave the compiler unable to count what is outstanding, and it then waits
+// for every load at each step.  The weight pointers come from the job table,
+// which the compiler can only address with flat loads; those also count
+// against the LDS counter, so the wait before each barrier would drain them.
+// The weights are read with buffer loads instead, through a resource over the
+// tile's own rows (uniform base, 32-bit byte offsets, and a record count that
+// bounds every access to those rows).
 constexpr int kBN = 128;
 constexpr int kGemmStages = 2;  // K slices loaded ahead of the one being multiplied
 
-template <bool UP, int P, int BM>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint16_t *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), 0, bytes, 0x00020000);
+}
+
+typedef uint32_t gemm_u32x4 __attribute__((ext_vector_type(4)));  // a 16-byte slice as a register value
+
+__device__ __forceinline__ gemm_u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(gemm_u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+
+template <bool UP, int P, int BM, bool RAGGED>
 __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_gemm_kernel(
     const GemmTile *tiles, const GemmJob *jobs, const uint16_t *a_src, const int32_t *perm_tok, void *out, int d,
     int d_ff) {
@@ -499,47 +522,48 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
   const int ldo = N;
   // staging: thread -> rows (tid / 4) + 64 h, 16-byte quarter tid % 4
   const int r0 = tid / 4, q = tid % 4;
+  if (j.nrows <= 0) return;  // no rows: nothing to clamp to (the plan makes no such tiles)
   const uint16_t *ap[HA];
-  const uint16_t *bp[NB][2];
 #pragma unroll
   for (int h = 0; h < HA; ++h) {
-    const int m = t.m0 + r0 + 64 * h;
-    ap[h] = m < j.nrows ? (UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff)
-                        : nullptr;
+    const int m = min(t.m0 + r0 + 64 * h, j.nrows - 1);
+    ap[h] = UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff;
   }
+  // weight rows n0 .. n0 + nb - 1 of each B matrix (nb <= 128)
+  const int nb = min(kBN, N - t.n0);
+  __amdgpu_buffer_rsrc_t brs[NB];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int n = t.n0 + r0 + 64 * h;
+  for (int b = 0; b < NB; ++b)
+    brs[b] = rows_rsrc(j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)t.n0 * K,
+                       (uint32_t)nb * K * 2);
+  uint32_t boff[2];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const uint16_t *w = j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d);
-      bp[b][h] = n < N ? w + (size_t)n * K : nullptr;
-    }
-  }
+  for (int h = 0; h < 2; ++h) boff[h] = (uint32_t)min(r0 + 64 * h, nb - 1) * K * 2;
   // K slices loaded ahead live in a ring of P register slots: slice t >= 1
   // sits in slot (t - 1) % P until it is stored to LDS.
-  uint4 ra[P][HA], rb[P][NB][2];
+  gemm_u32x4 ra[P][HA], rb[P][NB][2];
   auto gload = [&](int slot, int k0) {
-    const int k = k0 + q * 8;
+    const int k = RAGGED ? min(k0 + q * 8, K - 8) : k0 + q * 8;  // K is a multiple of 8
 #pragma unroll
-    for (int h = 0; h < HA; ++h)
-      ra[slot][h] = (ap[h] && k < K) ? *reinterpret_cast<const uint4 *>(ap[h] + k) : make_uint4(0, 0, 0, 0);
+    for (int h = 0; h < HA; ++h) ra[slot][h] = *reinterpret_cast<const gemm_u32x4 *>(ap[h] + k);
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
-        rb[slot][b][h] = (bp[b][h] && k < K) ? *reinterpret_cast<const uint4 *>(bp[b][h] + k)
-                                             : make_uint4(0, 0, 0, 0);
+      for (int b = 0; b < NB; ++b) rb[slot][b][h] = buffer_load16(brs[b], boff[h] + 2 * k);
   };
-  auto lstore = [&](int slot, int buf) {
+  auto lstore = [&](int slot, int buf, int k0) {
+    const bool tail = RAGGED && k0 + q * 8 >= K;
+    const gemm_u32x4 zero = {0, 0, 0, 0};
 #pragma unroll
     for (int h = 0; h < HA; ++h)
-      *reinterpret_cast<uint4 *>(&As[buf][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) = ra[slot][h];
+      *reinterpret_cast<gemm_u32x4 *>(&As[buf][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) =
+          tail ? zero : ra[slot][h];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
       for (int b = 0; b < NB; ++b)
-        *reinterpret_cast<uint4 *>(&Bs[buf][b][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) = rb[slot][b][h];
+        *reinterpret_cast<gemm_u32x4 *>(&Bs[buf][b][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) =
+            tail ? zero : rb[slot][b][h];
   };
   floatx4 c[NB][MX][4];
 #pragma unroll
@@ -551,39 +575,50 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
 #pragma unroll
         for (int i = 0; i < 4; ++i) c[b][x][y][i] = 0.0f;
 
+  // The main loop is straight-line (every step stores a slice and loads one,
+  // clamped to the last slice past the end, whose data is then never used), so
+  // the compiler can keep the loads of the other ring slots in flight; the
+  // last steps, which load nothing, are peeled off.
+  auto mma = [&](int buf) {
+    bf16x8 af[MX];
+#pragma unroll
+    for (int x = 0; x < MX; ++x) af[x] = lds_frag(As[buf], wm * (BM / 2) + x * 16 + lane % 16, lane);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      bf16x8 bf[4];
+#pragma unroll
+      for (int y = 0; y < 4; ++y) bf[y] = lds_frag(Bs[buf][b], wn * 64 + y * 16 + lane % 16, lane);
+#pragma unroll
+      for (int x = 0; x < MX; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y)
+          c[b][x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
+    }
+  };
   const int nk = (K + kKStep - 1) / kKStep;
   gload(0, 0);
-  lstore(0, 0);
+  lstore(0, 0, 0);
 #pragma unroll
-  for (int t = 1; t <= P; ++t)
-    if (t < nk) gload(t - 1, t * kKStep);
+  for (int t = 1; t <= P; ++t) gload(t - 1, min(t, nk - 1) * kKStep);
   __syncthreads();
-  for (int i = 0; i < nk; i += P) {
+  int i = 0;
+  for (; i + P < nk; i += P) {  // steps i .. i + P - 1, each followed by another
 #pragma unroll
     for (int u = 0; u < P; ++u) {
       const int s = i + u;  // slice multiplied now, out of LDS buffer s & 1
-      if (s < nk) {
-        const int buf = s & 1;
-        bf16x8 af[MX];
+      mma(s & 1);
+      lstore(u, (s & 1) ^ 1, (s + 1) * kKStep);            // slice s + 1 lives in slot s % P = u
+      gload(u, min(s + 1 + P, nk - 1) * kKStep);           // slot u is free again
+      __syncthreads();
+    }
+  }
 #pragma unroll
-        for (int x = 0; x < MX; ++x) af[x] = lds_frag(As[buf], wm * (BM / 2) + x * 16 + lane % 16, lane);
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          bf16x8 bf[4];
-#pragma unroll
-          for (int y = 0; y < 4; ++y) bf[y] = lds_frag(Bs[buf][b], wn * 64 + y * 16 + lane % 16, lane);
-#pragma unroll
-          for (int x = 0; x < MX; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y)
-              c[b][x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
-        }
-        if (s + 1 < nk) {
-          lstore(u, buf ^ 1);                                // slice s + 1 lives in slot s % P = u
-          if (s + 1 + P < nk) gload(u, (s + 1 + P) * kKStep);  // slot u is free again
-        }
-        __syncthreads();
-      }
+  for (int u = 0; u < P; ++u) {  // the last nk - i <= P steps; their slices are all loaded
+    const int s = i + u;
+    if (s < nk) {
+      mma(s & 1);
+      if (s + 1 < nk) lstore(u, (s & 1) ^ 1, (s + 1) * kKStep);
+      __syncthreads();
     }
   }
 #pragma unroll
@@ -803,12 +838,16 @@ hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l) {
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  if (rows == 64)
-    MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, 64>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn,
-               perm_tok, (void *)act, d, d_ff);
-  else
-    MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, 128>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn,
-               perm_tok, (void *)act, d, d_ff);
+#define MOE_GEMM_UP(BM, RG)                                                                                  \
+  MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, BM, RG>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, \
+             perm_tok, (void *)act, d, d_ff)
+  const bool ragged = d % kKStep != 0;
+  if (rows == 64) {
+    if (ragged) MOE_GEMM_UP(64, true); else MOE_GEMM_UP(64, false);
+  } else {
+    if (ragged) MOE_GEMM_UP(128, true); else MOE_GEMM_UP(128, false);
+  }
+#undef MOE_GEMM_UP
   return hipGetLastError();
 }
 
@@ -831,12 +870,16 @@ hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const G
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
                                float *Y, int d, int d_ff, int rows, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  if (rows == 64)
-    MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, 64>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
-               (const int32_t *)nullptr, (void *)Y, d, d_ff);
-  else
-    MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, 128>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act,
-               (const int32_t *)nullptr, (void *)Y, d, d_ff);
+#define MOE_GEMM_DOWN(BM, RG)                                                                                 \
+  MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, BM, RG>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act, \
+             (const int32_t *)nullptr, (void *)Y, d, d_ff)
+  const bool ragged = d_ff % kKStep != 0;
+  if (rows == 64) {
+    if (ragged) MOE_GEMM_DOWN(64, true); else MOE_GEMM_DOWN(64, false);
+  } else {
+    if (ragged) MOE_GEMM_DOWN(128, true); else MOE_GEMM_DOWN(128, false);
+  }
+#undef MOE_GEMM_DOWN
   return hipGetLastError();
 }
 
