@@ -197,12 +197,14 @@ hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l);
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l);
 // Small-M grouped GEMMs: one tile {job, 0, 0} per expert, each with at most
-// kSkinnyRows rows; a workgroup per (tile, 16 output features).
+// max_rows <= kSkinnyRows rows (the caller's bound: rows beyond 16 are read
+// only when max_rows > 16); a workgroup per (tile, 16 output features).
 constexpr int kSkinnyRows = 32;
 hipError_t launch_prefill_skinny_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                                    const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l);
+                                    const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int max_rows,
+                                    const Launch &l);
 hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                                      float *Y, int d, int d_ff, const Launch &l);
+                                      float *Y, int d, int d_ff, int max_rows, const Launch &l);
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
                                float *Y, int d, int d_ff, int rows, const Launch &l);
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,

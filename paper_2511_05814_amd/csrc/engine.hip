@@ -829,10 +829,10 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     const double rows = (double)T * c->K;
     Launch lu, ld;
     HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_GEMM_UP));
-    HIP_TRY(c, launch_prefill_skinny_up(tiles, c->E, jobs, xn, perm, act, c->d, c->dff, lu));
+    HIP_TRY(c, launch_prefill_skinny_up(tiles, c->E, jobs, xn, perm, act, c->d, c->dff, T, lu));
     kernel_span_done(c, SPAN_GEMM_UP, lu, rows * 4.0 * c->d * c->dff);
     HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
-    HIP_TRY(c, launch_prefill_skinny_down(tiles, c->E, jobs, act, Y, c->d, c->dff, ld));
+    HIP_TRY(c, launch_prefill_skinny_down(tiles, c->E, jobs, act, Y, c->d, c->dff, T, ld));
     kernel_span_done(c, SPAN_GEMM_DOWN, ld, rows * 2.0 * c->d * c->dff);
     HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, Launch{c->cs}));
     HIP_TRY(c, span_end(c, c->cs, SPAN_PREFILL, tp));
@@ -938,7 +938,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       group_rows[gi] += pl[e].n;
     }
     if (most <= kSkinnyRows) {
-      skinny[gi] = 1;
+      skinny[gi] = std::max(most, 1);  // the group's largest row count
       up_first[gi] = dn_first[gi] = nt;
       for (int e : group) {
         if (nt >= p.tile_cap) {
@@ -1021,13 +1021,14 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     Launch lu, ld;
     HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_GEMM_UP));
     if (skinny[gi])
-      HIP_TRY(c, launch_prefill_skinny_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, lu));
+      HIP_TRY(c, launch_prefill_skinny_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff,
+                                            skinny[gi], lu));
     else
       HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, up_rows[gi], lu));
     kernel_span_done(c, SPAN_GEMM_UP, lu, group_rows[gi] * up_flop_per_row);
     HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
     if (skinny[gi])
-      HIP_TRY(c, launch_prefill_skinny_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, ld));
+      HIP_TRY(c, launch_prefill_skinny_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, skinny[gi], ld));
     else
       HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, dn_rows[gi], ld));
     kernel_span_done(c, SPAN_GEMM_DOWN, ld, group_rows[gi] * down_flop_per_row);

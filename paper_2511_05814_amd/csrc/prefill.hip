@@ -655,13 +655,14 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
 constexpr int kSkinnyAheadUp = 8, kSkinnyAheadDown = 8;  // steps in flight per wave
 
 __device__ __forceinline__ bf16x8 load_frag(const uint16_t *p) {
-  const uint4 v = *reinterpret_cast<const uint4 *>(p);
-  bf16x8 r;
-  __builtin_memcpy(&r, &v, sizeof v);
-  return r;
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const gemm_u32x4 *>(p));
 }
 
-template <bool UP, int AHEAD>
+__device__ __forceinline__ bf16x8 load_frag(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(bf16x8, buffer_load16(r, byte_off));
+}
+
+template <bool UP, int AHEAD, bool TWO>
 __global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *tiles, const GemmJob *jobs,
                                                              const uint16_t *a_src, const int32_t *perm_tok,
                                                              void *out, int d, int d_ff) {
@@ -675,7 +676,7 @@ __global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *til
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int M = min(j.nrows, kSkinnyRows);
   if (M <= 0) return;       // the host makes tiles only for experts with rows
-  const bool two = M > 16;  // second 16-row block
+  const bool two = TWO && M > 16;  // second 16-row block (TWO: the launch may have groups of 17-32 rows)
   const int kg = (lane / 16) * 8;  // this lane's 8 elements of a 32-deep step
   // A rows (tokens of the expert) and B rows (features) of this lane, clamped
   const uint16_t *ap[2];
@@ -684,11 +685,16 @@ __global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *til
     const int m = min(tb * 16 + lane % 16, M - 1);
     ap[tb] = (UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff) + kg;
   }
-  const int f = min(fb * 16 + lane % 16, N - 1);
-  const uint16_t *bp[NB];
+  // B rows: features fb * 16 .. + nf - 1 of each weight matrix, read with
+  // buffer loads (the pointer comes from the job table; flat loads would make
+  // every wait drain all the loads in flight)
+  const int nf = min(16, N - fb * 16);
+  __amdgpu_buffer_rsrc_t brs[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b)
-    bp[b] = j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)f * K + kg;
+    brs[b] = rows_rsrc(j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)fb * 16 * K,
+                       (uint32_t)nf * K * 2);
+  const uint32_t boff = ((uint32_t)min(lane % 16, nf - 1) * K + kg) * 2;
 
   floatx4 c[NB][2];
 #pragma unroll
@@ -702,12 +708,15 @@ __global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *til
   const int s0 = min(wave * q, full), s1 = min(s0 + q, full);
   const int n = s1 - s0;
   bf16x8 wa[AHEAD][NB], xa[AHEAD][2];
+  // no load is conditional (in a launch with groups of more than 16 rows,
+  // the second row block reads clamped rows where a group has fewer), so the
+  // compiler can count the loads in flight
   auto load = [&](int slot, int step) {
     const int k = step * 32;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) wa[slot][b] = load_frag(bp[b] + k);
+    for (int b = 0; b < NB; ++b) wa[slot][b] = load_frag(brs[b], boff + 2 * k);
     xa[slot][0] = load_frag(ap[0] + k);
-    if (two) xa[slot][1] = load_frag(ap[1] + k);
+    if (TWO) xa[slot][1] = load_frag(ap[1] + k);
   };
   auto mma = [&](int slot) {
 #pragma unroll
@@ -716,17 +725,23 @@ __global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *til
       if (two) c[b][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[slot][1], wa[slot][b], c[b][1], 0, 0, 0);
     }
   };
+  // straight-line main loop: a step past the wave's last reloads that step
+  // (in bounds, never used); the last steps, which load nothing, are peeled
+  if (n > 0) {
 #pragma unroll
-  for (int u = 0; u < AHEAD; ++u)
-    if (u < n) load(u, s0 + u);
-  for (int i = 0; i < n; i += AHEAD) {
+    for (int u = 0; u < AHEAD; ++u) load(u, s0 + min(u, n - 1));
+    int i = 0;
+    for (; i + AHEAD < n; i += AHEAD) {
 #pragma unroll
-    for (int u = 0; u < AHEAD; ++u) {
-      if (i + u < n) {
+      for (int u = 0; u < AHEAD; ++u) {
         mma(u);
-        if (i + u + AHEAD < n) load(u, s0 + i + u + AHEAD);
+        load(u, s0 + min(i + u + AHEAD, n - 1));
+        __builtin_amdgcn_sched_barrier(0);  // keep each refill next to its step, not batched at the end
       }
     }
+#pragma unroll
+    for (int u = 0; u < AHEAD; ++u)
+      if (i + u < n) mma(u);
   }
   // K tail (K not a multiple of 32): the last wave adds it, zeroing past K
   if (K % 32 && wave == 3) {
@@ -735,12 +750,15 @@ __global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *til
     const bf16x8 z = {};
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const bf16x8 v = load_frag(bp[b] + k);
+      const bf16x8 v = load_frag(brs[b], boff + 2 * k);
       wa[0][b] = in ? v : z;
     }
-    const bf16x8 x0 = load_frag(ap[0] + k), x1 = load_frag(ap[1] + k);
+    const bf16x8 x0 = load_frag(ap[0] + k);
     xa[0][0] = in ? x0 : z;
-    xa[0][1] = in ? x1 : z;
+    if (TWO) {
+      const bf16x8 x1 = load_frag(ap[1] + k);
+      xa[0][1] = in ? x1 : z;
+    }
     mma(0);
   }
 #pragma unroll
@@ -852,18 +870,29 @@ hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *j
 }
 
 hipError_t launch_prefill_skinny_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                                    const int32_t *perm_tok, uint16_t *act, int d, int d_ff, const Launch &l) {
+                                    const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int max_rows,
+                                    const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH((prefill_skinny_kernel<true, kSkinnyAheadUp>), dim3(ntiles * ((d_ff + 15) / 16)), dim3(256), 0, l, tiles, jobs, xn,
-             perm_tok, (void *)act, d, d_ff);
+  if (max_rows < 1 || max_rows > kSkinnyRows) return hipErrorInvalidValue;
+  if (max_rows > 16)
+    MOE_LAUNCH((prefill_skinny_kernel<true, kSkinnyAheadUp, true>), dim3(ntiles * ((d_ff + 15) / 16)), dim3(256), 0, l,
+               tiles, jobs, xn, perm_tok, (void *)act, d, d_ff);
+  else
+    MOE_LAUNCH((prefill_skinny_kernel<true, kSkinnyAheadUp, false>), dim3(ntiles * ((d_ff + 15) / 16)), dim3(256), 0, l,
+               tiles, jobs, xn, perm_tok, (void *)act, d, d_ff);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                                      float *Y, int d, int d_ff, const Launch &l) {
+                                      float *Y, int d, int d_ff, int max_rows, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-  MOE_LAUNCH((prefill_skinny_kernel<false, kSkinnyAheadDown>), dim3(ntiles * ((d + 15) / 16)), dim3(256), 0, l, tiles, jobs, act,
-             nullptr, (void *)Y, d, d_ff);
+  if (max_rows < 1 || max_rows > kSkinnyRows) return hipErrorInvalidValue;
+  if (max_rows > 16)
+    MOE_LAUNCH((prefill_skinny_kernel<false, kSkinnyAheadDown, true>), dim3(ntiles * ((d + 15) / 16)), dim3(256), 0, l,
+               tiles, jobs, act, nullptr, (void *)Y, d, d_ff);
+  else
+    MOE_LAUNCH((prefill_skinny_kernel<false, kSkinnyAheadDown, false>), dim3(ntiles * ((d + 15) / 16)), dim3(256), 0, l,
+               tiles, jobs, act, nullptr, (void *)Y, d, d_ff);
   return hipGetLastError();
 }
 
