@@ -1,26 +1,28 @@
 """Benchmark: batch-1 MoE decode under expert offloading on one MI355X.
 
-Default workload (one step): 256 batch-1 decode tokens through one
-Mixtral-8x7B-shaped MoE layer (8 experts, top-2, d=4096, d_ff=14336, bf16
-experts in pinned host memory), 4 HBM expert slots, LFU eviction; seeded
-synthetic hidden states with Zipf(1.1) concept skew and Markov(0.6)
-persistence.  Each step starts from the same warm cache (experts 0..S-1
-resident); the warm start and the restore of the input hidden states are
-outside the timed region.
+Default workload: the 32-layer Mixtral-8x7B-shaped stack (8 experts per
+layer, top-2, d=4096, d_ff=14336, bf16 experts in pinned host memory), 4 HBM
+expert slots per layer, LFU eviction (Table 2's setting), all 512 batch-1
+decode tokens of the seeded synthetic stream (Zipf(1.1) concept skew,
+Markov(0.6) persistence) from the warm start.  A step decodes the next chunk
+of consecutive tokens through all 32 layers; the cache carries over between
+steps, so the K timed steps together are one pass over the 512 tokens.  The
+W warm-up steps are a separate pass over the first W chunks, after which the
+cache is reset to the warm start.
 
-`--workload` selects one of the other configurations instead (32-layer
-Mixtral-shaped stack with 2/4/6 slots, the same stack with next-layer
-prefetch, the 64-expert stack with a 4096-token prefill); those print the
-same JSON schema.
+Beside the headline the JSON line carries: comparison runs on stated token
+prefixes (LRU at 4 slots, 2 and 6 slots under both policies, next-layer
+prefetch of 2) and the one-layer Mixtral workload under LFU and LRU; hit
+rates with Belady's MIN; trace analytics (per-layer hit rates, the paper's
+per-layer activation histograms, repeat rates against random routing); the
+decode FFN up kernel's HBM roofline (HIP events stamped by its dispatches in
+the timed pass); the fetch kernel's host-link roofline against the best of a
+DMA copy and a shader copy measured here; a streaming HBM read probe and a
+bf16 MFMA probe; and the fp64 oracle timed on a bounded sample on the host
+cores.
 
-Prints one JSON line: decode tokens/s (LFU) and, alongside, LRU tokens/s,
-hit rates, cache and speculation precision/recall, the decode FFN up
-kernel's HBM roofline (HIP events stamped by its dispatches inside the timed
-region; the other kernels' durations, the copy/compute overlap and the
-prefill GEMM rates come from one more pass of the same work with every launch
-timed, since events on every launch cost GPU time), the fetch kernel's
-host-link roofline against the H2D rate measured here, a streaming HBM read
-probe, and the fp64 oracle timed on a bounded sample on the host cores.
+`--workload` selects another configuration (the one-layer workloads and the
+64-expert stack keep one pass over their tokens per step).
 """
 from __future__ import annotations
 
@@ -67,20 +69,41 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def measure_link(torch, nbytes=1 << 30, reps=3):
-    """Best pinned host -> HBM copy rate (GB/s) on a 1 GiB transfer."""
+def measure_link(torch, b, nbytes=1 << 30, reps=3):
+    """Host-to-device link ceiling: the best of a 1 GiB pinned-to-HBM copy by
+    the DMA engines (hipMemcpyAsync) and by the library's shader-copy probe
+    (the fetch kernel's access pattern) at 64, 128 and 256 workgroups, over the
+    same pinned buffer.  Returns {"best", "best_is", "sdma", "shader"} (GB/s)."""
     src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
     dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-    best = 0.0
+    sdma = 0.0
     for _ in range(reps):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         dst.copy_(src, non_blocking=True)
-        b.record()
-        b.synchronize()
-        best = max(best, nbytes / (a.elapsed_time(b) * 1e-3) / 1e9)
+        e.record()
+        e.synchronize()
+        sdma = max(sdma, nbytes / (a.elapsed_time(e) * 1e-3) / 1e9)
+    stream = torch.cuda.current_stream().cuda_stream
+    shader = {wg: b.moe_probe_h2d_copy(src.data_ptr(), dst.data_ptr(), nbytes, wg, reps, stream)
+              for wg in (64, 128, 256)}
+    torch.cuda.synchronize()
     del src, dst
-    return best
+    best_wg = max(shader, key=shader.get)
+    if shader[best_wg] > sdma:
+        best, best_is = shader[best_wg], f"shader copy probe, {best_wg} workgroups, 1 GiB pinned -> HBM"
+    else:
+        best, best_is = sdma, "DMA copy (hipMemcpyAsync), 1 GiB pinned -> HBM"
+    return {"best": best, "best_is": best_is, "sdma": round(sdma, 2),
+            "shader": {str(k): round(v, 2) for k, v in shader.items()}}
+
+
+def measure_mfma(torch, b):
+    """bf16 matrix-core ceiling (TFLOP/s) of a register-only MFMA loop, for
+    both bf16 instruction shapes."""
+    stream = torch.cuda.current_stream().cuda_stream
+    return {"v_mfma_f32_16x16x32_bf16": round(b.moe_probe_mfma_bf16(0, 4096, stream), 1),
+            "v_mfma_f32_32x32x16_bf16": round(b.moe_probe_mfma_bf16(1, 2048, stream), 1)}
 
 
 def measure_hbm_read(torch, b, nbytes=1 << 30, reps=20):
@@ -272,42 +295,313 @@ def batch_report(args, cfg, results, link):
     }
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="mixtral-layer", choices=sorted(DESCRIPTIONS))
-    ap.add_argument("--cpu-tokens", type=int, default=0,
-                    help="most decode tokens the fp64 oracle is timed on (0: the whole workload)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="time budget of the fp64 oracle baseline")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--fetch", choices=["split", "kernel", "dma"], default="split",
-                    help="split: demand misses by the copy kernel, speculative prefetches by the DMA engines")
-    ap.add_argument("--tokens", type=int, default=0,
-                    help="decode only the first N tokens of the workload (profiling passes)")
-    ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
-    ap.add_argument("--layers", type=int, default=0, help="run only the first N layers of the workload")
-    ap.add_argument("--prefill-tokens", type=int, default=-1,
-                    help="prefill at most this many tokens (0: decode only)")
-    ap.add_argument("--slots", type=int, default=0,
-                    help="HBM slots per layer (default 4, 16 for the 64-expert workload; "
-                         "slots = experts keeps every expert resident)")
-    ap.add_argument("--host-store", choices=["plain", "packed", "entropy"], default="plain",
-                    help="packed / entropy: bf16 experts coded losslessly in host memory (~12.25 / ~10.9 bits a "
-                         "weight) and rebuilt on the GPU after each copy")
-    ap.add_argument("--prefetch-max", type=int, default=-1,
-                    help="override the workload's cap on next-layer experts prefetched per layer (0 turns "
-                         "speculation off)")
-    ap.add_argument("--batch", type=int, default=1,
-                    help="decode B tokens per step through the batch path (bf16 experts; no speculation)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the decode path runs on a single GPU with no collectives)", file=sys.stderr)
-        sys.exit(2)
+# Stack workloads: the metric's own unit, tokens/s through a whole MoE stack.
+STACK_WORKLOADS = ("mixtral-stack", "mixtral-stack-prefetch", "mixtral-stack-q2")
+# comparison runs of the 32-layer stack: (policy, slots, speculate, token prefix)
+STACK_COMPARISONS = {
+    "mixtral-stack": [("lru", 4, False, 128), ("lfu", 2, False, 48), ("lru", 2, False, 48),
+                      ("lfu", 6, False, 96), ("lru", 6, False, 96), ("lfu", 4, True, 64)],
+    "mixtral-stack-prefetch": [("lfu", 4, False, 64)],
+    "mixtral-stack-q2": [("lfu", 4, False, 64)],
+}
 
+
+def run_chunks(torch, b, moe, H0, H, steps, chunk, tokens, timing, flags=0):
+    """One pass over the first `tokens` decode tokens from the warm start, in
+    `steps` steps of `chunk` consecutive tokens (the last may be shorter), each
+    through every layer; the cache carries over from step to step.  The
+    region from the first step's start to the last step's end is timed with
+    the device drained at both ends."""
+    b.moe_cache_set_timing(moe.handle, timing)
+    moe.reset()
+    H.copy_(H0)
+    torch.cuda.synchronize()
+    if timing:
+        b.moe_cache_read_timing(moe.handle)  # drop spans of the reset
+    step_s = []
+    t_start = time.perf_counter()
+    for i in range(steps):
+        a, z = i * chunk, min(tokens, (i + 1) * chunk)
+        if a >= z:
+            break
+        t0 = time.perf_counter()
+        moe.decode(H[a:z], flags=flags)
+        moe.sync()
+        torch.cuda.synchronize()
+        step_s.append(time.perf_counter() - t0)
+    total = time.perf_counter() - t_start
+    tim = b.moe_cache_read_timing(moe.handle) if timing else None
+    b.moe_cache_set_timing(moe.handle, b.MOE_TIMING_OFF)
+    recs, dropped = moe.trace_records()
+    if dropped:
+        raise RuntimeError(f"trace ring overflowed ({dropped} records lost)")
+    return {"total": total, "step_s": step_s, "tim": tim, "stats": moe.stats(), "recs": recs,
+            "tokens": tokens}
+
+
+def pass_summary(cfg, r, slots, flags):
+    """Tokens/s, hit rate, cache and guess precision/recall of one pass."""
+    from paper_2511_05814_amd import analysis
+    acc = [x for x in r["recs"] if x[0] != 2]
+    out = {"tokens": r["tokens"],
+           "tokens_per_s": round(r["tokens"] / r["total"], 3),
+           "hit_rate": round(analysis.hit_rate(acc), 4),
+           "cache_precision_recall": [round(v, 4) for v in analysis.cache_precision_recall(acc, slots)],
+           "bytes_fetched": sum(s["bytes_fetched"] for s in r["stats"])}
+    if flags:
+        p, rc = analysis.guess_precision_recall(acc)
+        out["guess_precision_recall"] = [round(p, 4), round(rc, 4)]
+        out["transfer_precision"] = round(analysis.transfer_precision(acc), 4)
+    else:
+        out["belady_min_hit_rate"] = round(analysis.belady_hit_rate(acc, slots), 4)
+    return out
+
+
+def layer_comparison(torch, b, offload, wl, fetch_mode):
+    """The one-layer Mixtral-shaped workload (its own seed, 256 tokens, 4
+    slots) under LFU and LRU: one pass each from the warm start."""
+    cfg = wl.CONFIGS["mixtral-layer"]
+    store = offload.HostStore(cfg)
+    gates = offload.DeviceGates(cfg)
+    H0 = torch.from_numpy(wl.hidden_states(cfg)).to("cuda")
+    H = torch.empty_like(H0)
+    out = {"workload": DESCRIPTIONS["mixtral-layer"]}
+    try:
+        for policy in ("lfu", "lru"):
+            moe = offload.OffloadedMoE(cfg, store, gates, 4, policy, fetch_mode=fetch_mode)
+            run_chunks(torch, b, moe, H0, H, 1, cfg.tokens, cfg.tokens, b.MOE_TIMING_OFF)  # warm-up pass
+            r = run_chunks(torch, b, moe, H0, H, 1, cfg.tokens, cfg.tokens, b.MOE_TIMING_OFF)
+            moe.close()
+            out[f"{policy}-s4"] = pass_summary(cfg, r, 4, 0)
+            log("mixtral-layer", policy, 4, f"{out[f'{policy}-s4']['tokens_per_s']:.2f} tok/s")
+    finally:
+        store.close()
+    return out
+
+
+def stack_main(args):
+    """The metric's headline: batch-1 decode tokens/s through the whole
+    32-layer stack at a fixed number of slots per layer (Table 2's setting:
+    4 slots, Sec. 5.3), over every token of the workload from the warm start.
+    Each step decodes the next chunk of consecutive tokens through all layers
+    and the cache carries over between steps."""
+    import math
+
+    import torch
+
+    from paper_2511_05814_amd import analysis
+    from paper_2511_05814_amd import binding as b
+    from paper_2511_05814_amd import offload, workload as wl
+
+    cfg = wl.CONFIGS[args.workload]
+    if args.prefetch_max >= 0:
+        cfg = cfg.with_(prefetch_max=min(args.prefetch_max, cfg.top_k))
+    if args.tokens:
+        cfg = cfg.with_(tokens=min(args.tokens, cfg.tokens))
+    if args.layers:
+        cfg = cfg.with_(layers=min(args.layers, cfg.layers))
+    fetch_mode = {"kernel": b.MOE_FETCH_KERNEL, "dma": b.MOE_FETCH_DMA, "split": b.MOE_FETCH_SPLIT}[args.fetch]
+    slots = args.slots or 4
+    if not cfg.top_k <= slots <= cfg.experts:
+        sys.exit(f"--slots must lie in [top_k, experts] = [{cfg.top_k}, {cfg.experts}]")
+    if args.host_store != "plain" and cfg.dtype != "bf16":
+        sys.exit("a coded host store holds bf16 experts")
+    steps = max(1, args.steps)
+    chunk = math.ceil(cfg.tokens / steps)
+    steps = math.ceil(cfg.tokens / chunk)  # every step decodes at least one token
+    spec = cfg.prefetch_max > 0
+    flags = b.MOE_PREFETCH_NEXT if spec else 0
+
+    log("generating", cfg.name, "host store", cfg.layers * cfg.experts * cfg.expert_bytes / 1e9, "GB")
+    t0 = time.perf_counter()
+    store = offload.HostStore(cfg, fmt=args.host_store)
+    gates = offload.DeviceGates(cfg)
+    h0 = wl.hidden_states(cfg)
+    log(f"inputs ready in {time.perf_counter() - t0:.1f}s ({store.distinct} distinct layers pinned)")
+    link_info = measure_link(torch, b)
+    link = link_info["best"]
+    log(f"host link ceiling: {link:.2f} GB/s ({link_info['best_is']}; DMA {link_info['sdma']} GB/s)")
+    hbm_probe = measure_hbm_read(torch, b)
+    log(f"HBM read probe: {hbm_probe:.1f} GB/s")
+    mfma = measure_mfma(torch, b)
+    log("bf16 MFMA probe:", mfma)
+    calibrate_counters(torch)
+
+    H0 = torch.from_numpy(h0[:cfg.tokens]).to("cuda")
+    H = torch.empty_like(H0)
+    moe = offload.OffloadedMoE(cfg, store, gates, slots, "lfu", prefetch_max=cfg.prefetch_max if spec else 0,
+                               fetch_mode=fetch_mode)
+    if args.warmup:
+        wt = min(cfg.tokens, args.warmup * chunk)
+        w = run_chunks(torch, b, moe, H0, H, args.warmup, chunk, wt, b.MOE_TIMING_OFF, flags)
+        log(f"warm-up: {args.warmup} steps, {wt} tokens, {wt / w['total']:.2f} tok/s")
+    # timed pass: events on the decode FFN up launches only (the roofline kernel)
+    head = run_chunks(torch, b, moe, H0, H, steps, chunk, cfg.tokens, b.MOE_TIMING_FFN_UP, flags)
+    tokens_per_s = cfg.tokens / head["total"]
+    log(f"lfu {slots} {'prefetch ' if spec else ''}{tokens_per_s:.3f} tok/s over {cfg.tokens} tokens "
+        f"in {steps} steps of {chunk}")
+    # every launch timed, on a prefix: kernel breakdown, copy time, overlap
+    bd_tokens = max(1, min(cfg.tokens, args.breakdown_tokens))
+    bd = run_chunks(torch, b, moe, H0, H, 1, bd_tokens, bd_tokens, b.MOE_TIMING_ALL, flags)
+    moe.close()
+
+    comparisons = {}
+    if not args.lfu_only:
+        for policy, s_, sp, prefix in STACK_COMPARISONS[args.workload]:
+            if not cfg.top_k <= s_ <= cfg.experts:
+                continue
+            n = min(prefix, cfg.tokens)
+            m = offload.OffloadedMoE(cfg, store, gates, s_, policy, prefetch_max=2 if sp else 0,
+                                     fetch_mode=fetch_mode)
+            r = run_chunks(torch, b, m, H0, H, 1, n, n, b.MOE_TIMING_OFF, b.MOE_PREFETCH_NEXT if sp else 0)
+            m.close()
+            key = f"{policy}-s{s_}" + ("-prefetch2" if sp else "")
+            comparisons[key] = pass_summary(cfg, r, s_, sp)
+            comparisons[key]["prefix"] = f"first {n} of the {cfg.tokens} tokens, one pass from the warm start"
+            log(key, f"{comparisons[key]['tokens_per_s']:.3f} tok/s over {n} tokens")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cap = min(args.cpu_tokens, cfg.tokens) if args.cpu_tokens > 0 else cfg.tokens
+        cpu = cpu_baseline(cfg, store, gates.host, h0, cap, slots, "lfu", args.cpu_seconds)
+    aliased = store.aliased
+    distinct = store.distinct
+    store.close()
+    layer_cmp = None
+    if args.workload == "mixtral-stack" and not args.lfu_only and not args.no_layer_comparison:
+        layer_cmp = layer_comparison(torch, b, offload, wl, fetch_mode)
+
+    # ---- the report ---------------------------------------------------------
+    K, d, dff, mb = cfg.top_k, cfg.d_model, cfg.d_ff, cfg.matrix_bytes
+    up_bytes = K * 2 * mb + d * 4 + K * dff * 4
+    down_bytes = K * mb + K * dff * 4 + d * 4
+    ut = head["tim"]
+    up_ms = ut["ffn_up_ms"] / ut["ffn_up_n"]
+    up_gbps = up_bytes / (up_ms * 1e-3) / 1e9
+    bt = bd["tim"]
+    down_ms = bt["ffn_down_ms"] / max(1, bt["ffn_down_n"])
+    down_gbps = down_bytes / (down_ms * 1e-3) / 1e9 if down_ms > 0 else None
+    fetched = sum(s["bytes_fetched"] for s in head["stats"])
+    bd_fetched = sum(s["bytes_fetched"] for s in bd["stats"])
+    copy_ms = bt["fetch_ms"] + bt["pf_fetch_ms"]
+    fetch_gbps = bd_fetched / (copy_ms * 1e-3) / 1e9 if copy_ms > 0 else None
+    acc = [x for x in head["recs"] if x[0] != 2]
+    headline = pass_summary(cfg, head, slots, flags)
+    kind = "ffnq" if cfg.dtype == "q2g16" else "ffn"
+    desc = (DESCRIPTIONS[args.workload]
+            + f"; {cfg.tokens} batch-1 decode tokens from the warm start, {slots} HBM slots per layer, LFU"
+            + (f", next-layer prefetch of up to {cfg.prefetch_max}" if spec else "")
+            + f"; each step decodes {chunk} consecutive tokens through all {cfg.layers} layers and the "
+              f"cache carries over between steps"
+            + (f"; only the first {cfg.layers} layers" if args.layers else "")
+            + (f"; the pinned store holds {distinct} distinct layers and layer l >= {distinct} reuses the "
+               f"pages of layer l mod {distinct} (the driver pins about 70 GB at most): every miss still moves "
+               f"a whole expert over the host link, only weight values repeat, gates are per layer"
+               if aliased else ""))
+    out = {
+        "metric": METRIC,
+        "value": round(tokens_per_s, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * head["total"] / steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": desc,
+            "weights_dtype": cfg.dtype,
+            "layers": cfg.layers,
+            "policy": "lfu",
+            "slots": slots,
+            "speculative_prefetch": cfg.prefetch_max if spec else 0,
+            "decode_tokens": cfg.tokens,
+            "decode_tokens_per_step": chunk,
+            "fetch": args.fetch,
+            "host_store": args.host_store if args.host_store != "plain" else cfg.dtype,
+        },
+        "hit_rate": headline["hit_rate"],
+        "headline_run": headline,
+        "step_ms": {"min": round(1e3 * min(head["step_s"]), 1), "max": round(1e3 * max(head["step_s"]), 1),
+                    "median": round(1e3 * sorted(head["step_s"])[len(head["step_s"]) // 2], 1)},
+        "runs": comparisons,
+        "roofline": {
+            "kernel": f"{kind}_up_kernel",
+            "bound": "hbm",
+            "achieved": round(up_gbps, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(up_gbps / HBM_PEAK_GBPS, 4),
+            "traffic": pmc_traffic() if kind == "ffn" else None,
+            "bytes_per_launch": up_bytes,
+            "avg_launch_us": round(up_ms * 1e3, 2),
+            "launches": ut["ffn_up_n"],
+            "note": "events stamped by every up launch of the timed pass; the step itself is bound by the "
+                    "host link (link_roofline)",
+        },
+        "ffn_down": {"kernel": f"{kind}_down_kernel", "achieved_gbps": round(down_gbps, 1) if down_gbps else None,
+                     "frac": round(down_gbps / HBM_PEAK_GBPS, 4) if down_gbps else None,
+                     "bytes_per_launch": down_bytes, "avg_launch_us": round(down_ms * 1e3, 2),
+                     "reduce_avg_us": round(1e3 * bt["ffn_reduce_ms"] / max(1, bt["ffn_reduce_n"]), 2),
+                     "from": f"the {bd_tokens}-token pass with every launch timed"},
+        "hbm_read_probe": {"kernel": "hbm_read_probe_kernel", "gbps": round(hbm_probe, 1), "bytes": 1 << 30,
+                           "roofline_kernel_frac_of_probe": round(up_gbps / hbm_probe, 4) if hbm_probe else None},
+        "mfma_bf16_probe_tflops": mfma,
+        "link_roofline": {
+            "kernel": "fetch_kernel",
+            "bound": "host-link",
+            "achieved": round(fetch_gbps, 2) if fetch_gbps else None,
+            "peak": round(link, 2),
+            "unit": "GB/s",
+            "frac": round(fetch_gbps / link, 4) if fetch_gbps else None,
+            "peak_is": link_info["best_is"],
+            "probes_gbps": {"dma": link_info["sdma"], "shader_by_workgroups": link_info["shader"]},
+            "achieved_is": f"bytes fetched / copy time of the {bd_tokens}-token pass with every launch timed",
+            "bytes_fetched_timed_pass": fetched,
+            "link_rate_over_timed_pass_gbps": round(fetched / head["total"] / 1e9, 2),
+        },
+        "router_us": round(1e3 * bt["router_ms"] / max(1, bt["router_n"]), 2),
+    }
+    ffn_bytes = cfg.tokens * cfg.layers * (up_bytes + down_bytes)
+    link_s = fetched / (link * 1e9)
+    hbm_s = ffn_bytes / (HBM_PEAK_GBPS * 1e9)
+    out["step_roofline"] = {
+        "bound_s": round(link_s + hbm_s, 3), "achieved_s": round(head["total"], 3),
+        "frac": round((link_s + hbm_s) / head["total"], 4),
+        "terms": "whole timed pass: its link bytes / link ceiling + FFN weight bytes / 8 TB/s (no overlap)",
+        "overlap_bound_s": round(max(link_s, hbm_s), 3),
+        "overlap_frac": round(max(link_s, hbm_s) / head["total"], 4),
+    }
+    bd_ms = 1e3 * bd["total"]
+    out["copy_overlap"] = {
+        "tokens": bd_tokens,
+        "demand_copy_ms": round(bt["fetch_ms"], 2), "prefetch_copy_ms": round(bt["pf_fetch_ms"], 2),
+        "compute_wait_ms": round(bt["wait_ms"], 2), "pass_ms": round(bd_ms, 2),
+        "link_busy_frac": round(copy_ms / bd_ms, 4) if bd_ms > 0 else None,
+        "hidden_copy_frac": round(max(0.0, 1.0 - bt["wait_ms"] / copy_ms), 4) if copy_ms > 0 else None,
+        "definition": "hidden_copy_frac = 1 - compute wait / copy time: the share of the copy time "
+                      "(demand + speculative) during which the compute stream was not waiting",
+    }
+    out["trace_analytics"] = analysis.report(acc, cfg.layers, cfg.experts, cfg.top_k)
+    if layer_cmp:
+        out["mixtral_layer_runs"] = layer_cmp
+    if cpu is not None:
+        tps, n, dt, thr = cpu
+        out["cpu_baseline"] = {
+            "value": round(tps, 4), "unit": "tokens/s", "cores": thr, "kind": "oracle",
+            "sample": f"first {n} of the {cfg.tokens} decode tokens (a {args.cpu_seconds:g} s budget), fp64 router "
+                      f"+ LFU cache + SwiGLU FFN through all {cfg.layers} layers from the warm start (bf16->fp64 "
+                      f"widening of each used expert included), {dt:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
+def layer_main(args):
+    """Workloads whose step is a whole pass over the token set from the warm
+    start (the one-layer workloads, the 64-expert stack with its prefill,
+    batched decode)."""
     import torch
 
     from paper_2511_05814_amd import binding as b
@@ -361,8 +655,9 @@ def main():
     gates = offload.DeviceGates(cfg)
     h0 = wl.hidden_states(cfg)
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s")
-    link = measure_link(torch)
-    log(f"measured pinned H2D link: {link:.2f} GB/s")
+    link_info = measure_link(torch, b)
+    link = link_info["best"]
+    log(f"host link ceiling: {link:.2f} GB/s ({link_info['best_is']})")
     hbm_probe = measure_hbm_read(torch, b)
     log(f"HBM read probe: {hbm_probe:.1f} GB/s")
     calibrate_counters(torch)
@@ -507,7 +802,8 @@ def main():
             "peak": round(link, 2),
             "unit": "GB/s",
             "frac": round(fetch_gbps / link, 4) if fetch_gbps else None,
-            "peak_is": "best measured 1 GiB pinned H2D copy",
+            "peak_is": link_info["best_is"],
+            "probes_gbps": {"dma": link_info["sdma"], "shader_by_workgroups": link_info["shader"]},
             "decode_bytes_fetched_per_step": fetched // head["steps"],
         },
         "router_us": round(1e3 * tim["router_ms"] / tim["router_n"], 2),
@@ -517,10 +813,15 @@ def main():
     # experts' weights streamed from HBM at peak
     ffn_step_bytes = cfg.tokens * cfg.layers * (up_bytes + down_bytes)
     bound_s = fetched / head["steps"] / (link * 1e9) + ffn_step_bytes / (HBM_PEAK_GBPS * 1e9)
+    link_s = fetched / head["steps"] / (link * 1e9)
+    hbm_s = ffn_step_bytes / (HBM_PEAK_GBPS * 1e9)
+    step_s = head["dec"] / head["steps"]
     out["step_roofline"] = {"bound_ms_per_step": round(1e3 * bound_s, 3),
-                            "achieved_ms_per_step": round(1e3 * head["dec"] / head["steps"], 3),
-                            "frac": round(bound_s / (head["dec"] / head["steps"]), 4),
-                            "terms": "link bytes / measured link + FFN weight bytes / 8 TB/s"}
+                            "achieved_ms_per_step": round(1e3 * step_s, 3),
+                            "frac": round(bound_s / step_s, 4),
+                            "terms": "link bytes / measured link + FFN weight bytes / 8 TB/s (no overlap)",
+                            "overlap_bound_ms_per_step": round(1e3 * max(link_s, hbm_s), 3),
+                            "overlap_frac": round(max(link_s, hbm_s) / step_s, 4)}
     # how the copies overlap the compute: the compute stream's wait between
     # each router and its FFN against the copy time (demand + speculative)
     dec_ms = 1e3 * head["dec"] / head["steps"]
@@ -569,6 +870,51 @@ def main():
                                   f"start (bf16->fp64 widening included), {dt:.1f} s"}
     store.close()
     print(json.dumps(out), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mixtral-stack", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--cpu-tokens", type=int, default=0,
+                    help="most decode tokens the fp64 oracle is timed on (0: the whole workload)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="time budget of the fp64 oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fetch", choices=["split", "kernel", "dma"], default="split",
+                    help="split: demand misses by the copy kernel, speculative prefetches by the DMA engines")
+    ap.add_argument("--tokens", type=int, default=0,
+                    help="decode only the first N tokens of the workload (profiling passes)")
+    ap.add_argument("--lfu-only", action="store_true", help="skip the comparison runs")
+    ap.add_argument("--layers", type=int, default=0, help="run only the first N layers of the workload")
+    ap.add_argument("--prefill-tokens", type=int, default=-1,
+                    help="prefill at most this many tokens (0: decode only)")
+    ap.add_argument("--slots", type=int, default=0,
+                    help="HBM slots per layer (default 4, 16 for the 64-expert workload; "
+                         "slots = experts keeps every expert resident)")
+    ap.add_argument("--host-store", choices=["plain", "packed", "entropy"], default="plain",
+                    help="packed / entropy: bf16 experts coded losslessly in host memory (~12.25 / ~10.9 bits a "
+                         "weight) and rebuilt on the GPU after each copy")
+    ap.add_argument("--prefetch-max", type=int, default=-1,
+                    help="override the workload's cap on next-layer experts prefetched per layer (0 turns "
+                         "speculation off)")
+    ap.add_argument("--batch", type=int, default=1,
+                    help="decode B tokens per step through the batch path (bf16 experts; no speculation)")
+    ap.add_argument("--breakdown-tokens", type=int, default=32,
+                    help="stack workloads: tokens of the extra pass with every launch timed")
+    ap.add_argument("--no-layer-comparison", action="store_true",
+                    help="stack workloads: skip the one-layer Mixtral comparison runs")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the decode path runs on a single GPU with no collectives)", file=sys.stderr)
+        sys.exit(2)
+    if args.workload in STACK_WORKLOADS and args.batch == 1:
+        stack_main(args)
+    else:
+        layer_main(args)
 
 
 if __name__ == "__main__":

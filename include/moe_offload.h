@@ -21,8 +21,11 @@
  *     from hipHostMalloc (or moe_host_alloc); "host" is ordinary memory.
  *   - The caller owns every buffer it passes (gates, host store, arena,
  *     workspace, trace, hidden states) and both streams; they must outlive
- *     the handle.  The library owns the handle, its HIP events and a small
- *     pinned mirror; it never frees caller memory.
+ *     the handle.  The library owns the handle and the runtime objects it
+ *     uses (HIP events, a side stream, small pinned buffers); those come
+ *     from a process-wide pool and go back to it when the handle is
+ *     destroyed, and are released only when the process ends.  It never
+ *     frees caller memory.
  *   - Decode, prefetch, prefill and access calls only enqueue work on the
  *     streams; errors found while enqueuing are returned at once.  Faults of
  *     device work are sticky: they are reported by the next synchronising
@@ -205,7 +208,11 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d);
 
 /* Warm start (synchronous): slot s of every layer holds expert s, counts 0,
  * clocks 0, statistics and trace cleared; experts 0..S-1 are copied into the
- * slots.  Clears a sticky error. */
+ * slots.  Clears a sticky error.  The paper does not say how its caches start;
+ * this reading follows Table 2, whose cache recall is exactly twice its
+ * precision for a cache of 4 experts and top-2 routing (Sec. 5.3): that holds
+ * only if the cache is full from the first counted token, so the caches start
+ * full rather than empty. */
 int moe_cache_reset(moe_cache_t *c);
 
 /* One token through one layer (Sec. 2.2): route h [d] (device fp32, updated
@@ -215,12 +222,22 @@ int moe_cache_reset(moe_cache_t *c);
  * this h and fetch up to prefetch_max of them (Sec. 3.2).  Enqueue only. */
 int moe_decode_layer(moe_cache_t *c, int layer, float *h, int flags);
 
-/* The speculative part alone: guess next_layer's experts from h (device fp32
- * [d], read only) with next_layer's gate and fetch up to max_experts of them
- * (0..K).  MOE_ERR_ARG if next_layer is 0 or >= L. Enqueue only. */
+/* The speculative part alone (Sec. 3.2, Sec. 4.3: each layer also holds the
+ * next layer's gate, and that gate applied to the current hidden state,
+ * followed by softmax and top-K, guesses the next layer's experts): guess
+ * next_layer's experts from h (device fp32 [d], read only) with next_layer's
+ * gate and fetch up to max_experts of them (0..K), evicting by the layer's
+ * policy with all K guesses protected; an inserted guess takes one tick of
+ * the layer's clock and does not count as a use.  MOE_ERR_ARG if next_layer
+ * is 0 or >= L, or max_experts is outside 0..K.  Enqueue only. */
 int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts);
 
-/* A batch of `tokens` rows H [tokens][d] (device fp32, in place) through one
+/* Batched prefill.  The paper measures generated tokens only and says nothing
+ * about the prompt (Sec. 5.1); this call is this library's reading: the batch
+ * is routed and computed row by row exactly as decode tokens (Sec. 2.2, Sec.
+ * 4.3), and the cache takes the batch's routing at once by the same policy
+ * (Sec. 3.1 LRU, Sec. 4.2 LFU).
+ * A batch of `tokens` rows H [tokens][d] (device fp32, in place) through one
  * layer: every row is routed and computed as a decode token would be; the
  * layer's cache takes the batch's routing at once (counts += per-expert
  * routings, the clock ticks once per (token, rank), then the S experts with the
@@ -234,10 +251,14 @@ int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts
  * routing then surfaces at the next synchronising call. */
 int moe_prefill_layer(moe_cache_t *c, int layer, float *H, int tokens);
 
-/* Injected routing (test hook): run layer `layer`'s cache lookup, fetches and
- * trace for the K expert ids at `ids` (device int32 [K], rank order, distinct,
- * each in [0, E)).  Invalid ids are detected on the device, nothing is
- * changed, and the next synchronising call returns MOE_ERR_ARG. */
+/* Injected routing (test hook): the cache lookup alone (Sec. 3.1: a selected
+ * expert already in the layer's cache is reused, a missing one is loaded and
+ * the least recently used one evicted; Sec. 4.2: LFU keeps a usage count per
+ * expert and evicts the least frequently used).  Runs layer `layer`'s lookup,
+ * fetches and trace for the K expert ids at `ids` (device int32 [K], rank
+ * order, distinct, each in [0, E)), with no router and no FFN.  Invalid ids
+ * are detected on the device, nothing is changed, and the next synchronising
+ * call returns MOE_ERR_ARG. */
 int moe_cache_access(moe_cache_t *c, int layer, const int *ids);
 
 /* Wait for both streams; report sticky errors. */
@@ -293,11 +314,14 @@ enum { MOE_TIMING_OFF = 0, MOE_TIMING_ALL = 1, MOE_TIMING_FFN_UP = 2 };
 int moe_cache_set_timing(moe_cache_t *c, int enable);
 int moe_cache_read_timing(moe_cache_t *c, moe_timing *out);
 
-/* Drain the streams, release events; NULL-safe. */
+/* Drain every stream the handle enqueued on, return its events, side stream
+ * and pinned buffers to the process pool, free the handle; NULL-safe. */
 void moe_cache_destroy(moe_cache_t *c);
 
 /* Pinned host memory for the expert store (hipHostMalloc); *out is usable
- * from both host and device.  moe_host_free(NULL) is a no-op. */
+ * from both host and device.  moe_host_free waits for all work on the current
+ * device (copies from the store may still be queued) before it frees;
+ * moe_host_free(NULL) is a no-op. */
 int moe_host_alloc(size_t bytes, void **out);
 int moe_host_free(void *p);
 
@@ -328,6 +352,32 @@ int moe_entropy_pack(const uint16_t *w, size_t n, size_t cap_words, void *out, s
  * Synchronous.  MOE_ERR_ARG for bad arguments, MOE_ERR_HIP for runtime
  * failures.  Use a buffer well above the 256 MB last-level cache. */
 int moe_probe_hbm_read(const void *buf, size_t bytes, int reps, void *stream, double *gbps);
+
+/* Calibration, not part of the decode path: the host-to-device rate (GB/s)
+ * of a shader copy with the fetch kernel's access pattern (16-byte loads from
+ * mapped pinned host memory, four in flight a lane, `workgroups` workgroups
+ * of 256 lanes, 1..4096), the other way besides the DMA engines that experts
+ * reach HBM (Sec. 2.2: experts are loaded into GPU memory on demand).  Copies
+ * `bytes` (a positive multiple of 16) from host_src (pinned host memory from
+ * hipHostMalloc / moe_host_alloc, mapped for the device, 16-byte aligned) to
+ * dev_dst (device, 16-byte aligned) `reps` times (1..1000) on `stream` after
+ * one untimed copy; *gbps = bytes * reps over the time between events
+ * recorded around the timed copies.  Synchronous.  MOE_ERR_ARG for bad
+ * arguments or a host buffer the device cannot address, MOE_ERR_HIP for
+ * runtime failures. */
+int moe_probe_h2d_copy(const void *host_src, void *dev_dst, size_t bytes, int workgroups, int reps,
+                       void *stream, double *gbps);
+
+/* Calibration, not part of the decode path: the bf16 matrix-core rate
+ * (TFLOP/s) of a kernel that does nothing but issue MFMA instructions on
+ * register operands (four independent accumulations per wave, 32 waves per
+ * compute unit), the practical ceiling of the batched prefill's grouped GEMMs
+ * (Sec. 2.1: the experts of a batch are dense products).  shape 0:
+ * v_mfma_f32_16x16x32_bf16 (the grouped GEMMs' instruction), 1:
+ * v_mfma_f32_32x32x16_bf16; `iters` (1..2^20) instructions per accumulation.
+ * One untimed launch, then one timed launch on `stream`.  Synchronous.
+ * MOE_ERR_ARG for bad arguments, MOE_ERR_HIP for runtime failures. */
+int moe_probe_mfma_bf16(int shape, int iters, void *stream, double *tflops);
 
 /* Thread-local message of the last failure on this thread ("" if none). */
 const char *moe_last_error(void);

@@ -10,6 +10,18 @@
   positive if the expert is activated at that layer for the same token.  With
   K guesses and K activations every wrong guess is one false positive and one
   false negative, so precision = recall.  Layer 0 has no guess and is left out.
+* Transfer precision (this implementation's reading; the paper only logged
+  guesses, Sec. 4.3): prefetched experts whose next lookup at that layer uses
+  them / prefetched experts fetched.
+* Per-layer activation histograms (Sec. 5.2) and the rate at which a token
+  reuses the previous token's experts at a layer, compared in Sec. 3.1 with
+  the 1/E of random routing.
+
+Pins: guess_pr and transfer_precision against hand-worked three-token traces
+(including records keyed one token or one layer off, which must change the
+result); cache_pr against Table 2's printed pairs; the histogram and repeat
+rates against hand-worked traces and against their closed forms (K/E and 1/E)
+under uniform random routing.
 """
 from __future__ import annotations
 
@@ -79,3 +91,41 @@ def per_layer_hit_rate(records: Iterable[Rec]):
             n[r.layer] += 1
             h[r.layer] += bool(r.flags & F_HIT)
     return {l: h[l] / n[l] for l in sorted(n)}
+
+
+def activation_histogram(records: Iterable[Rec], layer: int, experts: int):
+    """Activations of each expert at one layer (Sec. 5.2)."""
+    h = [0] * experts
+    for r in records:
+        if r.kind == KIND_ACCESS and r.layer == layer:
+            h[r.expert] += 1
+    return h
+
+
+def _by_lookup(records, layer):
+    ids = defaultdict(dict)
+    for r in records:
+        if r.kind == KIND_ACCESS and r.layer == layer:
+            ids[r.token][r.rank] = r.expert
+    return ids
+
+
+def repeat_rate(records: Iterable[Rec], layer: int) -> float:
+    """Over consecutive lookups (t-1, t) at one layer: experts of token t that
+    token t-1 also selected / experts of token t."""
+    ids = _by_lookup(records, layer)
+    same = total = 0
+    for t in sorted(ids):
+        if t - 1 in ids:
+            prev = set(ids[t - 1].values())
+            same += sum(1 for e in ids[t].values() if e in prev)
+            total += len(ids[t])
+    return same / total if total else 0.0
+
+
+def top1_repeat_rate(records: Iterable[Rec], layer: int) -> float:
+    """Over consecutive lookups (t-1, t) at one layer: the share whose
+    first-ranked experts are the same (1/E under uniform random routing)."""
+    ids = _by_lookup(records, layer)
+    pairs = [(ids[t - 1][0], ids[t][0]) for t in sorted(ids) if t - 1 in ids]
+    return sum(1 for a, b in pairs if a == b) / len(pairs) if pairs else 0.0

@@ -32,6 +32,10 @@ class Model:
         self._experts: Dict[tuple, tuple] = {}
         self._gates: Dict[int, np.ndarray] = {}
 
+    def forget(self) -> None:
+        """Drop the widened experts kept so far (bounds memory in long checks)."""
+        self._experts.clear()
+
     def gate(self, l: int) -> np.ndarray:
         # the gate of a group-quantised model stays bf16
         if l not in self._gates:

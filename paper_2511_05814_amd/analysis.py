@@ -98,6 +98,47 @@ def repeat_rate(records, layer: int) -> float:
     return same / total if total else 0.0
 
 
+def top1_repeat_rate(records, layer: int) -> float:
+    """Fraction of tokens whose first-ranked expert at this layer is the
+    previous token's first-ranked expert (consecutive lookups only).  With
+    uniform random routing this is 1/E, the baseline Sec. 3.1 quotes."""
+    first = {}
+    for r in records:
+        if r[0] == ACCESS and r[2] == layer and r[3] == 0:
+            first[r[1]] = r[4]
+    toks = sorted(first)
+    pairs = [(a, b) for a, b in zip(toks[:-1], toks[1:]) if b == a + 1]
+    return sum(1 for a, b in pairs if first[a] == first[b]) / len(pairs) if pairs else 0.0
+
+
+# Layers whose activation histograms Sec. 5.2 shows (1-based, as the paper
+# numbers them): the first two layers and pairs around each quarter.
+PAPER_HISTOGRAM_LAYERS = (1, 2, 7, 8, 15, 16, 23, 24, 31, 32)
+
+
+def report(records, layers: int, experts: int, top_k: int):
+    """The analyses of Sec. 3.1 and Sec. 5.2 over one run's trace: hit rate
+    per layer, activation histograms of the paper's layer set (those that
+    exist; 0-based layer = paper layer - 1), and per layer the share of a
+    token's experts the previous token also selected (random routing: K/E)
+    and the first-ranked expert's repeat rate (random routing: 1/E)."""
+    acc, _, _ = split(records)
+    hist_layers = [p - 1 for p in PAPER_HISTOGRAM_LAYERS if p <= layers] or list(range(min(layers, 2)))
+    rep = [repeat_rate(acc, l) for l in range(layers)]
+    top1 = [top1_repeat_rate(acc, l) for l in range(layers)]
+    return {
+        "per_layer_hit_rate": [round(v, 4) for v in per_layer_hit_rate(acc).values()],
+        "activation_histograms": {str(l + 1): activation_histogram(acc, l, experts) for l in hist_layers},
+        "histogram_layers_are": "1-based layer numbers as in Sec. 5.2",
+        "repeat_rate": {"mean": round(sum(rep) / max(1, len(rep)), 4),
+                        "per_layer": [round(v, 4) for v in rep],
+                        "random_routing": round(top_k / experts, 4)},
+        "top1_repeat_rate": {"mean": round(sum(top1) / max(1, len(top1)), 4),
+                             "per_layer": [round(v, 4) for v in top1],
+                             "random_routing": round(1 / experts, 4)},
+    }
+
+
 def demand_sequences(records):
     """Per layer, the experts of its access records in (token, rank) order."""
     acc, _, _ = split(records)

@@ -115,6 +115,10 @@ _SIGNATURES = [
      [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_void_p, ctypes.POINTER(ctypes.c_size_t)]),
     ("moe_probe_hbm_read", ctypes.c_int,
      [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
+    ("moe_probe_h2d_copy", ctypes.c_int,
+     [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+      ctypes.POINTER(ctypes.c_double)]),
+    ("moe_probe_mfma_bf16", ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
     ("moe_last_error", ctypes.c_char_p, []),
 ]
 EXPORTED = [s[0] for s in _SIGNATURES]
@@ -255,6 +259,21 @@ def moe_probe_hbm_read(buf_ptr: int, nbytes: int, reps: int, stream: int) -> flo
     """Streaming read rate (GB/s) of nbytes of device memory at buf_ptr."""
     out = ctypes.c_double()
     _check(lib().moe_probe_hbm_read(buf_ptr, nbytes, reps, stream, ctypes.byref(out)), "moe_probe_hbm_read")
+    return out.value
+
+
+def moe_probe_h2d_copy(host_ptr: int, dev_ptr: int, nbytes: int, workgroups: int, reps: int, stream: int) -> float:
+    """Host-to-device shader-copy rate (GB/s) from pinned host_ptr to dev_ptr."""
+    out = ctypes.c_double()
+    _check(lib().moe_probe_h2d_copy(host_ptr, dev_ptr, nbytes, workgroups, reps, stream, ctypes.byref(out)),
+           "moe_probe_h2d_copy")
+    return out.value
+
+
+def moe_probe_mfma_bf16(shape: int, iters: int, stream: int) -> float:
+    """bf16 matrix-core rate (TFLOP/s) of a register-only MFMA loop."""
+    out = ctypes.c_double()
+    _check(lib().moe_probe_mfma_bf16(shape, iters, stream, ctypes.byref(out)), "moe_probe_mfma_bf16")
     return out.value
 
 

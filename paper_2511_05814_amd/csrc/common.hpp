@@ -94,7 +94,6 @@ struct FfnArgs {
   float *part;             // [chunks][d]
   uint64_t expert_bytes;
   int layer, S, K, d, d_ff;
-  int phase;               // up: 0 all ranks, 1 hit ranks, 2 missed ranks
 };
 
 // ---- batched prefill ------------------------------------------------------
@@ -162,6 +161,11 @@ struct Launch {
 // Streaming read of bytes (a multiple of 16) at buf with the given number of
 // workgroups; reads only.
 hipError_t launch_hbm_read_probe(const void *buf, size_t bytes, int workgroups, hipStream_t s);
+// Copy bytes (a multiple of 16) from src_dev (the device address of mapped
+// pinned host memory) to dst with the fetch kernel's access pattern.
+hipError_t launch_h2d_copy_probe(const void *src_dev, void *dst, size_t bytes, int workgroups, hipStream_t s);
+// Register-only bf16 MFMA loop; returns the flops the launch performs.
+double launch_mfma_bf16_probe(int shape, int workgroups, int iters, hipStream_t s);
 hipError_t launch_router(const RouterArgs &a, const Launch &l);
 // Copies of a fetch list: expert e of the list's layer from its host store
 // (stride src_stride) into its HBM slot (stride expert_bytes), or, when

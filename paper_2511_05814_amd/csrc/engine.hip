@@ -22,6 +22,8 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -50,6 +52,79 @@ struct Layout {
 };
 
 bool misaligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) != 0; }
+
+// Process-wide pool of the runtime objects handles own: events, the side
+// stream and the small pinned host buffers.  A handle takes them at bind and
+// gives them back at destroy; they are never destroyed while the process
+// runs.  Draining a stream only waits for its last completion signal: the
+// runtime, and a profiler attached to it, may still be running completion
+// handlers for the same dispatches on worker threads, and those handlers
+// read the events the dispatches stamped.  Releasing an event, stream or
+// pinned buffer right after the drain could pull memory out from under such
+// a handler; returning it to this pool cannot.
+struct Pool {
+  std::vector<hipEvent_t> sync_ev, timed_ev;
+  std::vector<hipStream_t> streams;
+  std::multimap<size_t, void *> pinned;  // by size
+};
+std::mutex g_pool_mu;
+std::map<int, Pool> g_pool;  // by device
+
+hipError_t pool_event(int dev, bool timed, hipEvent_t *e) {
+  {
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    auto &v = timed ? g_pool[dev].timed_ev : g_pool[dev].sync_ev;
+    if (!v.empty()) {
+      *e = v.back();
+      v.pop_back();
+      return hipSuccess;
+    }
+  }
+  return timed ? hipEventCreate(e) : hipEventCreateWithFlags(e, hipEventDisableTiming);
+}
+
+hipError_t pool_stream(int dev, hipStream_t *s) {
+  {
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    auto &v = g_pool[dev].streams;
+    if (!v.empty()) {
+      *s = v.back();
+      v.pop_back();
+      return hipSuccess;
+    }
+  }
+  return hipStreamCreateWithFlags(s, hipStreamNonBlocking);
+}
+
+// Pinned host memory of at least `bytes`; *got = the size actually held.
+hipError_t pool_pinned(int dev, size_t bytes, void **p, size_t *got) {
+  {
+    std::lock_guard<std::mutex> g(g_pool_mu);
+    auto &m = g_pool[dev].pinned;
+    auto it = m.lower_bound(bytes);
+    if (it != m.end() && it->first <= 2 * bytes + 4096) {
+      *got = it->first;
+      *p = it->second;
+      m.erase(it);
+      return hipSuccess;
+    }
+  }
+  *got = bytes;
+  return hipHostMalloc(p, bytes, hipHostMallocDefault);
+}
+
+void pool_give_back(int dev, const std::vector<hipEvent_t> &sync_ev, const std::vector<hipEvent_t> &timed_ev,
+                    hipStream_t stream, const std::vector<std::pair<size_t, void *>> &pinned) {
+  std::lock_guard<std::mutex> g(g_pool_mu);
+  Pool &pl = g_pool[dev];
+  for (hipEvent_t e : sync_ev)
+    if (e) pl.sync_ev.push_back(e);
+  for (hipEvent_t e : timed_ev)
+    if (e) pl.timed_ev.push_back(e);
+  if (stream) pl.streams.push_back(stream);
+  for (const auto &b : pinned)
+    if (b.second) pl.pinned.emplace(b.first, b.second);
+}
 
 }  // namespace
 
@@ -103,6 +178,7 @@ static PrefillLayout prefill_layout(int K, int d, int d_ff, int E, int S, int T,
 struct moe_cache {
   int L = 0, E = 0, S = 0, policy = 0;
   bool bound = false;
+  bool pooled = false;   // holds runtime objects taken from the process pool
   moe_model_desc desc{};
   int K = 0, d = 0, dff = 0, dtype = 0, pmax = 0, fetch_mode = 0, max_T = 0;
   uint64_t B = 0;        // bytes of one expert in an HBM slot
@@ -131,7 +207,9 @@ struct moe_cache {
   hipStream_t ms = nullptr;  // library-owned: prefetch-list read-back (split fetch mode)
   std::vector<uint8_t> demand_pending, pf_pending;
   int sticky = MOE_OK;
+  int dev = 0;                  // device the handle was bound on (owner of its pooled objects)
   FetchList *mirror = nullptr;  // pinned host: demand list, prefetch list, error word (DMA / split modes)
+  size_t mirror_bytes = 0, plan_bytes = 0, sched_bytes = 0;  // sizes of the pooled pinned buffers
   int last_route_kind = 0;      // 0 none, 1 decode, 2 prefill
   int last_prefill_T = 0;
   // batched prefill
@@ -161,18 +239,24 @@ bool timed(const moe_cache *c, int kind) {
   return c->timing == MOE_TIMING_ALL || (c->timing == MOE_TIMING_FFN_UP && kind == SPAN_UP);
 }
 
+// An event for a timed span: the handle's own spare, else one from the
+// process pool.
+hipError_t take_timed_event(moe_cache *c, hipEvent_t *e) {
+  if (!c->ev_pool.empty()) {
+    *e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return hipSuccess;
+  }
+  return pool_event(c->dev, true, e);
+}
+
 // Start/stop a timed span on stream s (no-op unless its kind is timed).
 hipError_t span_begin(moe_cache *c, hipStream_t s, hipEvent_t *out, int kind) {
   *out = nullptr;
   if (!timed(c, kind)) return hipSuccess;
   hipEvent_t e;
-  if (!c->ev_pool.empty()) {
-    e = c->ev_pool.back();
-    c->ev_pool.pop_back();
-  } else {
-    hipError_t r = hipEventCreate(&e);
-    if (r != hipSuccess) return r;
-  }
+  hipError_t r = take_timed_event(c, &e);
+  if (r != hipSuccess) return r;
   *out = e;
   return hipEventRecord(e, s);
 }
@@ -180,13 +264,8 @@ hipError_t span_begin(moe_cache *c, hipStream_t s, hipEvent_t *out, int kind) {
 hipError_t span_end(moe_cache *c, hipStream_t s, int kind, hipEvent_t begin, double flop = 0.0) {
   if (!begin) return hipSuccess;
   hipEvent_t e;
-  if (!c->ev_pool.empty()) {
-    e = c->ev_pool.back();
-    c->ev_pool.pop_back();
-  } else {
-    hipError_t r = hipEventCreate(&e);
-    if (r != hipSuccess) return r;
-  }
+  hipError_t r = take_timed_event(c, &e);
+  if (r != hipSuccess) return r;
   c->spans.push_back({kind, begin, e, flop});
   return hipEventRecord(e, s);
 }
@@ -198,13 +277,8 @@ hipError_t kernel_span(moe_cache *c, hipStream_t s, Launch *l, int kind) {
   l->start = l->stop = nullptr;
   if (!timed(c, kind)) return hipSuccess;
   for (hipEvent_t *e : {&l->start, &l->stop}) {
-    if (!c->ev_pool.empty()) {
-      *e = c->ev_pool.back();
-      c->ev_pool.pop_back();
-    } else {
-      hipError_t r = hipEventCreate(e);
-      if (r != hipSuccess) return r;
-    }
+    hipError_t r = take_timed_event(c, e);
+    if (r != hipSuccess) return r;
   }
   return hipSuccess;
 }
@@ -448,29 +522,30 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   c->dev_layer_host = dl;
   HIP_TRY0(hipMemcpy(c->ws + lay.hostptrs, dl.data(), sizeof(void *) * c->L, hipMemcpyHostToDevice));
 
+  // runtime objects come from the process pool (released there by destroy,
+  // also when bind fails half way)
+  HIP_TRY0(hipGetDevice(&c->dev));
   c->ev_demand.assign(c->L, nullptr);
   c->ev_pf.assign(c->L, nullptr);
   c->demand_pending.assign(c->L, 0);
   c->pf_pending.assign(c->L, 0);
+  c->pooled = true;  // from here on destroy returns what was taken
   for (int l = 0; l < c->L; ++l) {
-    HIP_TRY0(hipEventCreateWithFlags(&c->ev_demand[l], hipEventDisableTiming));
-    HIP_TRY0(hipEventCreateWithFlags(&c->ev_pf[l], hipEventDisableTiming));
+    HIP_TRY0(pool_event(c->dev, false, &c->ev_demand[l]));
+    HIP_TRY0(pool_event(c->dev, false, &c->ev_pf[l]));
   }
-  HIP_TRY0(hipEventCreateWithFlags(&c->ev_router, hipEventDisableTiming));
-  if (c->fetch_mode == MOE_FETCH_SPLIT && !c->one_stream)
-    HIP_TRY0(hipStreamCreateWithFlags(&c->ms, hipStreamNonBlocking));
-  HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->mirror), 3 * sizeof(FetchList),
-                                 hipHostMallocDefault));
+  HIP_TRY0(pool_event(c->dev, false, &c->ev_router));
+  if (c->fetch_mode == MOE_FETCH_SPLIT && !c->one_stream) HIP_TRY0(pool_stream(c->dev, &c->ms));
+  HIP_TRY0(pool_pinned(c->dev, 3 * sizeof(FetchList), reinterpret_cast<void **>(&c->mirror), &c->mirror_bytes));
   if (c->max_T > 0) {
     c->play = prefill_layout(c->K, c->d, c->dff, c->E, c->S, c->max_T, c->B, coded_store(c->host_format) ? c->Bh : 0);
-    HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->h_plan), sizeof(PrefillPlan) * kMaxE,
-                           hipHostMallocDefault));
-    HIP_TRY0(hipHostMalloc(reinterpret_cast<void **>(&c->h_sched),
-                           sizeof(GemmJob) * kMaxE + sizeof(GemmTile) * (size_t)c->play.tile_cap +
-                               sizeof(FetchList) * kPrefillLists,
-                           hipHostMallocDefault));
+    HIP_TRY0(pool_pinned(c->dev, sizeof(PrefillPlan) * kMaxE, reinterpret_cast<void **>(&c->h_plan), &c->plan_bytes));
+    HIP_TRY0(pool_pinned(c->dev,
+                         sizeof(GemmJob) * kMaxE + sizeof(GemmTile) * (size_t)c->play.tile_cap +
+                             sizeof(FetchList) * kPrefillLists,
+                         reinterpret_cast<void **>(&c->h_sched), &c->sched_bytes));
     c->pf_ev.assign(2 * kMaxE + 4, nullptr);
-    for (auto &e : c->pf_ev) HIP_TRY0(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    for (auto &e : c->pf_ev) HIP_TRY0(pool_event(c->dev, false, &e));
   }
   c->bound = true;
   c->sticky = MOE_ERR_STATE;  // decode needs a reset first
@@ -716,7 +791,6 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     f.K = c->K;
     f.d = c->d;
     f.d_ff = c->dff;
-    f.phase = 0;
     HIP_TRY(c, span_end(c, c->cs, SPAN_WAIT, t_wait));
     Launch lu, ld, lx;
     HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_UP));
@@ -1121,6 +1195,32 @@ int prefill_routing(moe_cache *c, int32_t *ids, float *g, size_t cap, size_t *n)
 
 }  // namespace moe
 
+namespace {
+// Milliseconds between events recorded around `reps` calls of launch() on s,
+// after one untimed call.  The events come from the process pool.
+template <class F>
+int time_launches(hipStream_t s, int reps, F launch, const char *what, float *ms) {
+  int dev = 0;
+  HIP_TRY0(hipGetDevice(&dev));
+  hipEvent_t a = nullptr, b = nullptr;
+  HIP_TRY0(pool_event(dev, true, &a));
+  hipError_t e = pool_event(dev, true, &b);
+  if (e == hipSuccess) e = launch();  // warm-up
+  if (e == hipSuccess) e = hipEventRecord(a, s);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) e = launch();
+  if (e == hipSuccess) e = hipEventRecord(b, s);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  if (e == hipSuccess) e = hipEventElapsedTime(ms, a, b);
+  pool_give_back(dev, {}, {a, b}, nullptr, {});
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(MOE_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
+  }
+  return MOE_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int moe_decode_layer(moe_cache_t *c, int layer, float *h, int flags) {
@@ -1315,21 +1415,19 @@ void moe_cache_destroy(moe_cache_t *c) {
     c->ev_pool.push_back(sp.a);
     c->ev_pool.push_back(sp.b);
   }
-  if (c->bound) {
+  if (c->pooled) {
+    // drain every stream the handle enqueued on (its own side stream too),
+    // then hand its runtime objects back to the process pool rather than
+    // releasing them (see Pool)
     (void)hipStreamSynchronize(c->cs);
     if (!c->one_stream) (void)hipStreamSynchronize(c->xs);
-    for (hipEvent_t e : c->ev_demand)
-      if (e) (void)hipEventDestroy(e);
-    for (hipEvent_t e : c->ev_pf)
-      if (e) (void)hipEventDestroy(e);
-    if (c->ev_router) (void)hipEventDestroy(c->ev_router);
-    if (c->ms) (void)hipStreamDestroy(c->ms);
-    if (c->mirror) (void)hipHostFree(c->mirror);
-    if (c->h_plan) (void)hipHostFree(c->h_plan);
-    if (c->h_sched) (void)hipHostFree(c->h_sched);
-    for (hipEvent_t e : c->pf_ev)
-      if (e) (void)hipEventDestroy(e);
-    for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
+    if (c->ms) (void)hipStreamSynchronize(c->ms);
+    std::vector<hipEvent_t> sync_ev(c->ev_demand);
+    sync_ev.insert(sync_ev.end(), c->ev_pf.begin(), c->ev_pf.end());
+    sync_ev.insert(sync_ev.end(), c->pf_ev.begin(), c->pf_ev.end());
+    sync_ev.push_back(c->ev_router);
+    pool_give_back(c->dev, sync_ev, c->ev_pool, c->ms,
+                   {{c->mirror_bytes, c->mirror}, {c->plan_bytes, c->h_plan}, {c->sched_bytes, c->h_sched}});
     (void)hipGetLastError();
   }
   delete c;
@@ -1349,7 +1447,11 @@ int moe_host_alloc(size_t bytes, void **out) {
 
 int moe_host_free(void *p) {
   if (!p) return MOE_OK;
-  hipError_t e = hipHostFree(p);
+  // copies from the store may still be queued on caller streams: let every
+  // one of them finish before the pages go
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return fail(MOE_ERR_HIP, "hipDeviceSynchronize before hipHostFree failed: %s", hipGetErrorString(e));
+  e = hipHostFree(p);
   if (e != hipSuccess) return fail(MOE_ERR_HIP, "hipHostFree failed: %s", hipGetErrorString(e));
   return MOE_OK;
 }
@@ -1365,6 +1467,48 @@ int moe_entropy_pack(const uint16_t *w, size_t n, size_t cap_words, void *out, s
   return MOE_OK;
 }
 
+int moe_probe_h2d_copy(const void *host_src, void *dev_dst, size_t bytes, int workgroups, int reps, void *stream,
+                       double *gbps) {
+  if (!host_src || !dev_dst || !gbps) return fail(MOE_ERR_ARG, "NULL pointer");
+  if (misaligned(host_src, 16) || misaligned(dev_dst, 16) || bytes < 16 || bytes % 16)
+    return fail(MOE_ERR_ARG, "buffers must be 16-byte aligned and bytes a positive multiple of 16");
+  if (workgroups < 1 || workgroups > 4096) return fail(MOE_ERR_ARG, "workgroups must be in [1, 4096]");
+  if (reps < 1 || reps > 1000) return fail(MOE_ERR_ARG, "reps must be in [1, 1000]");
+  void *src = nullptr;
+  hipError_t he = hipHostGetDevicePointer(&src, const_cast<void *>(host_src), 0);
+  if (he != hipSuccess || !src) {
+    (void)hipGetLastError();
+    return fail(MOE_ERR_ARG, "host_src is not pinned host memory mapped for the device (%s)", hipGetErrorString(he));
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float ms = 0.0f;
+  int rc = time_launches(s, reps, [&] { return launch_h2d_copy_probe(src, dev_dst, bytes, workgroups, s); },
+                         "host-to-device copy probe", &ms);
+  if (rc != MOE_OK) return rc;
+  *gbps = ms > 0.0f ? (double)bytes * reps / (ms * 1e-3) / 1e9 : 0.0;
+  return MOE_OK;
+}
+
+int moe_probe_mfma_bf16(int shape, int iters, void *stream, double *tflops) {
+  if (!tflops) return fail(MOE_ERR_ARG, "NULL pointer");
+  if (shape != 0 && shape != 1) return fail(MOE_ERR_ARG, "shape must be 0 (16x16x32) or 1 (32x32x16)");
+  if (iters < 1 || iters > (1 << 20)) return fail(MOE_ERR_ARG, "iters must be in [1, 2^20]");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0, cus = 0;
+  HIP_TRY0(hipGetDevice(&dev));
+  HIP_TRY0(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+  const int wgs = 8 * cus;  // 32 waves per compute unit, 8 per SIMD
+  double flop = 0.0;
+  float ms = 0.0f;
+  int rc = time_launches(s, 1, [&] {
+    flop = launch_mfma_bf16_probe(shape, wgs, iters, s);
+    return hipGetLastError();
+  }, "MFMA probe", &ms);
+  if (rc != MOE_OK) return rc;
+  *tflops = ms > 0.0f ? flop / (ms * 1e-3) / 1e12 : 0.0;
+  return MOE_OK;
+}
+
 int moe_probe_hbm_read(const void *buf, size_t bytes, int reps, void *stream, double *gbps) {
   if (!buf || !gbps) return fail(MOE_ERR_ARG, "NULL pointer");
   if (misaligned(buf, 16) || bytes < 16 || bytes % 16)
@@ -1374,22 +1518,9 @@ int moe_probe_hbm_read(const void *buf, size_t bytes, int reps, void *stream, do
   int dev = 0, cus = 0;
   HIP_TRY0(hipGetDevice(&dev));
   HIP_TRY0(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
-  hipEvent_t a = nullptr, b = nullptr;
-  HIP_TRY0(hipEventCreate(&a));
-  hipError_t e = hipEventCreate(&b);
-  if (e == hipSuccess) e = launch_hbm_read_probe(buf, bytes, cus, s);  // warm-up
-  if (e == hipSuccess) e = hipEventRecord(a, s);
-  for (int r = 0; r < reps && e == hipSuccess; ++r) e = launch_hbm_read_probe(buf, bytes, cus, s);
-  if (e == hipSuccess) e = hipEventRecord(b, s);
-  if (e == hipSuccess) e = hipEventSynchronize(b);
   float ms = 0.0f;
-  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
-  (void)hipEventDestroy(a);
-  if (b) (void)hipEventDestroy(b);
-  if (e != hipSuccess) {
-    (void)hipGetLastError();
-    return fail(MOE_ERR_HIP, "HBM read probe failed: %s", hipGetErrorString(e));
-  }
+  int rc = time_launches(s, reps, [&] { return launch_hbm_read_probe(buf, bytes, cus, s); }, "HBM read probe", &ms);
+  if (rc != MOE_OK) return rc;
   *gbps = ms > 0.0f ? (double)bytes * reps / (ms * 1e-3) / 1e9 : 0.0;
   return MOE_OK;
 }

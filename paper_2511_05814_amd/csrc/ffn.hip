@@ -155,8 +155,6 @@ __global__ __launch_bounds__(kThreads) void ffn_up_kernel(FfnArgs a) {
   const int rank = blockIdx.x / bpr;
   const int rb = blockIdx.x - rank * bpr;
   if (rank >= a.route->k) return;
-  const int hit = a.route->hit[rank];
-  if ((a.phase == 1 && !hit) || (a.phase == 2 && hit)) return;
   const int slot = a.route->slot[rank];
   if (slot < 0 || slot >= a.S) return;
   const int d = a.d, d_ff = a.d_ff;
@@ -202,8 +200,6 @@ __global__ __launch_bounds__(kThreads) void ffn_up_lds_kernel(FfnArgs a) {
   const int rank = blockIdx.x / bpr;
   const int rb = blockIdx.x - rank * bpr;
   if (rank >= a.route->k) return;
-  const int hit = a.route->hit[rank];
-  if ((a.phase == 1 && !hit) || (a.phase == 2 && hit)) return;
   const int slot = a.route->slot[rank];
   if (slot < 0 || slot >= a.S) return;
 

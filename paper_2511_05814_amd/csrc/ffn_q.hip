@@ -135,8 +135,6 @@ __global__ __launch_bounds__(kThreads) void ffnq_up_kernel(FfnArgs a, int G) {
   const int rank = blockIdx.x / G;
   const int gb = blockIdx.x - rank * G;
   if (rank >= a.route->k) return;
-  const int hit = a.route->hit[rank];
-  if ((a.phase == 1 && !hit) || (a.phase == 2 && hit)) return;
   const int slot = a.route->slot[rank];
   if (slot < 0 || slot >= a.S) return;
   const int d = a.d, d_ff = a.d_ff;

@@ -38,7 +38,81 @@ __global__ __launch_bounds__(kProbeThreads) void hbm_read_probe_kernel(const u32
   if (sink) out[tid] = acc;
 }
 
+// Host-to-device shader copy: the fetch kernel's access pattern (16-byte
+// loads from mapped pinned host memory, four in flight a lane, grid-stride)
+// over one buffer, so the host link's ceiling for a copy kernel is measured
+// the same way as the runtime's DMA copy.
+__global__ __launch_bounds__(kProbeThreads) void h2d_copy_probe_kernel(const uint4 *__restrict__ src,
+                                                                       uint4 *__restrict__ dst, size_t nv) {
+  const size_t stride = (size_t)gridDim.x * kProbeThreads;
+  size_t j = (size_t)blockIdx.x * kProbeThreads + threadIdx.x;
+  for (; j + 3 * stride < nv; j += 4 * stride) {
+    const uint4 a = src[j], b = src[j + stride], c = src[j + 2 * stride], d = src[j + 3 * stride];
+    dst[j] = a;
+    dst[j + stride] = b;
+    dst[j + 2 * stride] = c;
+    dst[j + 3 * stride] = d;
+  }
+  for (; j < nv; j += stride) dst[j] = src[j];
+}
+
+// Matrix-core issue rate: every wave keeps `kChains` independent bf16 MFMA
+// accumulations going on register operands, with no memory traffic, so the
+// kernel is bound by the matrix cores alone.  SHAPE 0: v_mfma_f32_16x16x32_bf16
+// (the prefill GEMMs' instruction, 16384 flop), 1: v_mfma_f32_32x32x16_bf16
+// (32768 flop).  sink is 0 on every launch; its store keeps the results live.
+typedef __bf16 probe_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float probe_f32x4 __attribute__((ext_vector_type(4)));
+typedef float probe_f32x16 __attribute__((ext_vector_type(16)));
+constexpr int kChains = 4;
+
+template <int SHAPE>
+__global__ __launch_bounds__(kProbeThreads) void mfma_bf16_probe_kernel(int iters, int sink, float *out) {
+  probe_bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(float)((threadIdx.x + i) & 7);
+    b[i] = (__bf16)(float)((threadIdx.x * 3 + i) & 7);
+  }
+  float total = 0.0f;
+  if constexpr (SHAPE == 0) {
+    probe_f32x4 c[kChains] = {};
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int k = 0; k < kChains; ++k) c[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c[k], 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kChains; ++k) total += c[k][0] + c[k][3];
+  } else {
+    probe_f32x16 c[kChains] = {};
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int k = 0; k < kChains; ++k) c[k] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c[k], 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kChains; ++k) total += c[k][0] + c[k][15];
+  }
+  if (sink) out[(size_t)blockIdx.x * kProbeThreads + threadIdx.x] = total;
+}
+
 }  // namespace
+
+hipError_t launch_h2d_copy_probe(const void *src_dev, void *dst, size_t bytes, int workgroups, hipStream_t s) {
+  hipLaunchKernelGGL(h2d_copy_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, s,
+                     static_cast<const uint4 *>(src_dev), static_cast<uint4 *>(dst), bytes / 16);
+  return hipGetLastError();
+}
+
+double launch_mfma_bf16_probe(int shape, int workgroups, int iters, hipStream_t s) {
+  if (shape == 0)
+    hipLaunchKernelGGL(mfma_bf16_probe_kernel<0>, dim3(workgroups), dim3(kProbeThreads), 0, s, iters, 0,
+                       static_cast<float *>(nullptr));
+  else
+    hipLaunchKernelGGL(mfma_bf16_probe_kernel<1>, dim3(workgroups), dim3(kProbeThreads), 0, s, iters, 0,
+                       static_cast<float *>(nullptr));
+  const double per_inst = shape == 0 ? 2.0 * 16 * 16 * 32 : 2.0 * 32 * 32 * 16;
+  return per_inst * kChains * iters * (double)workgroups * (kProbeThreads / kWave);
+}
 
 hipError_t launch_hbm_read_probe(const void *buf, size_t bytes, int workgroups, hipStream_t s) {
   hipLaunchKernelGGL(hbm_read_probe_kernel, dim3(workgroups), dim3(kProbeThreads), 0, s,

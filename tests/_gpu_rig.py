@@ -10,10 +10,26 @@ def _say(*a):
     print("[gpu-test]", *a, flush=True)
 
 
+# The layer-output bounds the specification states (relative L2 against the
+# fp64 oracle): 2e-2 for bf16 experts, 1e-5 for fp32 experts.  Group-quantised
+# experts dequantise to exact fp32 numbers on both sides, so they take 1e-5.
+SPEC_TOL = {"bf16": 2e-2, "f32": 1e-5, "q2g16": 1e-5}
+# What the kernels are held to, well inside that ceiling, so that a dropped or
+# mis-weighted rank (a combine weight of 0.01 among eight is a 1e-2 error)
+# cannot pass: decode keeps fp32 activations and accumulates in fp32 on
+# weights that are exact in fp32 (measured about 1e-6); the batch path rounds
+# its activations to bf16 for the matrix cores (measured about 3e-3).
+DECODE_TOL = 1e-4
+BATCH_TOL = 6e-3
+
+
 def _tol(cfg):
-    # fp32 and group-quantised weights are exact fp32 numbers on both sides;
-    # bf16 uses the bound stated for bf16 experts
-    return 2e-2 if cfg.dtype == "bf16" else 1e-5
+    """Decode bound for this weight type (never above the stated ceiling)."""
+    return min(SPEC_TOL[cfg.dtype], DECODE_TOL)
+
+
+def _batch_tol(cfg):
+    return min(SPEC_TOL[cfg.dtype], BATCH_TOL)
 
 
 class Rig:

@@ -21,8 +21,9 @@ def rel_l2(a, b):
 
 
 def check_decode(cfg, model, hs, gpu_recs, slots, policy, prefetch=False, pmax=0,
-                 y_tokens=None, tol=1e-5, caches=None):
-    """Returns (worst relative L2 of y, uncertified decisions, oracle caches)."""
+                 y_tokens=None, tol=1e-5, caches=None, records_out=None):
+    """Returns (worst relative L2 of y, uncertified decisions, oracle caches);
+    the oracle's records are appended to records_out when it is a list."""
     L, K = cfg.layers, cfg.top_k
     gpu_ids = {}
     gpu_guess = {}
@@ -56,6 +57,8 @@ def check_decode(cfg, model, hs, gpu_recs, slots, policy, prefetch=False, pmax=0
                 want += caches[l + 1].prefetch(g, pmax)
             if with_ffn:
                 worst = max(worst, rel_l2(hs[t, l + 1] - hs[t, l], st["y"]))
+    if records_out is not None:
+        records_out.extend(want)
     got = [tuple(int(v) for v in r) for r in gpu_recs]
     exp = [w.astuple() for w in want]
     if got != exp:
@@ -65,3 +68,18 @@ def check_decode(cfg, model, hs, gpu_recs, slots, policy, prefetch=False, pmax=0
         raise AssertionError(f"trace length differs: gpu {len(got)} oracle {len(exp)}")
     assert worst <= tol, f"y relative L2 {worst:.3e} > {tol:.1e}"
     return worst, unc, caches
+
+
+def check_y_by_layer(model, hs, layers, k, tol):
+    """y = h_{l+1} - h_l of every token at each of `layers` against the fp64
+    oracle (teacher-forced from the device's h_l).  `model` keeps widened
+    experts; they are dropped after each layer, so a layer's experts are
+    widened once however many tokens use them.  Returns the worst relative L2."""
+    worst = 0.0
+    for l in layers:
+        for t in range(hs.shape[0]):
+            st = stack.layer_step(model, l, hs[t, l], k)
+            worst = max(worst, rel_l2(hs[t, l + 1] - hs[t, l], st["y"]))
+        model.forget()
+    assert worst <= tol, f"y relative L2 {worst:.3e} > {tol:.1e}"
+    return worst

@@ -85,6 +85,18 @@ int main(void) {
     CHECK(moe_probe_hbm_read(buf + 4, 48, 1, NULL, &g) == MOE_ERR_ARG); /* misaligned */
     CHECK(moe_probe_hbm_read(buf, 40, 1, NULL, &g) == MOE_ERR_ARG);     /* not a multiple of 16 */
     CHECK(moe_probe_hbm_read(buf, 64, 0, NULL, &g) == MOE_ERR_ARG);     /* reps */
+    /* host-to-device copy and MFMA probes: the same */
+    CHECK(moe_probe_h2d_copy(NULL, buf, 64, 64, 1, NULL, &g) == MOE_ERR_ARG);
+    CHECK(moe_probe_h2d_copy(buf, NULL, 64, 64, 1, NULL, &g) == MOE_ERR_ARG);
+    CHECK(moe_probe_h2d_copy(buf, buf, 64, 64, 1, NULL, NULL) == MOE_ERR_ARG);
+    CHECK(moe_probe_h2d_copy(buf + 4, buf, 48, 64, 1, NULL, &g) == MOE_ERR_ARG);
+    CHECK(moe_probe_h2d_copy(buf, buf, 40, 64, 1, NULL, &g) == MOE_ERR_ARG);
+    CHECK(moe_probe_h2d_copy(buf, buf, 64, 0, 1, NULL, &g) == MOE_ERR_ARG);    /* workgroups */
+    CHECK(moe_probe_h2d_copy(buf, buf, 64, 5000, 1, NULL, &g) == MOE_ERR_ARG);
+    CHECK(moe_probe_h2d_copy(buf, buf, 64, 64, 0, NULL, &g) == MOE_ERR_ARG);   /* reps */
+    CHECK(moe_probe_mfma_bf16(2, 16, NULL, &g) == MOE_ERR_ARG);                /* shape */
+    CHECK(moe_probe_mfma_bf16(0, 0, NULL, &g) == MOE_ERR_ARG);                 /* iters */
+    CHECK(moe_probe_mfma_bf16(0, 16, NULL, NULL) == MOE_ERR_ARG);
   }
   if (fails == 0) printf("ok\n");
   return fails != 0;

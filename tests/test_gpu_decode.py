@@ -2,8 +2,9 @@
 
 Every test drives the HIP library through the C ABI (binding -> offload) and
 compares, teacher-forced, with the oracle: routing, next-layer guesses and the
-cache trace bit for bit, layer outputs within 1e-5 (fp32 weights) or 2e-2
-(bf16 weights) relative L2.
+cache trace bit for bit, layer outputs within 1e-5 (fp32 weights) or 1e-4
+(bf16 weights, inside the 2e-2 stated for them: decode keeps fp32
+activations) relative L2.
 """
 import numpy as np
 import pytest

@@ -3,8 +3,9 @@
 Per layer: the routing of every row must equal the oracle's fp64 routing
 wherever certified, the per-expert prefill records and the final tables must
 match the oracle's batch rule exactly, and sampled rows' outputs must match
-the fp64 SwiGLU within 2e-2 relative L2 (bf16 weights; the grouped GEMMs take
-bf16 inputs).  Decode then continues from the prefilled caches and is checked
+the fp64 SwiGLU within the batch path's bound (6e-3 relative L2, inside the
+2e-2 stated for bf16 experts; the grouped GEMMs take bf16 activations).
+Decode then continues from the prefilled caches and is checked
 teacher-forced like any decode run.
 """
 import numpy as np
@@ -15,7 +16,7 @@ from oracle import stack
 from oracle.cache import make_caches
 from paper_2511_05814_amd import binding as b
 from paper_2511_05814_amd import workload as wl
-from tests._gpu_rig import Rig, _say
+from tests._gpu_rig import Rig, _batch_tol, _say, _tol
 from tests._parity import check_decode, rel_l2
 
 pytestmark = pytest.mark.gpu
@@ -23,8 +24,9 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 
-def prefill_and_check(rig, moe, policy, slots, T, sample_rows, tol=2e-2):
+def prefill_and_check(rig, moe, policy, slots, T, sample_rows, tol=None):
     cfg = rig.cfg
+    tol = _batch_tol(cfg) if tol is None else tol
     K, L = cfg.top_k, cfg.layers
     h = wl.hidden_states(cfg, T + cfg.tokens)
     H = torch.from_numpy(np.ascontiguousarray(h[:T])).to("cuda")
@@ -66,7 +68,7 @@ def test_prefill_fine_grained_two_layers(policy):
     _say("prefill fine-grained", policy, cfg)
     rig = Rig(cfg)
     moe = rig.cache(16, policy, prefetch_max=2, max_prefill_tokens=300)
-    h, caches, worst, unc = prefill_and_check(rig, moe, policy, 16, 300, [0, 1, 63, 64, 150, 299])
+    h, caches, worst, unc = prefill_and_check(rig, moe, policy, 16, 300, list(range(0, 300, 7)) + [299])
     _say("prefill worst y", worst, "uncertified", unc)
     # decode continues from the prefilled caches
     hs = []
@@ -77,7 +79,7 @@ def test_prefill_fine_grained_two_layers(policy):
     recs, _ = moe.trace_records()
     dec = [r for r in recs if r[0] != 2]
     check_decode(cfg, rig.model, snaps.cpu().numpy().astype(np.float64), dec, 16, policy,
-                 prefetch=True, pmax=2, y_tokens=[0, 9], tol=2e-2, caches=caches)
+                 prefetch=True, pmax=2, tol=_tol(cfg), caches=caches)
     st = moe.stats()
     for l in range(cfg.layers):
         assert st[l]["lookups"] == 300 + cfg.tokens
@@ -178,6 +180,6 @@ def test_batched_decode_mixtral_shape(slots):
             worst = max(worst, rel_l2(hout[t] - hin[t], y))
         assert moe.state(0) == caches[0].state()
     _say("batched decode worst y", worst)
-    assert worst <= 2e-2
+    assert worst <= _batch_tol(cfg)
     moe.close()
     rig.store.close()

@@ -259,6 +259,148 @@ def test_guess_precision_equals_recall_and_sec54_value():
     assert float(prec) == float(rec)
 
 
+# Hand-worked guesses for three layers and three tokens (E = 4, K = 2).  Layer
+# 0 has activations only (nothing guesses it).  Per (layer, token):
+#   activations  L0: {0,1} {0,2} {1,3}   L1: {2,3} {2,0} {1,0}   L2: {0,3} {1,2} {3,2}
+#   guesses                              L1: {2,3} {2,1} {0,1}   L2: {0,1} {1,2} {3,0}
+#   true pos.                            L1:   2     1     2     L2:   1     2     1
+# so TP = 9 of 12 guesses and 12 activations: P = R = 3/4 (Sec. 5.4).
+_HAND_ACT = {0: [[0, 1], [0, 2], [1, 3]], 1: [[2, 3], [2, 0], [1, 0]], 2: [[0, 3], [1, 2], [3, 2]]}
+_HAND_GUESS = {1: [[2, 3], [2, 1], [0, 1]], 2: [[0, 1], [1, 2], [3, 0]]}
+
+
+def _hand_records(guess_layer_shift=0, guess_token_shift=0):
+    recs = []
+    for l, rows in _HAND_ACT.items():
+        for t, ids in enumerate(rows):
+            recs += [Rec(KIND_ACCESS, t, l, r, e, 0, -1, -1) for r, e in enumerate(ids)]
+    for l, rows in _HAND_GUESS.items():
+        for t, ids in enumerate(rows):
+            recs += [Rec(KIND_PREFETCH, t + guess_token_shift, l + guess_layer_shift, r, e, 0, -1, -1)
+                     for r, e in enumerate(ids)]
+    return recs
+
+
+def test_guess_pr_hand_worked_three_layers_three_tokens():
+    assert metrics.guess_pr(_hand_records()) == (0.75, 0.75, 9, 12, 12)
+    # a guess belongs to the guessed layer and the same token: keyed one token
+    # late, L1 t0 {2,3} meets t1 {2,0} (1), L1 t1 meets t2 (1), L2 t0 {0,1}
+    # meets {1,2} (1), L2 t1 {1,2} meets {3,2} (1); the t2 guesses find no
+    # activations: 4 of 8
+    assert metrics.guess_pr(_hand_records(guess_token_shift=1)) == (0.5, 0.5, 4, 8, 8)
+    # keyed to the layer that made the guess (l - 1): L1's guesses against
+    # L0's activations give 0 + 1 + 1, L2's against L1's 0 + 1 + 1: 4 of 12
+    p, r, tp, ng, na = metrics.guess_pr(_hand_records(guess_layer_shift=-1))
+    assert (tp, ng, na) == (4, 12, 12) and p == r == pytest.approx(1 / 3)
+    # perfect guesses (guess = the same token's activations at that layer)
+    perfect = [Rec(KIND_PREFETCH, t, l, r, e, 0, -1, -1)
+               for l in (1, 2) for t, ids in enumerate(_HAND_ACT[l]) for r, e in enumerate(ids)]
+    acts = [x for x in _hand_records() if x.kind == KIND_ACCESS]
+    assert metrics.guess_pr(acts + perfect) == (1.0, 1.0, 12, 12, 12)
+    # the product's analytics give the same numbers on the same records
+    from paper_2511_05814_amd import analysis
+    for shift, want in (({}, 0.75), ({"guess_token_shift": 1}, 0.5)):
+        tup = [x.astuple() for x in _hand_records(**shift)]
+        assert analysis.guess_precision_recall(tup) == (want, want)
+
+
+def test_transfer_precision_hand_worked_lfu():
+    # One layer's cache (layer 1), E = 5, S = 3, K = 2, LFU, warm start
+    # slots [0, 1, 2], last = -3, -2, -1 (experts 3 and 4: -4).  Keys
+    # (count, last, slot); prefetches tick the clock but leave counts alone.
+    c = LayerCache(5, 3, "lfu", layer=1)
+    recs = []
+    # token 0: guesses [3, 0] (max 2).  3 is fetched at tick 1 into slot 1,
+    # evicting 1 (key (0,-2,1) < (0,-1,2); 0 is pinned as a guess); 0 is resident.
+    recs += c.prefetch([3, 0], 2)
+    # access [3, 4]: 3 hits and is the prefetch's first use (useful); 4 misses
+    # at tick 3 and evicts 0 (slot 0, key (0,-3,0)).
+    recs += c.access([3, 4])
+    # token 1: guesses [1, 0] (max 2).  1 at tick 4 evicts 2 (count 0) from slot
+    # 2; 0 at tick 5 evicts 3 (key (1,2,1) < 4's (1,3,0)) from slot 1.
+    recs += c.prefetch([1, 0], 2)
+    # access [0, 2]: 0 hits (useful); 2 misses at tick 7 and evicts the
+    # prefetched, never used 1 (count 0): wasted before its use.
+    recs += c.access([0, 2])
+    # token 2: guesses [3, 1] (max 1).  3 at tick 8 evicts 4 (key (1,3,0));
+    # 1 is not fetched (cap reached).
+    recs += c.prefetch([3, 1], 1)
+    # access [1, 0]: 1 misses at tick 9 and evicts 2 (key (1,7,2) before 3's
+    # (1,8,0)); 0 hits; the prefetched 3 was never used: wasted.
+    recs += c.access([1, 0])
+    assert [r.astuple() for r in recs] == [
+        (1, 0, 1, 0, 3, 2, 1, 1), (1, 0, 1, 1, 0, 1, 0, -1),
+        (0, 0, 1, 0, 3, 3, 1, -1), (0, 0, 1, 1, 4, 0, 0, 0),
+        (1, 1, 1, 0, 1, 2, 2, 2), (1, 1, 1, 1, 0, 2, 1, 3),
+        (0, 1, 1, 0, 0, 3, 1, -1), (0, 1, 1, 1, 2, 0, 2, 1),
+        (1, 2, 1, 0, 3, 2, 0, 4), (1, 2, 1, 1, 1, 0, -1, -1),
+        (0, 2, 1, 0, 1, 0, 2, 2), (0, 2, 1, 1, 0, 1, 1, -1),
+    ]
+    s = c.stats
+    assert (s.pf_guesses, s.pf_issued, s.pf_useful, s.pf_wasted) == (6, 4, 2, 2)
+    assert metrics.transfer_precision(recs) == 0.5          # 2 useful of 4 issued
+    # guesses {3,0} {1,0} {3,1} against activations {3,4} {0,2} {1,0}: 1 + 1 + 1
+    assert metrics.guess_pr(recs) == (0.5, 0.5, 3, 6, 6)
+    from paper_2511_05814_amd import analysis
+    tup = [r.astuple() for r in recs]
+    assert analysis.transfer_precision(tup) == 0.5
+    assert analysis.guess_precision_recall(tup) == (0.5, 0.5)
+    # with perfect guesses every fetched guess is used: transfer precision 1
+    c = LayerCache(5, 3, "lfu", layer=1)
+    recs = []
+    for ids in ([3, 4], [0, 2], [1, 0]):
+        recs += c.prefetch(ids, 2) + c.access(ids)
+    assert c.stats.pf_issued == 4 and c.stats.pf_wasted == 0
+    assert metrics.transfer_precision(recs) == 1.0
+    assert metrics.guess_pr(recs)[:2] == (1.0, 1.0)
+
+
+def test_cache_pr_reproduces_table2_pairs():
+    # a run of 1000 lookups of K = 2 with 1164 (LRU) or 1196 (LFU) hits and 4
+    # slots gives exactly Table 2's printed cache precision / recall
+    for _, prec, rec in _read_golden("table2_cache_precision_recall.txt"):
+        hits = round(float(rec) * 20)
+        recs = [Rec(KIND_ACCESS, t, 0, r, r, F_HIT if 2 * t + r < hits else 0, r, -1)
+                for t in range(1000) for r in range(2)]
+        p, r = metrics.cache_pr(recs, 4)
+        assert (round(100 * p, 1), round(100 * r, 1)) == (float(prec), float(rec))
+
+
+def test_histogram_and_repeat_rates_hand_worked():
+    # layer 0, four lookups: [1, 2] [2, 3] [2, 3] [5, 6]; layer 1 is noise
+    rows = [[1, 2], [2, 3], [2, 3], [5, 6]]
+    recs = [Rec(KIND_ACCESS, t, 0, r, e, 0, -1, -1) for t, ids in enumerate(rows) for r, e in enumerate(ids)]
+    recs += [Rec(KIND_ACCESS, t, 1, r, (e + 3) % 8, 0, -1, -1) for t, ids in enumerate(rows)
+             for r, e in enumerate(ids)]
+    assert metrics.activation_histogram(recs, 0, 8) == [0, 1, 3, 2, 0, 1, 1, 0]
+    # token 1 repeats 2 (1 of 2), token 2 repeats 2 and 3 (2 of 2), token 3 none
+    assert metrics.repeat_rate(recs, 0) == 3 / 6
+    # first-ranked experts 1, 2, 2, 5: one repeat in three consecutive pairs
+    assert metrics.top1_repeat_rate(recs, 0) == 1 / 3
+    # a gap in the lookup indices breaks the pair
+    gap = [x for x in recs if not (x.layer == 0 and x.token == 1)]
+    assert metrics.top1_repeat_rate(gap, 0) == 0.0 and metrics.repeat_rate(gap, 0) == 0.0
+    from paper_2511_05814_amd import analysis
+    tup = [x.astuple() for x in recs]
+    assert analysis.activation_histogram(tup, 0, 8) == metrics.activation_histogram(recs, 0, 8)
+    assert analysis.repeat_rate(tup, 0) == metrics.repeat_rate(recs, 0)
+    assert analysis.top1_repeat_rate(tup, 0) == metrics.top1_repeat_rate(recs, 0)
+
+
+def test_repeat_rates_of_random_routing_are_k_over_e_and_one_over_e():
+    # Sec. 3.1: with random choices the same expert comes back with
+    # probability 1/E (12.5 % for 8 experts); a top-K set shares K/E of its
+    # experts with the previous one on average
+    rng = np.random.default_rng(24)
+    E, K, T = 8, 2, 40000
+    recs = [Rec(KIND_ACCESS, t, 0, r, int(e), 0, -1, -1)
+            for t in range(T) for r, e in enumerate(rng.choice(E, K, replace=False))]
+    assert metrics.top1_repeat_rate(recs, 0) == pytest.approx(1 / E, abs=0.01)
+    assert metrics.repeat_rate(recs, 0) == pytest.approx(K / E, abs=0.01)
+    (e8, pct), = _read_golden("sec31_random_repeat.txt")
+    assert 100 / int(e8) == pytest.approx(float(pct))
+
+
 def test_random_repeat_probability_sec31():
     (E, pct), = _read_golden("sec31_random_repeat.txt")
     assert 100.0 / int(E) == pytest.approx(float(pct))
