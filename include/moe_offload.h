@@ -222,6 +222,21 @@ int moe_cache_reset(moe_cache_t *c);
  * this h and fetch up to prefetch_max of them (Sec. 3.2).  Enqueue only. */
 int moe_decode_layer(moe_cache_t *c, int layer, float *h, int flags);
 
+/* moe_decode_layer for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, work and results as moe_decode_layer (the
+ * same kernels), but the call's scratch (the FFN's top_k x d_ff activations,
+ * its partial row sums of d_model rows, the router's logits) lives in a
+ * static 4 MiB device array that the library holds on each device until the
+ * process ends, instead of the bound workspace; the call allocates nothing
+ * (no hipMalloc, no event creation).  Every call on one device shares that
+ * array and it keeps the last call's contents (each call writes all of it
+ * that it reads): calls that overlap on one device, from any handle, race.
+ * MOE_ERR_ARG if the model needs more scratch than the array holds (the
+ * message gives the size), MOE_ERR_STATE if kernel timing is on (timed
+ * spans create events); otherwise as moe_decode_layer.  Enqueue only. */
+int moe_decode_layer_noalloc(moe_cache_t *c, int layer, float *h, int flags);
+
 /* The speculative part alone (Sec. 3.2, Sec. 4.3: each layer also holds the
  * next layer's gate, and that gate applied to the current hidden state,
  * followed by softmax and top-K, guesses the next layer's experts): guess

@@ -91,6 +91,7 @@ _SIGNATURES = [
     ("moe_cache_bind", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(moe_model_desc)]),
     ("moe_cache_reset", ctypes.c_int, [ctypes.c_void_p]),
     ("moe_decode_layer", ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int]),
+    ("moe_decode_layer_noalloc", ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int]),
     ("moe_prefetch", ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int]),
     ("moe_prefill_layer", ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int]),
     ("moe_cache_access", ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]),
@@ -170,6 +171,10 @@ def moe_cache_reset(cache: int) -> None:
 
 def moe_decode_layer(cache: int, layer: int, h: int, flags: int = 0) -> None:
     _check(lib().moe_decode_layer(cache, layer, h, flags), "moe_decode_layer")
+
+
+def moe_decode_layer_noalloc(cache: int, layer: int, h: int, flags: int = 0) -> None:
+    _check(lib().moe_decode_layer_noalloc(cache, layer, h, flags), "moe_decode_layer_noalloc")
 
 
 def moe_prefetch(cache: int, next_layer: int, h: int, max_experts: int) -> None:

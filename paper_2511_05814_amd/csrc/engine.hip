@@ -126,6 +126,34 @@ void pool_give_back(int dev, const std::vector<hipEvent_t> &sync_ev, const std::
     if (b.second) pl.pinned.emplace(b.first, b.second);
 }
 
+// Scratch of moe_decode_layer_noalloc: the decode FFN's activations
+// [K][d_ff] and partial row sums [chunks][d], and the router's logits of a
+// separate GEMV launch, in device memory the library holds for the life of
+// the process (one copy per device).  Host code never uses the array's name
+// as an address: each device's address comes from hipGetSymbolAddress.
+constexpr size_t kNoAllocScratchBytes = size_t(4) << 20;
+}  // namespace
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+namespace {
+std::mutex g_scratch_mu;
+std::map<int, uint8_t *> g_scratch_ptr;  // by device
+
+// The current device's copy of `scratch` (resolved once per device).
+hipError_t scratch_on_device(int dev, uint8_t **out) {
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  auto it = g_scratch_ptr.find(dev);
+  if (it != g_scratch_ptr.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  void *p = nullptr;
+  hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || p == nullptr) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+  g_scratch_ptr[dev] = static_cast<uint8_t *>(p);
+  *out = static_cast<uint8_t *>(p);
+  return hipSuccess;
+}
+
 }  // namespace
 
 namespace moe {
@@ -208,6 +236,7 @@ struct moe_cache {
   std::vector<uint8_t> demand_pending, pf_pending;
   int sticky = MOE_OK;
   int dev = 0;                  // device the handle was bound on (owner of its pooled objects)
+  uint8_t *scratch = nullptr;   // that device's static scratch (moe_decode_layer_noalloc)
   FetchList *mirror = nullptr;  // pinned host: demand list, prefetch list, error word (DMA / split modes)
   size_t mirror_bytes = 0, plan_bytes = 0, sched_bytes = 0;  // sizes of the pooled pinned buffers
   int last_route_kind = 0;      // 0 none, 1 decode, 2 prefill
@@ -525,6 +554,7 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   // runtime objects come from the process pool (released there by destroy,
   // also when bind fails half way)
   HIP_TRY0(hipGetDevice(&c->dev));
+  HIP_TRY0(scratch_on_device(c->dev, &c->scratch));
   c->ev_demand.assign(c->L, nullptr);
   c->ev_pf.assign(c->L, nullptr);
   c->demand_pending.assign(c->L, 0);
@@ -679,8 +709,18 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
 }
 
 // Router (+ fetches, + FFN) for one call.  spec_layer < 0: no speculation.
+// Scratch of one call: FFN activations and partial sums, router logits.
+struct CallScratch {
+  float *act, *part;
+  double *zbuf;
+};
+
+static CallScratch workspace_scratch(moe_cache *c) {
+  return {c->act, c->part, reinterpret_cast<double *>(c->ws + c->lay.rz)};
+}
+
 static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, int demand,
-                         int spec_layer, int pmax, bool ffn) {
+                         int spec_layer, int pmax, bool ffn, const CallScratch &scr) {
   if (!c->one_stream) {
     if (demand && c->demand_pending[layer]) HIP_TRY(c, hipStreamWaitEvent(c->cs, c->ev_demand[layer], 0));
     if (spec_layer >= 0 && c->pf_pending[spec_layer])
@@ -712,7 +752,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.demand = demand;
   a.spec_layer = spec_layer;
   a.pmax = pmax;
-  a.zbuf = reinterpret_cast<double *>(c->ws + c->lay.rz);
+  a.zbuf = scr.zbuf;
   Launch lr;
   HIP_TRY(c, kernel_span(c, c->cs, &lr, SPAN_ROUTER));
   HIP_TRY(c, launch_router(a, lr));
@@ -783,8 +823,8 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     f.arena = static_cast<const uint8_t *>(c->desc.arena);
     f.route = c->route;
     f.h = h;
-    f.act = c->act;
-    f.part = c->part;
+    f.act = scr.act;
+    f.part = scr.part;
     f.expert_bytes = c->B;
     f.layer = layer;
     f.S = c->S;
@@ -1230,7 +1270,31 @@ int moe_decode_layer(moe_cache_t *c, int layer, float *h, int flags) {
   if (!h || misaligned(h, 16)) return fail(MOE_ERR_ARG, "h must be a non-NULL 16-byte aligned device pointer");
   if (flags & ~MOE_PREFETCH_NEXT) return fail(MOE_ERR_ARG, "unknown flags 0x%x", flags);
   const int spec = (flags & MOE_PREFETCH_NEXT) && layer + 1 < c->L ? layer + 1 : -1;
-  return enqueue_layer(c, layer, h, nullptr, 1, spec, c->pmax, true);
+  return enqueue_layer(c, layer, h, nullptr, 1, spec, c->pmax, true, workspace_scratch(c));
+}
+
+int moe_decode_layer_noalloc(moe_cache_t *c, int layer, float *h, int flags) {
+  if (!c) return fail(MOE_ERR_ARG, "NULL handle");
+  if (!c->bound || !c->scratch) return fail(MOE_ERR_STATE, "handle is not bound (call moe_cache_bind)");
+  const size_t act_bytes = align_up(sizeof(float) * (size_t)c->K * c->dff, 256);
+  const size_t part_bytes = align_up(sizeof(float) * (size_t)ffn_down_chunks(c->K, c->dff, c->dtype) * c->d, 256);
+  const size_t z_bytes = sizeof(double) * 2 * kMaxE;
+  if (act_bytes + part_bytes + z_bytes > kNoAllocScratchBytes)
+    return fail(MOE_ERR_ARG,
+                "this model needs %zu bytes of decode scratch (top_k * d_ff activations, partial sums of d_model "
+                "rows); the static scratch of moe_decode_layer_noalloc holds %zu: use moe_decode_layer",
+                act_bytes + part_bytes + z_bytes, kNoAllocScratchBytes);
+  int rc = check_ready(c);
+  if (rc != MOE_OK) return rc;
+  if (c->timing != MOE_TIMING_OFF)
+    return fail(MOE_ERR_STATE, "kernel timing creates events; turn it off (moe_cache_set_timing) for this call");
+  if (layer < 0 || layer >= c->L) return fail(MOE_ERR_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (!h || misaligned(h, 16)) return fail(MOE_ERR_ARG, "h must be a non-NULL 16-byte aligned device pointer");
+  if (flags & ~MOE_PREFETCH_NEXT) return fail(MOE_ERR_ARG, "unknown flags 0x%x", flags);
+  const int spec = (flags & MOE_PREFETCH_NEXT) && layer + 1 < c->L ? layer + 1 : -1;
+  const CallScratch scr{reinterpret_cast<float *>(c->scratch), reinterpret_cast<float *>(c->scratch + act_bytes),
+                        reinterpret_cast<double *>(c->scratch + act_bytes + part_bytes)};
+  return enqueue_layer(c, layer, h, nullptr, 1, spec, c->pmax, true, scr);
 }
 
 int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts) {
@@ -1240,7 +1304,8 @@ int moe_prefetch(moe_cache_t *c, int next_layer, const float *h, int max_experts
     return fail(MOE_ERR_ARG, "next_layer %d out of range [1, %d)", next_layer, c->L);
   if (!h || misaligned(h, 16)) return fail(MOE_ERR_ARG, "h must be a non-NULL 16-byte aligned device pointer");
   if (max_experts < 0 || max_experts > c->K) return fail(MOE_ERR_ARG, "max_experts must be in [0, top_k]");
-  return enqueue_layer(c, next_layer - 1, const_cast<float *>(h), nullptr, 0, next_layer, max_experts, false);
+  return enqueue_layer(c, next_layer - 1, const_cast<float *>(h), nullptr, 0, next_layer, max_experts, false,
+                       workspace_scratch(c));
 }
 
 int moe_cache_access(moe_cache_t *c, int layer, const int *ids) {
@@ -1248,7 +1313,8 @@ int moe_cache_access(moe_cache_t *c, int layer, const int *ids) {
   if (rc != MOE_OK) return rc;
   if (layer < 0 || layer >= c->L) return fail(MOE_ERR_ARG, "layer %d out of range [0, %d)", layer, c->L);
   if (!ids) return fail(MOE_ERR_ARG, "ids is NULL");
-  return enqueue_layer(c, layer, nullptr, reinterpret_cast<const int32_t *>(ids), 1, -1, 0, false);
+  return enqueue_layer(c, layer, nullptr, reinterpret_cast<const int32_t *>(ids), 1, -1, 0, false,
+                       workspace_scratch(c));
 }
 
 int moe_prefill_layer(moe_cache_t *c, int layer, float *H, int tokens) {

@@ -47,6 +47,8 @@ int main(void) {
 
   memset(h, 0, sizeof h);
   CHECK(moe_decode_layer(c, 0, h, 0) == MOE_ERR_STATE); /* not bound */
+  CHECK(moe_decode_layer_noalloc(c, 0, h, 0) == MOE_ERR_STATE);
+  CHECK(moe_decode_layer_noalloc(NULL, 0, h, 0) == MOE_ERR_ARG);
   CHECK(moe_cache_sync(c) == MOE_ERR_STATE);
 
   moe_cache_destroy(c);
