@@ -196,8 +196,8 @@ hipError_t launch_ffnq_down(const FfnArgs &a, const Launch &l);
 int ffnq_down_chunks(int K, int d_ff);
 hipError_t launch_prefill_gate(const PrefillArgs &a, const Launch &l);
 hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l);
-// grouped GEMMs over tiles of `rows` (64 or 128) sorted pairs by
-// prefill_tile_cols() output columns
+// grouped GEMMs over tiles of `rows` (64, 128 or 256) sorted pairs by
+// prefill_tile_cols(up) output columns
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l);
 // Small-M grouped GEMMs: one tile {job, 0, 0} per expert, each with at most
@@ -213,7 +213,7 @@ hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob 
                                float *Y, int d, int d_ff, int rows, const Launch &l);
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
                                     int d, int K, const Launch &l);
-int prefill_tile_cols();  // GEMM output tile columns (act for up, Y for down)
+int prefill_tile_cols(bool up);  // GEMM output tile columns (act for up, Y for down)
 
 // ---------------------------------------------------------------------------
 // device helpers

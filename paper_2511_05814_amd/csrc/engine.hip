@@ -1010,9 +1010,15 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       }
     }
   }
-  // Output tiles of 128 rows (sorted pairs) by 128 columns; a launch that
-  // would not give every CU two of them takes 64-row tiles instead.
-  const int cols = prefill_tile_cols();
+  // Output tiles of 256, 128 or 64 rows (sorted pairs) by 128 (up) or 256
+  // (down) columns: the
+  // tallest that still gives every CU two tiles (256-row tiles run one
+  // 512-lane workgroup per CU, the others two or three of 256 lanes).  Within
+  // an expert the tiles of one column block are consecutive, so a column
+  // block's weights are read once for all of the expert's row blocks by
+  // workgroups that run at the same time on one XCD (the kernel hands each
+  // XCD a contiguous stretch of this list).
+  const int up_cols = prefill_tile_cols(true), down_cols = prefill_tile_cols(false);
   int cus = 0;
   {
     int dev = 0;
@@ -1023,14 +1029,17 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   }
   int nt = 0;
   bool overflow = false;  // checked before each write: ht is a fixed-size pinned buffer
-  auto add_tiles = [&](const std::vector<int> &group, int ncols, int &first, int &count, int &rows) {
-    long big = 0;
-    for (int e : group) big += (long)((pl[e].n + 127) / 128) * ((ncols + cols - 1) / cols);
-    rows = big < 2L * cus ? 64 : 128;
+  auto add_tiles = [&](const std::vector<int> &group, int ncols, int cols, int &first, int &count, int &rows) {
+    auto tiles_of = [&](int r) {
+      long n = 0;
+      for (int e : group) n += (long)((pl[e].n + r - 1) / r) * ((ncols + cols - 1) / cols);
+      return n;
+    };
+    rows = tiles_of(256) >= 2L * cus ? 256 : (tiles_of(128) >= 2L * cus ? 128 : 64);
     first = nt;
     for (int e : group)
-      for (int m0 = 0; m0 < pl[e].n; m0 += rows)
-        for (int n0 = 0; n0 < ncols; n0 += cols) {
+      for (int n0 = 0; n0 < ncols; n0 += cols)
+        for (int m0 = 0; m0 < pl[e].n; m0 += rows) {
           if (nt >= p.tile_cap) {
             overflow = true;
             continue;
@@ -1063,8 +1072,8 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       }
       up_n[gi] = dn_n[gi] = nt - up_first[gi];
     } else {
-      add_tiles(group, c->dff, up_first[gi], up_n[gi], up_rows[gi]);
-      add_tiles(group, c->d, dn_first[gi], dn_n[gi], dn_rows[gi]);
+      add_tiles(group, c->dff, up_cols, up_first[gi], up_n[gi], up_rows[gi]);
+      add_tiles(group, c->d, down_cols, dn_first[gi], dn_n[gi], dn_rows[gi]);
     }
   };
   add_group(resident, 0);

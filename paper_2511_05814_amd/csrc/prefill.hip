@@ -35,6 +35,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef double double4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kGateTok = 16;     // tokens per gate workgroup
@@ -455,28 +456,43 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
 // 3. grouped GEMMs.  A rows come from the sorted pair order; B = expert
 // weights stored out x in (K contiguous), so both operands are K-major.
 
-// 16-byte chunk c of LDS row r sits at chunk c ^ ((r / 2) % 4) of the row:
-// rows are 64 bytes, so without the swizzle rows r and r + 2 would put the
-// same chunk in the same banks.
-__device__ __forceinline__ int lds_chunk(int row, int c) { return c ^ ((row >> 1) & 3); }
+// An LDS row holds one KS-deep slice of a row (KS = 32 or 64 bf16: 64 or
+// 128 bytes, 16 or 32 of the 64 four-byte banks), so R = 128 / KS
+// consecutive rows cover the banks once.  16-byte chunk c of row r sits at
+// chunk c ^ ((r / R) % (KS / 8)): any 16 consecutive rows read at one chunk
+// (the 16 lanes the LDS serves at once in a 16-byte read) touch all 64 banks
+// once, and so do the 16 lanes of a staging write.  (With c ^ ((r / 2) % 4)
+// on 64-byte rows, rows r and r + 8 collided, and bank conflicts took 37% of
+// the LDS's active cycles in the grouped GEMMs.)
+template <int KS>
+__device__ __forceinline__ int lds_chunk(int row, int c) {
+  return c ^ ((row / (128 / KS)) % (KS / 8));
+}
 
-// One MFMA 16x16x32 operand fragment from a K-major LDS tile: lane i holds
-// row (i % 16), elements (i / 16) * 8 .. + 8 of the 32-deep slice.
-__device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row, int lane) {
-  const uint4 v = *reinterpret_cast<const uint4 *>(&src[row][lds_chunk(row, lane / 16) * 8]);
+// One MFMA 32x32x16 operand fragment for 16-deep part `h` of a K-major LDS
+// tile: lane i holds row (i % 32), elements h * 16 + (i / 32) * 8 .. + 8.
+template <int KS>
+__device__ __forceinline__ bf16x8 lds_frag32(const uint16_t (*src)[KS], int row, int lane, int h) {
+  const uint4 v = *reinterpret_cast<const uint4 *>(&src[row][lds_chunk<KS>(row, 2 * h + lane / 32) * 8]);
   bf16x8 r;
   __builtin_memcpy(&r, &v, sizeof v);
   return r;
 }
 
-// A workgroup takes a BM x 128 output tile (BM = 128, or 64 for launches too
-// small to fill the chip with 128-row tiles), against both W1 and W3 in the
-// up projection and against W2 in the down projection.  Four waves each own
-// (BM / 2) x 64 of it as (BM / 32) x 4 v_mfma_f32_16x16x32_bf16 tiles.  (A
-// 128 x 256 down tile streams W2 no faster in isolation and halves the
-// workgroups of the small per-batch launches.)  The next 32-deep K slice is
-// loaded from global memory into registers kGemmStages slices ahead of the
-// one multiplied out of LDS; LDS is double-buffered so one barrier per step
+// A workgroup takes a BM x BN output tile, against both W1 and W3 in the up
+// projection (BN = 128) and against W2 in the down projection (BN = 256), so
+// both keep the same accumulators and stage the same bytes per step.  BM is
+// 256 (eight waves, one workgroup per CU) for launches with at least two such
+// tiles per CU, else 128 or 64 (four waves, two or three workgroups per CU).
+// The waves form a (waves / 2) x 2 grid; each owns a (BM / (waves / 2)) x
+// (BN / 2) block of the tile, multiplied as 32 x 32 v_mfma_f32_32x32x16_bf16
+// blocks, two per 32-deep slice.  (On MI355X a loop of nothing but 32x32x16
+// bf16 MFMAs issues 2.17 PFLOP/s against 1.31 for the 16x16x32 form, and
+// each 32-row fragment feeds twice the flops per LDS byte.)  A 256 x 128 up
+// tile stages 32 KB per 32-deep slice for 4.2 MFLOP, half the global bytes
+// per flop of a 128 x 128 one.  The next 32-deep K slice is loaded from
+// global memory into registers kGemmStages slices ahead of the one
+// multiplied out of LDS; LDS is double-buffered so one barrier per step
 // suffices.  Every output accumulates its K slices in ascending order.
 //
 // The loads ahead must stay in flight across steps, so none of them is
@@ -491,8 +507,16 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t (*src)[kLdsK], int row
 // The weights are read with buffer loads instead, through a resource over the
 // tile's own rows (uniform base, 32-bit byte offsets, and a record count that
 // bounds every access to those rows).
-constexpr int kBN = 128;
 constexpr int kGemmStages = 2;  // K slices loaded ahead of the one being multiplied
+#ifndef MOE_GEMM_STAGES_TALL
+#define MOE_GEMM_STAGES_TALL 2
+#endif
+#ifndef MOE_GEMM_KS_TALL
+#define MOE_GEMM_KS_TALL 64
+#endif
+// 256-row tiles: slices loaded ahead, and slice depth (bf16 elements)
+constexpr int kGemmStagesTall = MOE_GEMM_STAGES_TALL;
+constexpr int kKsTall = MOE_GEMM_KS_TALL;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const uint16_t *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), 0, bytes, 0x00020000);
@@ -504,50 +528,77 @@ __device__ __forceinline__ gemm_u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, ui
   return __builtin_bit_cast(gemm_u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
 }
 
-template <bool UP, int P, int BM, bool RAGGED>
-__global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_gemm_kernel(
+// Workgroup i runs on XCD i % 8; it takes tile (i % 8) * n / 8 + i / 8 (with
+// the remainder spread over the first XCDs), so each XCD works through one
+// contiguous stretch of the tile list and the tiles it runs at the same time
+// share their A and B panels in that XCD's L2.
+__device__ __forceinline__ int xcd_tile(int b, int n) {
+  constexpr int kXcds = 8;
+  const int x = b % kXcds, i = b / kXcds, per = n / kXcds, rem = n % kXcds;
+  return x * per + min(x, rem) + i;
+}
+
+// Output columns of a tile: 128 against W1 and W3 (the up projection keeps
+// two accumulators per output), 256 against W2, so both hold the same number
+// of accumulators and stage the same bytes per step.
+template <bool UP>
+constexpr int gemm_cols() {
+  return UP ? 128 : 256;
+}
+
+template <bool UP, int P, int BM, int THREADS, int KS, bool RAGGED>
+__global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) void prefill_gemm_kernel(
     const GemmTile *tiles, const GemmJob *jobs, const uint16_t *a_src, const int32_t *perm_tok, void *out, int d,
     int d_ff) {
-  constexpr int NB = UP ? 2 : 1;   // B matrices: W1 and W3, or W2
-  constexpr int HA = BM / 64;      // A rows each thread stages
-  constexpr int MX = BM / 32;      // 16-row MFMA blocks per wave
-  __shared__ uint16_t As[2][BM][kLdsK];
-  __shared__ uint16_t Bs[2][NB][kBN][kLdsK];
-  const GemmTile t = tiles[blockIdx.x];
+  constexpr int NB = UP ? 2 : 1;         // B matrices: W1 and W3, or W2
+  constexpr int BN = gemm_cols<UP>();    // output columns of the tile
+  constexpr int WM = THREADS / kWave / 2;  // waves along M (two along N)
+  constexpr int WR = BM / WM;            // output rows per wave
+  constexpr int WC = BN / 2;             // output columns per wave
+  constexpr int CH = KS / 8;             // 16-byte chunks of a slice row
+  constexpr int SR = THREADS / CH;       // rows one staging pass covers
+  constexpr int HA = BM / SR;            // A rows each thread stages
+  constexpr int HB = BN / SR;            // B rows each thread stages per matrix
+  constexpr int MX = WR / 32;            // 32-row MFMA blocks per wave
+  constexpr int NY = WC / 32;            // 32-column MFMA blocks per wave
+  static_assert(WR % 32 == 0 && BM % SR == 0 && BN % SR == 0, "tile shape");
+  __shared__ uint16_t As[2][BM][KS];
+  __shared__ uint16_t Bs[2][NB][BN][KS];
+  const GemmTile t = tiles[xcd_tile(blockIdx.x, gridDim.x)];
   const GemmJob j = jobs[t.job];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int wm = wave / 2, wn = wave % 2;
   const int K = UP ? d : d_ff;   // reduction length
   const int N = UP ? d_ff : d;   // output columns
   const int ldo = N;
-  // staging: thread -> rows (tid / 4) + 64 h, 16-byte quarter tid % 4
-  const int r0 = tid / 4, q = tid % 4;
+  // staging: thread -> rows (tid / CH) + SR h, 16-byte chunk tid % CH
+  const int r0 = tid / CH, q = tid % CH;
   if (j.nrows <= 0) return;  // no rows: nothing to clamp to (the plan makes no such tiles)
   const uint16_t *ap[HA];
 #pragma unroll
   for (int h = 0; h < HA; ++h) {
-    const int m = min(t.m0 + r0 + 64 * h, j.nrows - 1);
+    const int m = min(t.m0 + r0 + SR * h, j.nrows - 1);
     ap[h] = UP ? a_src + (size_t)perm_tok[j.row0 + m] * d : a_src + (size_t)(j.row0 + m) * d_ff;
   }
-  // weight rows n0 .. n0 + nb - 1 of each B matrix (nb <= 128)
-  const int nb = min(kBN, N - t.n0);
+  // weight rows n0 .. n0 + nb - 1 of each B matrix (nb <= BN)
+  const int nb = min(BN, N - t.n0);
   __amdgpu_buffer_rsrc_t brs[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b)
     brs[b] = rows_rsrc(j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)t.n0 * K,
                        (uint32_t)nb * K * 2);
-  uint32_t boff[2];
+  uint32_t boff[HB];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) boff[h] = (uint32_t)min(r0 + 64 * h, nb - 1) * K * 2;
+  for (int h = 0; h < HB; ++h) boff[h] = (uint32_t)min(r0 + SR * h, nb - 1) * K * 2;
   // K slices loaded ahead live in a ring of P register slots: slice t >= 1
   // sits in slot (t - 1) % P until it is stored to LDS.
-  gemm_u32x4 ra[P][HA], rb[P][NB][2];
+  gemm_u32x4 ra[P][HA], rb[P][NB][HB];
   auto gload = [&](int slot, int k0) {
     const int k = RAGGED ? min(k0 + q * 8, K - 8) : k0 + q * 8;  // K is a multiple of 8
 #pragma unroll
     for (int h = 0; h < HA; ++h) ra[slot][h] = *reinterpret_cast<const gemm_u32x4 *>(ap[h] + k);
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < HB; ++h)
 #pragma unroll
       for (int b = 0; b < NB; ++b) rb[slot][b][h] = buffer_load16(brs[b], boff[h] + 2 * k);
   };
@@ -556,50 +607,53 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
     const gemm_u32x4 zero = {0, 0, 0, 0};
 #pragma unroll
     for (int h = 0; h < HA; ++h)
-      *reinterpret_cast<gemm_u32x4 *>(&As[buf][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) =
+      *reinterpret_cast<gemm_u32x4 *>(&As[buf][r0 + SR * h][lds_chunk<KS>(r0 + SR * h, q) * 8]) =
           tail ? zero : ra[slot][h];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < HB; ++h)
 #pragma unroll
       for (int b = 0; b < NB; ++b)
-        *reinterpret_cast<gemm_u32x4 *>(&Bs[buf][b][r0 + 64 * h][lds_chunk(r0 + 64 * h, q) * 8]) =
+        *reinterpret_cast<gemm_u32x4 *>(&Bs[buf][b][r0 + SR * h][lds_chunk<KS>(r0 + SR * h, q) * 8]) =
             tail ? zero : rb[slot][b][h];
   };
-  floatx4 c[NB][MX][4];
+  floatx16 c[NB][MX][NY];
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
     for (int x = 0; x < MX; ++x)
 #pragma unroll
-      for (int y = 0; y < 4; ++y)
+      for (int y = 0; y < NY; ++y)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) c[b][x][y][i] = 0.0f;
+        for (int i = 0; i < 16; ++i) c[b][x][y][i] = 0.0f;
 
   // The main loop is straight-line (every step stores a slice and loads one,
   // clamped to the last slice past the end, whose data is then never used), so
   // the compiler can keep the loads of the other ring slots in flight; the
   // last steps, which load nothing, are peeled off.
   auto mma = [&](int buf) {
-    bf16x8 af[MX];
 #pragma unroll
-    for (int x = 0; x < MX; ++x) af[x] = lds_frag(As[buf], wm * (BM / 2) + x * 16 + lane % 16, lane);
+    for (int h = 0; h < KS / 16; ++h) {  // the 16-deep parts of the slice, in K order
+      bf16x8 af[MX];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      bf16x8 bf[4];
+      for (int x = 0; x < MX; ++x) af[x] = lds_frag32<KS>(As[buf], wm * WR + x * 32 + lane % 32, lane, h);
 #pragma unroll
-      for (int y = 0; y < 4; ++y) bf[y] = lds_frag(Bs[buf][b], wn * 64 + y * 16 + lane % 16, lane);
+      for (int b = 0; b < NB; ++b) {
+        bf16x8 bf[NY];
 #pragma unroll
-      for (int x = 0; x < MX; ++x)
+        for (int y = 0; y < NY; ++y) bf[y] = lds_frag32<KS>(Bs[buf][b], wn * WC + y * 32 + lane % 32, lane, h);
 #pragma unroll
-        for (int y = 0; y < 4; ++y)
-          c[b][x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
+        for (int x = 0; x < MX; ++x)
+#pragma unroll
+          for (int y = 0; y < NY; ++y)
+            c[b][x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
+      }
     }
   };
-  const int nk = (K + kKStep - 1) / kKStep;
+  const int nk = (K + KS - 1) / KS;
   gload(0, 0);
   lstore(0, 0, 0);
 #pragma unroll
-  for (int t = 1; t <= P; ++t) gload(t - 1, min(t, nk - 1) * kKStep);
+  for (int t = 1; t <= P; ++t) gload(t - 1, min(t, nk - 1) * KS);
   __syncthreads();
   int i = 0;
   for (; i + P < nk; i += P) {  // steps i .. i + P - 1, each followed by another
@@ -607,8 +661,8 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
     for (int u = 0; u < P; ++u) {
       const int s = i + u;  // slice multiplied now, out of LDS buffer s & 1
       mma(s & 1);
-      lstore(u, (s & 1) ^ 1, (s + 1) * kKStep);            // slice s + 1 lives in slot s % P = u
-      gload(u, min(s + 1 + P, nk - 1) * kKStep);           // slot u is free again
+      lstore(u, (s & 1) ^ 1, (s + 1) * KS);            // slice s + 1 lives in slot s % P = u
+      gload(u, min(s + 1 + P, nk - 1) * KS);           // slot u is free again
       __syncthreads();
     }
   }
@@ -617,19 +671,20 @@ __global__ __launch_bounds__(256, BM == 64 ? 3 : (P <= 2 ? 2 : 1)) void prefill_
     const int s = i + u;
     if (s < nk) {
       mma(s & 1);
-      if (s + 1 < nk) lstore(u, (s & 1) ^ 1, (s + 1) * kKStep);
+      if (s + 1 < nk) lstore(u, (s & 1) ^ 1, (s + 1) * KS);
       __syncthreads();
     }
   }
+  // lane i holds column i % 32 of each 32 x 32 block, rows 8 (v / 4) + 4 (i / 32) + v % 4
 #pragma unroll
   for (int x = 0; x < MX; ++x)
 #pragma unroll
-    for (int y = 0; y < 4; ++y)
+    for (int y = 0; y < NY; ++y)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = t.m0 + wm * (BM / 2) + x * 16 + (lane / 16) * 4 + i;
+      for (int i = 0; i < 16; ++i) {
+        const int m = t.m0 + wm * WR + x * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
         if (m >= j.nrows) continue;
-        const int n = t.n0 + wn * 64 + y * 16 + lane % 16;
+        const int n = t.n0 + wn * WC + y * 32 + lane % 32;
         if (n < N) {
           if (UP)
             static_cast<uint16_t *>(out)[(size_t)(j.row0 + m) * ldo + n] =
@@ -856,16 +911,30 @@ hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l) {
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-#define MOE_GEMM_UP(BM, RG)                                                                                  \
-  MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, BM, RG>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, xn, \
+#define MOE_GEMM_UP(BM, TH, RG)                                                                                   \
+  MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, BM, TH, kKStep, RG>), dim3(ntiles), dim3(TH), 0, l, tiles, jobs, xn, \
+             perm_tok, (void *)act, d, d_ff)
+#define MOE_GEMM_UP_TALL(RG)                                                                                     \
+  MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStagesTall, 256, 512, kKsTall, RG>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, \
+             xn, perm_tok, (void *)act, d, d_ff)
+  // a K not a multiple of the tall slice takes 32-deep slices three ahead
+  // (the 64-deep kernel with its K-tail handling would spill registers)
+#define MOE_GEMM_UP_TALL_RAGGED()                                                                                   \
+  MOE_LAUNCH((prefill_gemm_kernel<true, 3, 256, 512, kKStep, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, xn, \
              perm_tok, (void *)act, d, d_ff)
   const bool ragged = d % kKStep != 0;
   if (rows == 64) {
-    if (ragged) MOE_GEMM_UP(64, true); else MOE_GEMM_UP(64, false);
+    if (ragged) MOE_GEMM_UP(64, 256, true); else MOE_GEMM_UP(64, 256, false);
+  } else if (rows == 128) {
+    if (ragged) MOE_GEMM_UP(128, 256, true); else MOE_GEMM_UP(128, 256, false);
+  } else if (rows == 256) {
+    if (d % kKsTall == 0) MOE_GEMM_UP_TALL(false); else MOE_GEMM_UP_TALL_RAGGED();
   } else {
-    if (ragged) MOE_GEMM_UP(128, true); else MOE_GEMM_UP(128, false);
+    return hipErrorInvalidValue;
   }
 #undef MOE_GEMM_UP
+#undef MOE_GEMM_UP_TALL
+#undef MOE_GEMM_UP_TALL_RAGGED
   return hipGetLastError();
 }
 
@@ -899,16 +968,28 @@ hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const G
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
                                float *Y, int d, int d_ff, int rows, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
-#define MOE_GEMM_DOWN(BM, RG)                                                                                 \
-  MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, BM, RG>), dim3(ntiles), dim3(256), 0, l, tiles, jobs, act, \
+#define MOE_GEMM_DOWN(BM, TH, RG)                                                                                  \
+  MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, BM, TH, kKStep, RG>), dim3(ntiles), dim3(TH), 0, l, tiles, jobs, act, \
+             (const int32_t *)nullptr, (void *)Y, d, d_ff)
+#define MOE_GEMM_DOWN_TALL(RG)                                                                                     \
+  MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStagesTall, 256, 512, kKsTall, RG>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, \
+             act, (const int32_t *)nullptr, (void *)Y, d, d_ff)
+#define MOE_GEMM_DOWN_TALL_RAGGED()                                                                                  \
+  MOE_LAUNCH((prefill_gemm_kernel<false, 3, 256, 512, kKStep, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, act, \
              (const int32_t *)nullptr, (void *)Y, d, d_ff)
   const bool ragged = d_ff % kKStep != 0;
   if (rows == 64) {
-    if (ragged) MOE_GEMM_DOWN(64, true); else MOE_GEMM_DOWN(64, false);
+    if (ragged) MOE_GEMM_DOWN(64, 256, true); else MOE_GEMM_DOWN(64, 256, false);
+  } else if (rows == 128) {
+    if (ragged) MOE_GEMM_DOWN(128, 256, true); else MOE_GEMM_DOWN(128, 256, false);
+  } else if (rows == 256) {
+    if (d_ff % kKsTall == 0) MOE_GEMM_DOWN_TALL(false); else MOE_GEMM_DOWN_TALL_RAGGED();
   } else {
-    if (ragged) MOE_GEMM_DOWN(128, true); else MOE_GEMM_DOWN(128, false);
+    return hipErrorInvalidValue;
   }
 #undef MOE_GEMM_DOWN
+#undef MOE_GEMM_DOWN_TALL
+#undef MOE_GEMM_DOWN_TALL_RAGGED
   return hipGetLastError();
 }
 
@@ -918,6 +999,6 @@ hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, co
   return hipGetLastError();
 }
 
-int prefill_tile_cols() { return kBN; }
+int prefill_tile_cols(bool up) { return up ? gemm_cols<true>() : gemm_cols<false>(); }
 
 }  // namespace moe

@@ -100,6 +100,22 @@ def test_prefill_ragged_shapes():
     rig.store.close()
 
 
+def test_tall_tiles_with_a_k_tail():
+    # 4096 tokens over 8 experts (every expert resident): the up launch has
+    # enough 256-row tiles to take them, with K = d = 1032 (not a multiple of
+    # 32 or 64) and N = d_ff = 2056 (a partial column tile); the down launch
+    # reduces over d_ff = 2056 (not a multiple of 64)
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=1, experts=8, top_k=2, d_model=1032, d_ff=2056,
+                                         dtype="bf16", tokens=2, prefill_tokens=4096)
+    _say("tall tiles with a K tail", cfg)
+    rig = Rig(cfg)
+    moe = rig.cache(8, "lfu", max_prefill_tokens=4096)
+    _, _, worst, _ = prefill_and_check(rig, moe, "lfu", 8, 4096, list(range(0, 4096, 61)) + [4095])
+    _say("worst", worst)
+    moe.close()
+    rig.store.close()
+
+
 @pytest.mark.parametrize("T", [5, 64])
 def test_small_prefill_fine_grained(T):
     # small prefills at the 64-expert shape (d = 2048): a partial and a full
