@@ -65,6 +65,13 @@ DESCRIPTIONS = {
 }
 
 
+def ffn_kernels(cfg):
+    """Names of the decode FFN's up and down kernels for this model."""
+    if cfg.dtype == "q2g16":
+        return ("ffnq_up_lut_kernel" if cfg.d_model <= 4096 else "ffnq_up_kernel"), "ffnq_down_lut_kernel"
+    return "ffn_up_kernel", "ffn_down_kernel"
+
+
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
@@ -487,7 +494,7 @@ def stack_main(args):
     fetch_gbps = bd_fetched / (copy_ms * 1e-3) / 1e9 if copy_ms > 0 else None
     acc = [x for x in head["recs"] if x[0] != 2]
     headline = pass_summary(cfg, head, slots, flags)
-    kind = "ffnq" if cfg.dtype == "q2g16" else "ffn"
+    up_kernel, down_kernel = ffn_kernels(cfg)
     desc = (DESCRIPTIONS[args.workload]
             + f"; {cfg.tokens} batch-1 decode tokens from the warm start, {slots} HBM slots per layer, LFU"
             + (f", next-layer prefetch of up to {cfg.prefetch_max}" if spec else "")
@@ -529,20 +536,20 @@ def stack_main(args):
                     "median": round(1e3 * sorted(head["step_s"])[len(head["step_s"]) // 2], 1)},
         "runs": comparisons,
         "roofline": {
-            "kernel": f"{kind}_up_kernel",
+            "kernel": up_kernel,
             "bound": "hbm",
             "achieved": round(up_gbps, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(up_gbps / HBM_PEAK_GBPS, 4),
-            "traffic": pmc_traffic() if kind == "ffn" else None,
+            "traffic": pmc_traffic() if cfg.dtype == "bf16" else None,
             "bytes_per_launch": up_bytes,
             "avg_launch_us": round(up_ms * 1e3, 2),
             "launches": ut["ffn_up_n"],
             "note": "events stamped by every up launch of the timed pass; the step itself is bound by the "
                     "host link (link_roofline)",
         },
-        "ffn_down": {"kernel": f"{kind}_down_kernel", "achieved_gbps": round(down_gbps, 1) if down_gbps else None,
+        "ffn_down": {"kernel": down_kernel, "achieved_gbps": round(down_gbps, 1) if down_gbps else None,
                      "frac": round(down_gbps / HBM_PEAK_GBPS, 4) if down_gbps else None,
                      "bytes_per_launch": down_bytes, "avg_launch_us": round(down_ms * 1e3, 2),
                      "reduce_avg_us": round(1e3 * bt["ffn_reduce_ms"] / max(1, bt["ffn_reduce_n"]), 2),
@@ -773,7 +780,7 @@ def layer_main(args):
         "runs": summary,
         "ffn_hbm_gbps": round((up_bytes + down_bytes) / ((up_ms + down_ms) * 1e-3) / 1e9, 1),
         "roofline": {
-            "kernel": "ffnq_up_kernel" if cfg.dtype == "q2g16" else "ffn_up_kernel",
+            "kernel": ffn_kernels(cfg)[0],
             "bound": "hbm",
             "achieved": round(up_gbps, 1),
             "peak": HBM_PEAK_GBPS,
@@ -784,7 +791,7 @@ def layer_main(args):
             "avg_launch_us": round(up_ms * 1e3, 2),
             "launches": tim["ffn_up_n"],
         },
-        "ffn_down": {"kernel": "ffnq_down_kernel" if cfg.dtype == "q2g16" else "ffn_down_kernel",
+        "ffn_down": {"kernel": ffn_kernels(cfg)[1],
                      "achieved_gbps": round(down_gbps, 1), "frac": round(down_gbps / HBM_PEAK_GBPS, 4),
                      "bytes_per_launch": down_bytes, "avg_launch_us": round(down_ms * 1e3, 2),
                      "reduce_avg_us": round(1e3 * tim["ffn_reduce_ms"] / max(1, tim["ffn_reduce_n"]), 2)},

@@ -9,15 +9,17 @@
 // and the weight is (q - zero) * scale, an exact fp32 number.  An expert is
 // W1 [d_ff x d] | W3 [d_ff x d] | W2 [d x d_ff], 7 bytes per 16 weights.
 //
-// Same structure as the bf16/fp32 kernels: an HBM-bound GEMV with the
-// activation in registers, all of a wave's loads issued before its
-// arithmetic, and a down projection split along its reduction axis whose
-// partial sums the shared reduction kernel adds in a fixed order.  A lane owns
-// 64 consecutive columns (four groups) per step: 16 bytes of codes, 8 bytes
-// of scales and 4 bytes of zero codes.  Per group the dot product is taken as
-// scale * (sum_i q_i x_i - zero * sum_i x_i) with the group sums of x formed
-// once; four codes are masked out of a word at a time and converted byte by
-// byte, so a weight costs about 2.4 vector instructions.
+// Same structure as the bf16/fp32 kernels: an HBM-bound GEMV, all of a
+// wave's loads for the next rows issued before its arithmetic on the current
+// ones, and a down projection split along its reduction axis (chunks of 4096
+// columns) whose partial sums the shared reduction kernel adds in a fixed
+// order.  A lane owns 64 consecutive columns (four groups) of a row: 16 bytes
+// of codes, 8 bytes of scales and 4 bytes of zero codes.  Per group the dot
+// product is scale * (sum_i q_i x_i - zero * sum_i x_i) with the group sums of
+// x formed once.  For d <= 4096 (up) and for every 4096-column chunk (down)
+// the sums of q_i x_i come from a table in LDS (see ffnq_up_lut_kernel); the
+// up projection of wider models masks four codes out of a word at a time and
+// converts them byte by byte (about 2.4 vector instructions a weight).
 //
 // Loads are issued from addresses clamped into the matrix (rows past the end
 // read the last row, columns past the end the last unit) so that none sits
@@ -34,7 +36,6 @@ constexpr int kLaneCols = 64;                 // four groups of 16
 constexpr int kStepCols = kWave * kLaneCols;  // 4096 columns per wave step
 constexpr int kQUpRows = 2;                   // rows of W1 and of W3 per wave and step
 constexpr int kUpWaves = 256 * 4 * 3;         // waves of one up launch: 3 per SIMD
-constexpr int kQDownRows = 8;                 // rows of W2 per wave
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
@@ -126,6 +127,26 @@ __device__ __forceinline__ float unit_dot(const QUnit &u, const float *x, const 
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }
 
+// Sum over the 64 lanes of a wave, left in lane 63, through DPP moves (no LDS
+// round trips): running sums within each row of 16 lanes (row_shr 1, 2, 4,
+// 8), then lane 15 of rows 0 and 2 into rows 1 and 3 (row_bcast:15) and lane
+// 31 into rows 2 and 3 (row_bcast:31).  Lanes whose DPP source lies outside
+// the pattern add the 0 passed as the old value.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add(float v) {
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROW_MASK,
+                                                                   0xF, false));
+}
+__device__ __forceinline__ float wave_sum_to_lane63(float v) {
+  v = dpp_add<0x111, 0xF>(v);  // row_shr:1
+  v = dpp_add<0x112, 0xF>(v);  // row_shr:2
+  v = dpp_add<0x114, 0xF>(v);  // row_shr:4
+  v = dpp_add<0x118, 0xF>(v);  // row_shr:8
+  v = dpp_add<0x142, 0xA>(v);  // row_bcast:15
+  v = dpp_add<0x143, 0xC>(v);  // row_bcast:31
+  return v;
+}
+
 // act_r = SiLU(W1_r x) * (W3_r x), x = h / rms(h); d <= STEPS * 4096.
 // G workgroups per rank; each wave walks row groups of RPW rows with a stride
 // of G * 4 groups, loading the next group's weights before it works on the
@@ -197,10 +218,135 @@ __global__ __launch_bounds__(kThreads) void ffnq_up_kernel(FfnArgs a, int G) {
   }
 }
 
-// one (row block, rank, 4096-column chunk) per workgroup: partial sums of
-// g_r W2_r act_r for RPW rows per wave
-template <int RPW>
-__global__ __launch_bounds__(kThreads) void ffnq_down_kernel(FfnArgs a) {
+// up through a lookup table, for d <= 4096 (one 64-column unit per lane).
+// With x fixed for the whole launch, the contribution of a 4-bit nibble of
+// codes (two adjacent columns c, c + 1 of a lane's 64) is one of 16 values
+// q0 x_c + q1 x_c+1.  Each workgroup first writes those values for all 64
+// lanes' 32 column pairs to LDS, laid out [pair][nibble][lane] (128 KB), so
+// the 64 lanes of a lookup always hit 64 different banks.  A nibble then
+// costs one v_perm_b32, which forms the LDS address (nibble << 8 | lane << 2,
+// plus 64 KB for pairs 16..31) straight from the byte holding the nibble, one
+// LDS read and one add: with the byte masks and the per-group scale and zero
+// about 1.4 vector instructions a weight instead of 2.7, so the kernel is
+// bound by streaming the codes rather than by the vector ALUs.  The sums
+// differ from the direct form only in rounding (one rounding per table
+// entry).  One workgroup of 16 waves per CU; each wave walks rows of both
+// ranks (W1 and W3 of a row together), the codes of the next two rows in
+// flight while it works on the current one.
+constexpr int kLutThreads = 1024;
+constexpr int kLutWaves = kLutThreads / kWave;
+constexpr int kLutPairs = kLaneCols / 2;  // column pairs per lane
+
+// Writes the table for x_c = scale * src[c] over columns c < n of every
+// lane's 64 (zeros past n), then returns this lane's four group sums of x
+// divided by 64.  Called by all kLutThreads threads; ends with the table
+// readable.
+__device__ __forceinline__ void lut_build(float *tab, const float *src, int n, float scale, int lane, int wave,
+                                          float *xs64) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {  // wave w writes pairs w and w + 16 of every lane
+    const int p = wave + kLutWaves * i;
+    const int c = lane * kLaneCols + 2 * p;
+    float x0 = 0.0f, x1 = 0.0f;
+    if (c < n) {
+      const float2 v = *reinterpret_cast<const float2 *>(src + c);
+      x0 = v.x * scale;
+      x1 = v.y * scale;
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) tab[(p * 16 + v) * kWave + lane] = fmaf((float)(v >> 2), x1, (float)(v & 3) * x0);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {  // nibble 5 = codes 1, 1: x_c + x_c+1
+    float t = 0.0f;
+#pragma unroll
+    for (int n8 = 0; n8 < 8; ++n8) t += tab[((8 * g + n8) * 16 + 5) * kWave + lane];
+    xs64[g] = t * (1.0f / 64.0f);
+  }
+}
+
+// sum over this lane's 64 columns of w_c x_c for one unit, through the table
+__device__ __forceinline__ float lut_dot(const float *tab, const QUnit &u, int lane, const float *xs64) {
+  const uint32_t lb0 = (uint32_t)lane * 4u, lb1 = lb0 | 0x10000u;
+  const char *tb = reinterpret_cast<const char *>(tab);
+  float out = 0.0f;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const uint32_t w = u.c[g];
+    const uint32_t lo = w & 0x0F0F0F0Fu, hi = (w >> 4) & 0x0F0F0F0Fu;
+    const uint32_t lb = g < 2 ? lb0 : lb1;
+    float acc = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      // byte j of lo: pair 8 g + 2 j; of hi: pair 8 g + 2 j + 1
+      const uint32_t sel = 0x0C020000u | ((uint32_t)(4 + j) << 8);
+      const uint32_t alo = __builtin_amdgcn_perm(lo, lb, sel);
+      const uint32_t ahi = __builtin_amdgcn_perm(hi, lb, sel);
+      const int p = (8 * g + 2 * j) & 15;
+      acc += *reinterpret_cast<const float *>(tb + alo + p * 4096);
+      acc += *reinterpret_cast<const float *>(tb + ahi + (p + 1) * 4096);
+    }
+    const uint32_t sb = (u.s[g >> 1] >> (16 * (g & 1))) & 0xFFFFu;
+    const float sc = (float)__builtin_bit_cast(_Float16, (uint16_t)sb);
+    const float z = (float)((u.z >> (8 * g)) & 0xFFu);
+    out = fmaf(sc, fmaf(-z, xs64[g], acc), out);
+  }
+  return out;
+}
+
+__global__ __launch_bounds__(kLutThreads, 1) void ffnq_up_lut_kernel(FfnArgs a) {
+  __shared__ float tab[kLutPairs * 16 * kWave];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int d = a.d, d_ff = a.d_ff, K = a.route->k;
+  const uint8_t *const arena = a.arena;
+  const size_t mbytes = (size_t)d_ff * d / 16 * 7;
+  const int col = lane * kLaneCols;
+  // work: row r of rank k (W1 and W3) is item k * d_ff + r; wave w takes
+  // items w, w + stride, ... (with d_ff a multiple of 64 and 4096 waves, the
+  // Mixtral shape gives every wave 7 of them)
+  const int nitems = K * d_ff;
+  const int stride = gridDim.x * kLutWaves;
+  const int first = blockIdx.x * kLutWaves + wave;
+  auto load_item = [&](int it, QUnit (&u)[2]) {
+    it = min(it, nitems - 1);  // past the end: a valid row, never used
+    const int rank = it / d_ff, row = it - rank * d_ff;
+    int slot = a.route->slot[rank];
+    slot = slot < 0 ? 0 : (slot >= a.S ? a.S - 1 : slot);  // the router never writes these; clamp, not branch
+    const uint8_t *base = arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes;
+    u[0] = load_unit(qmat(base, d_ff, d), row, col);
+    u[1] = load_unit(qmat(base + mbytes, d_ff, d), row, col);
+  };
+  // the first two items' codes are on their way while the table is built
+  QUnit u0[2], u1[2];
+  load_item(first, u0);
+  load_item(first + stride, u1);
+  float xs64[4];
+  lut_build(tab, a.h, d, a.route->inv_r, lane, wave, xs64);
+  for (int it = first; it < nitems; it += stride) {
+    QUnit u2[2];
+    load_item(it + 2 * stride, u2);
+    const float a1 = wave_sum_to_lane63(lut_dot(tab, u0[0], lane, xs64));
+    const float a3 = wave_sum_to_lane63(lut_dot(tab, u0[1], lane, xs64));
+    if (lane == kWave - 1) a.act[it] = silu(a1) * a3;  // item it = rank * d_ff + row
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      u0[m] = u1[m];
+      u1[m] = u2[m];
+    }
+  }
+}
+
+// down through the same kind of table, for d_ff chunks of 4096 columns: one
+// workgroup per (block of `rpb` rows of W2, rank, chunk), the table built
+// from g_r act_r over the chunk; each wave takes every 16th row of the block
+// and writes the chunk's partial row sum.  Invalid ranks write zeros, as the
+// reduction reads every chunk.
+__global__ __launch_bounds__(kLutThreads, 1) void ffnq_down_lut_kernel(FfnArgs a, int rpb) {
+  __shared__ float tab[kLutPairs * 16 * kWave];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int d = a.d, d_ff = a.d_ff, K = a.route->k;
   const int cpr = (d_ff + kStepCols - 1) / kStepCols;
   const int nch = a.K * cpr;
@@ -208,27 +354,26 @@ __global__ __launch_bounds__(kThreads) void ffnq_down_kernel(FfnArgs a) {
   const int ch = blockIdx.x - rb * nch;
   const int rank = ch / cpr;
   const int c0 = (ch - rank * cpr) * kStepCols;
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int row0 = rb * kWpb * RPW + wave * RPW;
-
+  const int row_lo = rb * rpb, row_hi = min(d, row_lo + rpb);
   const int slot = rank < K ? a.route->slot[rank] : -1;
-  const bool valid = rank < K && slot >= 0 && slot < a.S;
-  float acc[RPW] = {};
-  if (valid) {
-    const uint8_t *base = a.arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes;
-    const QMat w2 = qmat(base + 2 * ((size_t)d_ff * d / 16 * 7), d, d_ff);
-    QUnit u[RPW];
-#pragma unroll
-    for (int q = 0; q < RPW; ++q) u[q] = load_unit(w2, row0 + q, c0 + lane * kLaneCols);
-    float x[kLaneCols], xs[4];
-    load_x(a.act + (size_t)rank * d_ff, c0 + lane * kLaneCols, d_ff, a.route->g[rank], x, xs);
-#pragma unroll
-    for (int q = 0; q < RPW; ++q) acc[q] = unit_dot(u[q], x, xs);
+  if (rank >= K || slot < 0 || slot >= a.S) {
+    for (int r = row_lo + tid; r < row_hi; r += kLutThreads) a.part[(size_t)ch * d + r] = 0.0f;
+    return;
   }
-#pragma unroll
-  for (int q = 0; q < RPW; ++q) {
-    const float s = wave_sum(acc[q]);
-    if (lane == 0 && row0 + q < d) a.part[(size_t)ch * d + row0 + q] = s;
+  const uint8_t *base = a.arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes;
+  const QMat w2 = qmat(base + 2 * ((size_t)d_ff * d / 16 * 7), d, d_ff);
+  const int col = c0 + lane * kLaneCols;  // load_unit clamps columns past d_ff (those x are zero)
+  const int first = row_lo + wave;
+  QUnit u0 = load_unit(w2, min(first, row_hi - 1), col);
+  QUnit u1 = load_unit(w2, min(first + kLutWaves, row_hi - 1), col);
+  float xs64[4];
+  lut_build(tab, a.act + (size_t)rank * d_ff + c0, d_ff - c0, a.route->g[rank], lane, wave, xs64);
+  for (int r = first; r < row_hi; r += kLutWaves) {
+    const QUnit u2 = load_unit(w2, min(r + 2 * kLutWaves, row_hi - 1), col);
+    const float s = wave_sum_to_lane63(lut_dot(tab, u0, lane, xs64));
+    if (lane == kWave - 1) a.part[(size_t)ch * d + r] = s;
+    u0 = u1;
+    u1 = u2;
   }
 }
 
@@ -237,6 +382,11 @@ __global__ __launch_bounds__(kThreads) void ffnq_down_kernel(FfnArgs a) {
 int ffnq_down_chunks(int K, int d_ff) { return K * ((d_ff + kStepCols - 1) / kStepCols); }
 
 hipError_t launch_ffnq_up(const FfnArgs &a, const Launch &l) {
+  if (a.d <= kStepCols) {
+    // one workgroup per CU (its 128 KB table leaves room for no second one)
+    MOE_LAUNCH(ffnq_up_lut_kernel, dim3(256), dim3(kLutThreads), 0, l, a);
+    return hipGetLastError();
+  }
   // about kUpWaves waves in total, at most one row group each
   const int groups = (a.d_ff + kQUpRows - 1) / kQUpRows;
   const int G = max(1, min((groups + kWpb - 1) / kWpb, kUpWaves / (kWpb * max(1, a.K))));
@@ -249,9 +399,11 @@ hipError_t launch_ffnq_up(const FfnArgs &a, const Launch &l) {
 }
 
 hipError_t launch_ffnq_down(const FfnArgs &a, const Launch &l) {
-  const int rows = kWpb * kQDownRows;
-  const dim3 grid(((a.d + rows - 1) / rows) * ffnq_down_chunks(a.K, a.d_ff));
-  MOE_LAUNCH((ffnq_down_kernel<kQDownRows>), grid, dim3(kThreads), 0, l, a);
+  // about one workgroup per CU: blocks of rows per (rank, chunk)
+  const int nch = ffnq_down_chunks(a.K, a.d_ff);
+  const int nrb = max(1, 256 / nch);
+  const int rpb = (a.d + nrb - 1) / nrb;
+  MOE_LAUNCH(ffnq_down_lut_kernel, dim3(((a.d + rpb - 1) / rpb) * nch), dim3(kLutThreads), 0, l, a, rpb);
   return hipGetLastError();
 }
 
