@@ -764,6 +764,11 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
 
   hipStream_t q = c->xs;
   const bool split = c->fetch_mode == MOE_FETCH_SPLIT;
+  // With a slot for every expert, all of them are resident from the warm
+  // start on and no lookup or guess can ever need a copy: the fetch lists the
+  // router writes are always empty, so no copy is issued and nothing waits
+  // for one (no fetch launch, no cross-stream event, no host read-back).
+  const bool no_copies = c->S == c->E;
   // A plain store's demand copies (kernel and split modes) go on the compute
   // stream: the FFN waits for them anyway, and stream order then replaces the
   // two cross-stream waits (router -> copy stream -> FFN) that cost tens of
@@ -772,7 +777,9 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   const bool demand_on_cs =
       !c->one_stream && c->fetch_mode != MOE_FETCH_DMA && !coded_store(c->host_format);
   hipStream_t qd = demand_on_cs ? c->cs : q;
-  if (c->fetch_mode != MOE_FETCH_DMA) {
+  if (no_copies) {
+    // nothing to copy (see above)
+  } else if (c->fetch_mode != MOE_FETCH_DMA) {
     if (!c->one_stream && ((demand && !demand_on_cs) || spec_layer >= 0)) {
       HIP_TRY(c, hipEventRecord(c->ev_router, c->cs));
       HIP_TRY(c, hipStreamWaitEvent(q, c->ev_router, 0));
@@ -786,7 +793,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     HIP_TRY(c, hipMemcpy(&e, c->err, sizeof e, hipMemcpyDeviceToHost));
     if (e != ERR_NONE) return MOE_OK;  // reported at the next synchronising call
   }
-  if (demand) {
+  if (demand && !no_copies) {
     // a slot the router just took may still be receiving a speculative copy
     if (demand_on_cs && c->pf_pending[layer]) {
       HIP_TRY(c, hipStreamWaitEvent(c->cs, c->ev_pf[layer], 0));
@@ -804,7 +811,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
       }
     }
   }
-  if (spec_layer >= 0 && !split) {
+  if (spec_layer >= 0 && !split && !no_copies) {
     int rc = issue_fetch(c, c->pl + spec_layer, 1, q);
     if (rc != MOE_OK) return rc;
     if (!c->one_stream) {
@@ -844,7 +851,7 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     kernel_span_done(c, SPAN_REDUCE, lx);
     c->last_route_kind = 1;
   }
-  if (spec_layer >= 0 && split) {
+  if (spec_layer >= 0 && split && !no_copies) {
     // The prefetch list comes back on the library's own stream, so neither the
     // FFN just enqueued nor the demand copies wait for the host; the runtime copies
     // then queue on the copy stream behind this layer's demand copies.

@@ -27,6 +27,10 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
 constexpr int kUpRows = 2;     // rows per wave (register path)
+#ifndef MOE_FFN_UP_ROWS_NARROW
+#define MOE_FFN_UP_ROWS_NARROW 2
+#endif
+constexpr int kUpRowsNarrow = MOE_FFN_UP_ROWS_NARROW;  // the same for d <= 2048 (2 or 4)
 constexpr int kUpLdsRows = 1;  // row pairs per wave on the wide-model path
 constexpr int kReduceThreads = 64;
 
@@ -312,29 +316,37 @@ DownShape down_shape(int d_ff, int dtype) {
   return {2, 2};
 }
 
-template <int DT, int STEPS>
-void launch_up_steps(dim3 grid, bool ragged, const FfnArgs &a, const Launch &l) {
+template <int DT, int STEPS, int RPW>
+void launch_up_steps(bool ragged, const FfnArgs &a, const Launch &l) {
+  constexpr int kRows = kWavesPerBlock / 2 * RPW;
+  const dim3 grid(a.K * ((a.d_ff + kRows - 1) / kRows));
   if (ragged)
-    MOE_LAUNCH((ffn_up_kernel<DT, STEPS, kUpRows, true>), grid, dim3(kThreads), 0, l, a);
+    MOE_LAUNCH((ffn_up_kernel<DT, STEPS, RPW, true>), grid, dim3(kThreads), 0, l, a);
   else
-    MOE_LAUNCH((ffn_up_kernel<DT, STEPS, kUpRows, false>), grid, dim3(kThreads), 0, l, a);
+    MOE_LAUNCH((ffn_up_kernel<DT, STEPS, RPW, false>), grid, dim3(kThreads), 0, l, a);
+}
+
+template <int DT, int STEPS>
+void launch_up_rows(bool ragged, const FfnArgs &a, const Launch &l) {
+  if (a.d <= 2048 && kUpRowsNarrow == 4)
+    launch_up_steps<DT, STEPS, 4>(ragged, a, l);
+  else
+    launch_up_steps<DT, STEPS, kUpRows>(ragged, a, l);
 }
 
 template <int DT>
 hipError_t launch_up_t(const FfnArgs &a, const Launch &l) {
   constexpr int COLS = kWave * Elem<DT>::kVec;
   const int steps = (a.d + COLS - 1) / COLS;
-  constexpr int kRows = kWavesPerBlock / 2 * kUpRows;
-  const dim3 grid(a.K * ((a.d_ff + kRows - 1) / kRows));
   const bool ragged = a.d % COLS != 0;
   if (steps <= 1)
-    launch_up_steps<DT, 1>(grid, ragged, a, l);
+    launch_up_rows<DT, 1>(ragged, a, l);
   else if (steps <= 2)
-    launch_up_steps<DT, 2>(grid, ragged, a, l);
+    launch_up_rows<DT, 2>(ragged, a, l);
   else if (steps <= 4)
-    launch_up_steps<DT, 4>(grid, ragged, a, l);
+    launch_up_rows<DT, 4>(ragged, a, l);
   else if (steps <= 8)
-    launch_up_steps<DT, 8>(grid, ragged, a, l);
+    launch_up_rows<DT, 8>(ragged, a, l);
   else {
     const dim3 g2(a.K * ((a.d_ff + kWavesPerBlock * kUpLdsRows - 1) / (kWavesPerBlock * kUpLdsRows)));
     MOE_LAUNCH((ffn_up_lds_kernel<DT, kUpLdsRows>), g2, dim3(kThreads), (uint32_t)(a.d * sizeof(float)), l, a);

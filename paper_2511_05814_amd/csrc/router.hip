@@ -1,8 +1,8 @@
 // Router and cache-table kernel for batch-1 decode.
 //
-// One workgroup per call; beyond 32 gate rows a first launch spreads the GEMV
-// over several workgroups (one row per wave) and the single workgroup of a
-// second launch reads the logits back.  All 16 waves first compute the gate logits
+// One workgroup per call (a two-launch form, the GEMV spread over several
+// workgroups, remains for more gate rows than this build has).  All 16 waves
+// first compute the gate logits
 // z = W_g h (Sec. 4.3: the gate is a linear map [len_hidden, num_experts]) for
 // the layer being decoded and, when speculating, for the next layer (Sec. 3.2:
 // the next layer's gate applied to the current hidden state).  Each product
@@ -31,18 +31,18 @@ constexpr int kWaves = kThreads / kWave;
 
 // Gate logits z[row] for up to two layers: rows 0..E-1 belong to a.layer (when
 // routing here), rows E..2E-1 to a.spec_layer (when speculating); only the
-// needed rows are visited.  Wave w owns needed rows r0 + w, r0 + w + kWaves,
-// ...; lane i covers columns EPL*i + EPL*64*c of a row (chunk c), accumulating
-// in fp64 in column order, and the wave sums the lanes at the end of each row.
-// h comes from LDS.  The weight loads of kBatch (row, chunk) items are issued
-// together, from addresses clamped into the gate array so that no load sits
-// behind a branch (a load under a condition is waited for on the spot), and
-// only then used.
-constexpr int kBatch = 8;
+// needed rows are visited.  Wave w owns needed rows r0 + w, r0 + w + stride,
+// ... (at most MR of them) and accumulates all of them at once, one fp64
+// chain per row: lane i covers columns EPL*i + EPL*64*c of a row (chunk c), in
+// chunk order, with h from LDS.  The loads of the next chunk of all the
+// wave's rows are issued before the current chunk's products, from addresses
+// clamped into the gate array (past the wave's rows or chunks they reread a
+// valid row or chunk, unused) so that no load sits behind a branch; the lanes
+// of each row are then summed with DPP moves (no LDS round trips).
 constexpr int kMaxD = 16384;
 
 struct GateWork {
-  int n = 0, cpr = 1;        // (row, chunk) items of this wave; chunks per row
+  int m = 0, cpr = 1;         // rows of this wave; 16-byte chunks per row
   int first = 0, stride = 1;  // this wave's rows: first, first + stride, ...
 };
 
@@ -54,73 +54,157 @@ __device__ __forceinline__ GateWork gate_work(const RouterArgs &a, int r0, int r
   g.cpr = (a.d + kWave * EPL - 1) / (kWave * EPL);
   g.first = r0 + (int)blockIdx.x * kWaves + wave;
   g.stride = (int)gridDim.x * kWaves;
-  const int M = g.first < r1 ? (r1 - g.first + g.stride - 1) / g.stride : 0;
-  g.n = M * g.cpr;
+  g.m = g.first < r1 ? (r1 - g.first + g.stride - 1) / g.stride : 0;
   return g;
 }
 
-// Issue the weight loads of items j0 .. j0 + kBatch - 1 (n > 0).
-template <int DT>
-__device__ __forceinline__ void gate_load(const RouterArgs &a, int lane, const GateWork &g, int j0, uint4 *v) {
+// Issue the weight loads of chunk c (clamped) of the wave's MR rows (m > 0).
+template <int DT, int MR>
+__device__ __forceinline__ void gate_load(const RouterArgs &a, int lane, const GateWork &g, int c, uint4 *v) {
   constexpr int EPL = DT == 1 ? 8 : 4;
   constexpr int ESZ = DT == 1 ? 2 : 4;
   const int E = a.E, d = a.d;
   const uint8_t *gate = static_cast<const uint8_t *>(a.gate);
+  const int col = min(min(c, g.cpr - 1) * kWave * EPL + lane * EPL, d - EPL);
 #pragma unroll
-  for (int u = 0; u < kBatch; ++u) {
-    const int j = min(j0 + u, g.n - 1);
-    const int row = g.first + g.stride * (j / g.cpr);
+  for (int i = 0; i < MR; ++i) {
+    const int row = g.first + g.stride * min(i, g.m - 1);
     const int gl = row < E ? a.layer : a.spec_layer;
     const int e = row < E ? row : row - E;
-    const int col = min((j % g.cpr) * kWave * EPL + lane * EPL, d - EPL);
-    v[u] = *reinterpret_cast<const uint4 *>(gate + (((size_t)gl * E + e) * d + col) * ESZ);
+    v[i] = *reinterpret_cast<const uint4 *>(gate + (((size_t)gl * E + e) * d + col) * ESZ);
   }
 }
 
-// v holds the first batch, loaded by gate_load(.., 0, v) before h was staged;
-// logit `row` goes to zs[row].
-template <int DT>
+// fp64 sum over a wave's lanes, left in lane 63: running sums within rows of
+// 16 lanes (row_shr 1, 2, 4, 8), then row_bcast:15 and row_bcast:31; lanes
+// whose DPP source lies outside the pattern add 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_add_d(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROW_MASK, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROW_MASK, 0xF, false);
+  return v + __hiloint2double(hi, lo);
+}
+__device__ __forceinline__ double wave_sum_d_to_lane63(double v) {
+  v = dpp_add_d<0x111, 0xF>(v);
+  v = dpp_add_d<0x112, 0xF>(v);
+  v = dpp_add_d<0x114, 0xF>(v);
+  v = dpp_add_d<0x118, 0xF>(v);
+  v = dpp_add_d<0x142, 0xA>(v);
+  v = dpp_add_d<0x143, 0xC>(v);
+  return v;
+}
+
+// The products of chunk c (whose weights are in v) into acc.
+template <int DT, int MR>
+__device__ __forceinline__ void gate_chunk(const float *hs, int d, int lane, int c, const uint4 *v, double *acc) {
+  constexpr int EPL = DT == 1 ? 8 : 4;
+  const int col = c * kWave * EPL + lane * EPL;
+  if (col < d) {
+    const float4 h0 = *reinterpret_cast<const float4 *>(hs + col);
+    if (DT == 1) {
+      const float4 h1 = *reinterpret_cast<const float4 *>(hs + col + 4);
+#pragma unroll
+      for (int i = 0; i < MR; ++i) {
+        float f[8];
+        bf16x8_to_f32(v[i], f);
+        acc[i] = fma((double)f[0], (double)h0.x, acc[i]);
+        acc[i] = fma((double)f[1], (double)h0.y, acc[i]);
+        acc[i] = fma((double)f[2], (double)h0.z, acc[i]);
+        acc[i] = fma((double)f[3], (double)h0.w, acc[i]);
+        acc[i] = fma((double)f[4], (double)h1.x, acc[i]);
+        acc[i] = fma((double)f[5], (double)h1.y, acc[i]);
+        acc[i] = fma((double)f[6], (double)h1.z, acc[i]);
+        acc[i] = fma((double)f[7], (double)h1.w, acc[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < MR; ++i) {
+        acc[i] = fma((double)__uint_as_float(v[i].x), (double)h0.x, acc[i]);
+        acc[i] = fma((double)__uint_as_float(v[i].y), (double)h0.y, acc[i]);
+        acc[i] = fma((double)__uint_as_float(v[i].z), (double)h0.z, acc[i]);
+        acc[i] = fma((double)__uint_as_float(v[i].w), (double)h0.w, acc[i]);
+      }
+    }
+  }
+}
+
+// All of a wave's gate weights at once, when its rows have at most 16 / MR
+// chunks (the 64-expert model: 4 rows of 4 chunks): the loads of chunks 1..
+// are issued before any product, so one CU keeps the whole gate in flight.
+// v holds chunk 0, loaded before h was staged.
+template <int DT, int MR>
+__device__ void gate_logits_all(const RouterArgs &a, const float *hs, int lane, const GateWork &g, uint4 *v,
+                                double *zs) {
+  constexpr int NC = 16 / MR;  // chunks held at once
+  uint4 w[NC - 1][MR];
+#pragma unroll
+  for (int c = 1; c < NC; ++c) gate_load<DT, MR>(a, lane, g, c, w[c - 1]);  // past cpr: the last chunk, unused
+  double acc[MR];
+#pragma unroll
+  for (int i = 0; i < MR; ++i) acc[i] = 0.0;
+  gate_chunk<DT, MR>(hs, a.d, lane, 0, v, acc);
+#pragma unroll
+  for (int c = 1; c < NC; ++c)
+    if (c < g.cpr) gate_chunk<DT, MR>(hs, a.d, lane, c, w[c - 1], acc);
+#pragma unroll
+  for (int i = 0; i < MR; ++i) {
+    const double z = wave_sum_d_to_lane63(acc[i]);
+    if (i < g.m && lane == kWave - 1) zs[g.first + g.stride * i] = z;
+  }
+}
+
+// v holds chunk 0 of the wave's rows, loaded by gate_load(.., 0, v) before h
+// was staged; logit `row` goes to zs[row].
+template <int DT, int MR>
 __device__ void gate_logits(const RouterArgs &a, const float *hs, int lane, const GateWork &g, uint4 *v,
                             double *zs) {
+  if (g.cpr * MR <= 16) {  // the same for the whole wave
+    gate_logits_all<DT, MR>(a, hs, lane, g, v, zs);
+    return;
+  }
   constexpr int EPL = DT == 1 ? 8 : 4;
-  const int d = a.d, n = g.n, cpr = g.cpr;
-  double acc = 0.0;
-  for (int j0 = 0; j0 < n; j0 += kBatch) {
-    if (j0 > 0) gate_load<DT>(a, lane, g, j0, v);
+  const int d = a.d, cpr = g.cpr;
+  double acc[MR];
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int j = j0 + u;
-      if (j < n) {
-        const int c = j % cpr;
-        const int col = c * kWave * EPL + lane * EPL;
-        if (col < d) {
-          const float4 h0 = *reinterpret_cast<const float4 *>(hs + col);
-          if (DT == 1) {
-            const float4 h1 = *reinterpret_cast<const float4 *>(hs + col + 4);
-            float f[8];
-            bf16x8_to_f32(v[u], f);
-            acc = fma((double)f[0], (double)h0.x, acc);
-            acc = fma((double)f[1], (double)h0.y, acc);
-            acc = fma((double)f[2], (double)h0.z, acc);
-            acc = fma((double)f[3], (double)h0.w, acc);
-            acc = fma((double)f[4], (double)h1.x, acc);
-            acc = fma((double)f[5], (double)h1.y, acc);
-            acc = fma((double)f[6], (double)h1.z, acc);
-            acc = fma((double)f[7], (double)h1.w, acc);
-          } else {
-            acc = fma((double)__uint_as_float(v[u].x), (double)h0.x, acc);
-            acc = fma((double)__uint_as_float(v[u].y), (double)h0.y, acc);
-            acc = fma((double)__uint_as_float(v[u].z), (double)h0.z, acc);
-            acc = fma((double)__uint_as_float(v[u].w), (double)h0.w, acc);
-          }
+  for (int i = 0; i < MR; ++i) acc[i] = 0.0;
+  for (int c = 0; c < cpr; ++c) {
+    uint4 nv[MR];
+    gate_load<DT, MR>(a, lane, g, c + 1, nv);  // the last chunk loads itself again, unused
+    const int col = c * kWave * EPL + lane * EPL;
+    if (col < d) {
+      const float4 h0 = *reinterpret_cast<const float4 *>(hs + col);
+      if (DT == 1) {
+        const float4 h1 = *reinterpret_cast<const float4 *>(hs + col + 4);
+#pragma unroll
+        for (int i = 0; i < MR; ++i) {
+          float f[8];
+          bf16x8_to_f32(v[i], f);
+          acc[i] = fma((double)f[0], (double)h0.x, acc[i]);
+          acc[i] = fma((double)f[1], (double)h0.y, acc[i]);
+          acc[i] = fma((double)f[2], (double)h0.z, acc[i]);
+          acc[i] = fma((double)f[3], (double)h0.w, acc[i]);
+          acc[i] = fma((double)f[4], (double)h1.x, acc[i]);
+          acc[i] = fma((double)f[5], (double)h1.y, acc[i]);
+          acc[i] = fma((double)f[6], (double)h1.z, acc[i]);
+          acc[i] = fma((double)f[7], (double)h1.w, acc[i]);
         }
-        if (c == cpr - 1) {
-          const double z = wave_sum_d(acc);
-          if (lane == 0) zs[g.first + g.stride * (j / cpr)] = z;
-          acc = 0.0;
+      } else {
+#pragma unroll
+        for (int i = 0; i < MR; ++i) {
+          acc[i] = fma((double)__uint_as_float(v[i].x), (double)h0.x, acc[i]);
+          acc[i] = fma((double)__uint_as_float(v[i].y), (double)h0.y, acc[i]);
+          acc[i] = fma((double)__uint_as_float(v[i].z), (double)h0.z, acc[i]);
+          acc[i] = fma((double)__uint_as_float(v[i].w), (double)h0.w, acc[i]);
         }
       }
     }
+#pragma unroll
+    for (int i = 0; i < MR; ++i) v[i] = nv[i];
+  }
+#pragma unroll
+  for (int i = 0; i < MR; ++i) {
+    const double z = wave_sum_d_to_lane63(acc[i]);
+    if (i < g.m && lane == kWave - 1) zs[g.first + g.stride * i] = z;
   }
 }
 
@@ -390,6 +474,9 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
   if (add) st->v[lane] = tv.stat + add;
 }
 
+// MR: most gate rows a wave holds at once.  TWO: the demand rows (0..E-1) and
+// the speculative rows (E..2E-1) in two passes, each within MR rows a wave.
+template <int MR, bool TWO>
 __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   __shared__ __align__(16) float hs[kMaxD];
   __shared__ double zs[2 * kMaxE];
@@ -415,15 +502,16 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   const int r0 = route_here ? 0 : E, r1 = spec ? 2 * E : E;
   double zv = 0.0;  // clamped index, not a guarded load (one would be waited for on the spot)
   if (phase == 2) zv = a.zbuf[min(r0 + tid, 2 * kMaxE - 1)];
-  uint4 gv[kBatch];
+  uint4 gv[MR];
   GateWork gw;
+  const int r1a = TWO ? E : r1;  // rows of the first pass
   if (phase != 2 && (route_here || spec)) {
-    gw = a.dtype == 1 ? gate_work<1>(a, r0, r1, wave) : gate_work<0>(a, r0, r1, wave);
-    if (gw.n > 0) {
+    gw = a.dtype == 1 ? gate_work<1>(a, r0, r1a, wave) : gate_work<0>(a, r0, r1a, wave);
+    if (gw.m > 0) {
       if (a.dtype == 1)
-        gate_load<1>(a, lane, gw, 0, gv);
+        gate_load<1, MR>(a, lane, gw, 0, gv);
       else
-        gate_load<0>(a, lane, gw, 0, gv);
+        gate_load<0, MR>(a, lane, gw, 0, gv);
     }
   }
   if (tid == 0) {
@@ -447,10 +535,24 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     __syncthreads();
     if (phase != 2) {
       double *zout = phase == 1 ? a.zbuf : zs;
-      if (a.dtype == 1)
-        gate_logits<1>(a, hs, lane, gw, gv, zout);
-      else
-        gate_logits<0>(a, hs, lane, gw, gv, zout);
+      if (gw.m > 0) {  // the same for the whole wave
+        if (a.dtype == 1)
+          gate_logits<1, MR>(a, hs, lane, gw, gv, zout);
+        else
+          gate_logits<0, MR>(a, hs, lane, gw, gv, zout);
+      }
+      if (TWO) {  // the speculative rows
+        const GateWork g2 = a.dtype == 1 ? gate_work<1>(a, E, r1, wave) : gate_work<0>(a, E, r1, wave);
+        if (g2.m > 0) {
+          if (a.dtype == 1) {
+            gate_load<1, MR>(a, lane, g2, 0, gv);
+            gate_logits<1, MR>(a, hs, lane, g2, gv, zout);
+          } else {
+            gate_load<0, MR>(a, lane, g2, 0, gv);
+            gate_logits<0, MR>(a, hs, lane, g2, gv, zout);
+          }
+        }
+      }
     }
   }
   if (phase == 1) return;  // the GEMV launch is done; the next launch reads zbuf
@@ -511,23 +613,48 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
 
 }  // namespace
 
+#ifndef MOE_ROUTER_ONE_LAUNCH_ROWS
+#define MOE_ROUTER_ONE_LAUNCH_ROWS 128
+#endif
+
 hipError_t launch_router(const RouterArgs &a, const Launch &l) {
-  // One workgroup converts and multiplies in fp64 at about 1 us per 16 gate
-  // rows on MI355X; beyond 32 rows (32 or 64 experts) the GEMV runs as its
-  // own launch, one row per wave, and the table work as a second one.  (A
-  // single launch whose last workgroup took over cost about 7 us in fences.)
+  // Up to MOE_ROUTER_ONE_LAUNCH_ROWS gate rows (every case of this build:
+  // at most 64 experts, twice that when speculating) run in one workgroup,
+  // each wave accumulating its up to 4 rows at once.  Beyond that the GEMV is
+  // a launch of its own, one row per wave, and the table work a second one.
+  // (A single launch whose last workgroup took over cost about 7 us in
+  // device-scope fences.)
   const int rows = (a.demand && a.inj_ids == nullptr ? a.E : 0) + (a.spec_layer >= 0 ? a.E : 0);
-  if (rows <= 32) {
+  if (rows <= MOE_ROUTER_ONE_LAUNCH_ROWS) {
     RouterArgs one = a;
     one.phase = 0;
-    MOE_LAUNCH(router_kernel, dim3(1), dim3(kThreads), 0, l, one);
+    // beyond 4 rows a wave (64 experts with speculation) the demand and the
+    // speculative rows go in two passes: 8 rows at once would spill
+    const bool two = (rows + kWaves - 1) / kWaves > 4 && a.demand && a.inj_ids == nullptr && a.spec_layer >= 0;
+    const int per_wave = ((two ? a.E : rows) + kWaves - 1) / kWaves;
+    if (per_wave > 4) return hipErrorInvalidValue;  // cannot happen with at most 64 experts
+#define MOE_ROUTER_ONE(MR)                                                          \
+  do {                                                                              \
+    if (two)                                                                        \
+      MOE_LAUNCH((router_kernel<MR, true>), dim3(1), dim3(kThreads), 0, l, one);    \
+    else                                                                            \
+      MOE_LAUNCH((router_kernel<MR, false>), dim3(1), dim3(kThreads), 0, l, one);   \
+  } while (0)
+    if (per_wave <= 1)
+      MOE_ROUTER_ONE(1);
+    else if (per_wave <= 2)
+      MOE_ROUTER_ONE(2);
+    else
+      MOE_ROUTER_ONE(4);
+#undef MOE_ROUTER_ONE
     return hipGetLastError();
   }
   RouterArgs g = a, t = a;
   g.phase = 1;
   t.phase = 2;
-  MOE_LAUNCH(router_kernel, dim3((rows + kWaves - 1) / kWaves), dim3(kThreads), 0, (Launch{l.s, l.start, nullptr}), g);
-  MOE_LAUNCH(router_kernel, dim3(1), dim3(kThreads), 0, (Launch{l.s, nullptr, l.stop}), t);
+  MOE_LAUNCH((router_kernel<1, false>), dim3((rows + kWaves - 1) / kWaves), dim3(kThreads), 0,
+             (Launch{l.s, l.start, nullptr}), g);
+  MOE_LAUNCH((router_kernel<1, false>), dim3(1), dim3(kThreads), 0, (Launch{l.s, nullptr, l.stop}), t);
   return hipGetLastError();
 }
 
