@@ -190,6 +190,8 @@ hipError_t launch_ffn_up(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_down(const FfnArgs &a, int dtype, const Launch &l);
 hipError_t launch_ffn_reduce(const FfnArgs &a, int dtype, const Launch &l);
 int ffn_down_chunks(int K, int d_ff, int dtype);
+// True when launch_ffn_down also adds the partials into h (no reduce launch).
+bool ffn_down_fused(int K, int d_ff, int dtype);
 // group-quantised experts (dtype 2)
 hipError_t launch_ffnq_up(const FfnArgs &a, const Launch &l);
 hipError_t launch_ffnq_down(const FfnArgs &a, const Launch &l);

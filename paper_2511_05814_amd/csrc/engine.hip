@@ -846,9 +846,11 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_DOWN));
     HIP_TRY(c, launch_ffn_down(f, c->dtype, ld));
     kernel_span_done(c, SPAN_DOWN, ld);
-    HIP_TRY(c, kernel_span(c, c->cs, &lx, SPAN_REDUCE));
-    HIP_TRY(c, launch_ffn_reduce(f, c->dtype, lx));
-    kernel_span_done(c, SPAN_REDUCE, lx);
+    if (!ffn_down_fused(c->K, c->dff, c->dtype)) {
+      HIP_TRY(c, kernel_span(c, c->cs, &lx, SPAN_REDUCE));
+      HIP_TRY(c, launch_ffn_reduce(f, c->dtype, lx));
+      kernel_span_done(c, SPAN_REDUCE, lx);
+    }
     c->last_route_kind = 1;
   }
   if (spec_layer >= 0 && split && !no_copies) {

@@ -17,7 +17,8 @@
 // The down projection is split along its reduction axis (rank, column chunk)
 // so that enough workgroups stream at once; each chunk writes a partial row
 // sum and a small kernel adds the partials in a fixed order, so the result
-// does not depend on scheduling.  Tile shapes were swept on MI355X at the
+// does not depend on scheduling.  Narrow experts (one chunk per rank) add the
+// rank partials inside the down kernel, in the same order, instead.  Tile shapes were swept on MI355X at the
 // Mixtral (d 4096, d_ff 14336) and 64-expert (d 2048, d_ff 1408) shapes.
 #include "common.hpp"
 
@@ -33,6 +34,11 @@ constexpr int kUpRows = 2;     // rows per wave (register path)
 constexpr int kUpRowsNarrow = MOE_FFN_UP_ROWS_NARROW;  // the same for d <= 2048 (2 or 4)
 constexpr int kUpLdsRows = 1;  // row pairs per wave on the wide-model path
 constexpr int kReduceThreads = 64;
+constexpr int kFusedThreads = 512;  // fused down: eight waves, one rank each
+#ifndef MOE_FFN_DOWN_FUSED_ROWS
+#define MOE_FFN_DOWN_FUSED_ROWS 4
+#endif
+constexpr int kFusedRows = MOE_FFN_DOWN_FUSED_ROWS;  // rows of h per workgroup
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -286,6 +292,50 @@ __global__ __launch_bounds__(kThreads) void ffn_down_kernel(FfnArgs a) {
   }
 }
 
+// down for narrow experts (each rank's row in one column chunk): the eight
+// waves of a workgroup share its RPW rows of h, wave w taking ranks w, w + 8,
+// ...; the rank partials meet in LDS and are added in rank order (the order
+// the reduction below uses) and into h, so no partial-sum buffer and no
+// second launch are needed.
+template <int DT, int STEPS, int RPW, bool RAGGED>
+__global__ __launch_bounds__(kFusedThreads) void ffn_down_fused_kernel(FfnArgs a) {
+  using E = Elem<DT>;
+  using T = typename E::T;
+  constexpr int V = E::kVec, W = kFusedThreads / kWave;
+  const int d = a.d, d_ff = a.d_ff, K = a.route->k;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int row0 = blockIdx.x * RPW;
+  __shared__ float dots[kMaxK][RPW];
+  for (int rank = wave; rank < a.K; rank += W) {
+    const int slot = rank < K ? a.route->slot[rank] : -1;
+    const bool valid = rank < K && slot >= 0 && slot < a.S;
+    float acc[RPW] = {};
+    if (valid) {
+      float x[STEPS][V];
+      load_x<V, STEPS, RAGGED>(a.act + (size_t)rank * d_ff, d_ff, lane, a.route->g[rank], x);
+      // rows past d re-read row d - 1 (not written)
+      const T *w2 = reinterpret_cast<const T *>(a.arena + ((size_t)a.layer * a.S + slot) * a.expert_bytes) +
+                    2 * (size_t)d_ff * d;
+      uint4 u[RPW][STEPS];
+#pragma unroll
+      for (int q = 0; q < RPW; ++q) load_row_strided<DT, STEPS, RAGGED>(w2, min(row0 + q, d - 1), d_ff, d_ff, lane, u[q]);
+#pragma unroll
+      for (int q = 0; q < RPW; ++q) acc[q] = row_dot<DT, STEPS>(u[q], x);
+    }
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      const float s = wave_sum(acc[q]);
+      if (lane == 0) dots[rank][q] = s;
+    }
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < RPW && row0 + (int)threadIdx.x < d) {
+    float sum = 0.0f;
+    for (int r = 0; r < a.K; ++r) sum += dots[r][threadIdx.x];
+    a.h[row0 + threadIdx.x] += sum;
+  }
+}
+
 // h += sum over chunks of the partial row sums, in chunk order; the loads of
 // eight chunks are issued together.
 __global__ __launch_bounds__(kReduceThreads) void ffn_reduce_kernel(const float *__restrict__ part, int nch,
@@ -328,6 +378,9 @@ void launch_up_steps(bool ragged, const FfnArgs &a, const Launch &l) {
 
 template <int DT, int STEPS>
 void launch_up_rows(bool ragged, const FfnArgs &a, const Launch &l) {
+  // rows of fewer than STEPS whole steps (d = 1536 in bf16 on the 4-step
+  // kernel) take the ragged form, which reads zeros past d
+  ragged = ragged || a.d != STEPS * kWave * Elem<DT>::kVec;
   if (a.d <= 2048 && kUpRowsNarrow == 4)
     launch_up_steps<DT, STEPS, 4>(ragged, a, l);
   else
@@ -362,9 +415,38 @@ void launch_down_shape(dim3 grid, bool ragged, const FfnArgs &a, const Launch &l
     MOE_LAUNCH((ffn_down_kernel<DT, STEPS, RPW, false>), grid, dim3(kThreads), 0, l, a);
 }
 
+template <int DT, int STEPS>
+void launch_down_fused(bool ragged, const FfnArgs &a, const Launch &l) {
+  const dim3 grid((a.d + kFusedRows - 1) / kFusedRows);
+  if (ragged)
+    MOE_LAUNCH((ffn_down_fused_kernel<DT, STEPS, kFusedRows, true>), grid, dim3(kFusedThreads), 0, l, a);
+  else
+    MOE_LAUNCH((ffn_down_fused_kernel<DT, STEPS, kFusedRows, false>), grid, dim3(kFusedThreads), 0, l, a);
+}
+
+#ifndef MOE_FFN_DOWN_FUSE
+#define MOE_FFN_DOWN_FUSE 1
+#endif
+
+bool down_fused(int K, int d_ff, int dtype) {
+  if (!MOE_FFN_DOWN_FUSE || (dtype != 0 && dtype != 1)) return false;
+  const int cols = kWave * (dtype == 1 ? 8 : 4);
+  return K <= kMaxK && d_ff <= 4 * cols;
+}
+
 template <int DT>
 hipError_t launch_down_t(const FfnArgs &a, const Launch &l) {
   const DownShape sh = down_shape(a.d_ff, DT);
+  if (down_fused(a.K, a.d_ff, DT)) {
+    const bool ragged = a.d_ff % (sh.steps * kWave * Elem<DT>::kVec) != 0;
+    switch (sh.steps) {
+      case 1: launch_down_fused<DT, 1>(ragged, a, l); break;
+      case 2: launch_down_fused<DT, 2>(ragged, a, l); break;
+      case 3: launch_down_fused<DT, 3>(ragged, a, l); break;
+      default: launch_down_fused<DT, 4>(ragged, a, l); break;
+    }
+    return hipGetLastError();
+  }
   const int rows = kWavesPerBlock * sh.rows;
   const int ch = sh.steps * kWave * Elem<DT>::kVec;
   const dim3 grid(((a.d + rows - 1) / rows) * ffn_down_chunks(a.K, a.d_ff, DT));
@@ -378,6 +460,8 @@ hipError_t launch_down_t(const FfnArgs &a, const Launch &l) {
 }
 
 }  // namespace
+
+bool ffn_down_fused(int K, int d_ff, int dtype) { return down_fused(K, d_ff, dtype); }
 
 int ffn_down_chunks(int K, int d_ff, int dtype) {
   if (dtype == 2) return ffnq_down_chunks(K, d_ff);

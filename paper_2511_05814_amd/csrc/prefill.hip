@@ -40,7 +40,6 @@ typedef double double4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kGateTok = 16;     // tokens per gate workgroup
 constexpr int kKStep = 32;       // GEMM reduction step (one MFMA depth)
-constexpr int kLdsK = kKStep;  // LDS row of one K slice (bf16 elements), 16-byte chunks swizzled
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);

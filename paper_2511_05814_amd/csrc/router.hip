@@ -10,9 +10,12 @@
 // are accumulated in fp64 so that the top-K decision is the one an fp64
 // evaluation makes.
 //
-// Then one wave owns each cache table: lane e holds expert e's slot, use count,
-// last-use tick and prefetched flag, and the K lookups of the token are
-// applied in rank order with wave-wide argmin reductions choosing the victim
+// The whole workgroup then counts the top-K ranks (each thread compares one
+// logit with an eighth of the others).  One wave owns each cache table: lane e
+// holds expert e's slot, use count, last-use tick and prefetched flag.  When
+// every selected expert is resident the K lookups change K distinct lanes and
+// evict nothing, so they are applied at once; otherwise they are applied one
+// by one in rank order, with wave-wide argmin reductions choosing the victim
 // (LRU, Sec. 3.1: smallest last-use tick; LFU, Sec. 4.2: smallest count, then
 // last-use tick; aged LFU, after Sec. 6.1: the count halved once per fixed
 // number of ticks since the last use, then last-use tick; then lower slot).
@@ -275,6 +278,10 @@ __device__ int wave_victim(bool cand, int policy, int aging, int64_t clock, uint
 // Value of x on lane src, for a src the whole wave agrees on (a scalar read,
 // not an LDS round trip like a general shuffle).
 __device__ __forceinline__ int lane_value(int x, int src) { return __builtin_amdgcn_readlane(x, src); }
+__device__ __forceinline__ double lane_value_d(double x, int src) {
+  return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(x), src),
+                          __builtin_amdgcn_readlane(__double2loint(x), src));
+}
 
 // Ring position of record base + r, from base % cap computed once.
 __device__ __forceinline__ uint64_t ring_pos(uint64_t base_pos, int r, uint64_t cap, int K) {
@@ -313,12 +320,38 @@ __device__ void demand_lookup(const RouterArgs &a, int idreg, int lane, uint64_t
   int64_t clock = tv.clock;
   const int64_t token = tv.lookups;
 
-  bool pinned = false;
-  for (int r = 0; r < K; ++r) pinned |= (lane_value(idreg, r) == lane);
+  int my_rank = -1;  // the rank that selected this lane's expert (ids are distinct)
+  for (int r = 0; r < K; ++r) my_rank = lane_value(idreg, r) == lane ? r : my_rank;
+  const bool pinned = my_rank >= 0;
   const uint64_t base_pos = a.trace_cap ? rec_base % a.trace_cap : 0;
 
+  // Rank lane r's expert: its slot and prefetched flag before the lookups.
+  const int j_l = lane < K ? idreg : 0;
+  const int slot_l = __shfl(my_slot, j_l, kWave);
+  const int pf_l = __shfl(my_pf, j_l, kWave);
+  const bool all_hit = __ballot(lane < K && slot_l < 0) == 0;
+
   int n_miss = 0, hits = 0, useful = 0, wasted = 0;
-  for (int r = 0; r < K; ++r) {
+  if (all_hit) {
+    // Nothing is evicted, so the K lookups touch K distinct lanes and run at
+    // once: rank r's use is tick clock + r + 1, as in the sequence below.
+    if (pinned) {
+      my_count += 1;
+      my_last = clock + my_rank + 1;
+      my_pf = 0;
+    }
+    clock += K;
+    hits = K;
+    useful = __popcll(__ballot(lane < K && pf_l != 0));
+    if (lane < K) {
+      const int flags = 1 | (pf_l ? 2 : 0);
+      a.route->ids[lane] = idreg;
+      a.route->slot[lane] = slot_l;
+      a.route->hit[lane] = 1;
+      put_rec(a, ring_pos(base_pos, lane, a.trace_cap, K), REC_ACCESS, token, a.layer, lane, idreg, flags, slot_l, -1);
+    }
+  }
+  for (int r = 0; r < (all_hit ? 0 : K); ++r) {
     const int j = lane_value(idreg, r);
     clock += 1;
     const int slot_j = lane_value(my_slot, j);
@@ -417,8 +450,14 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
   for (int r = 0; r < K; ++r) pinned |= (lane_value(greg, r) == lane);
   const uint64_t base_pos = a.trace_cap ? rec_base % a.trace_cap : 0;
 
+  // Every guess already resident: nothing to insert, only the records.
+  const int slot_l = __shfl(my_slot, lane < K ? greg : 0, kWave);
+  const bool all_res = __ballot(lane < K && slot_l < 0) == 0;
+  if (all_res && lane < K)
+    put_rec(a, ring_pos(base_pos, lane, a.trace_cap, K), REC_PREFETCH, token, L2, lane, greg, 1, slot_l, -1);
+
   int issued = 0, wasted = 0;
-  for (int r = 0; r < K; ++r) {
+  for (int r = 0; r < (all_res ? 0 : K); ++r) {
     const int j = lane_value(greg, r);
     const int slot_j = lane_value(my_slot, j);
     int flags = 0, slot = -1, victim = -1;
@@ -474,6 +513,46 @@ __device__ void prefetch_insert(const RouterArgs &a, int greg, int lane, uint64_
   if (add) st->v[lane] = tv.stat + add;
 }
 
+// Top-K of the logits in rank order: larger z first, lower id on ties, NaN
+// ranked as -inf.  An expert's rank is the number of logits that come before
+// it in that order; the whole workgroup counts, thread t taking expert t % 64
+// of set t / 512 (0: this layer's logits zs[0, E), 1: the next layer's
+// zs[E, 2E)) against the part (t / 64) % 8 of the other logits.
+constexpr int kRankParts = 8;
+static_assert(kThreads == 2 * kRankParts * kMaxE, "one thread per (set, part, expert)");
+
+__device__ __forceinline__ void rank_parts(const double *zs, int E, bool set0, bool set1, int tid,
+                                           int (*cnt)[kRankParts][kMaxE]) {
+  const int set = tid / (kRankParts * kMaxE), part = (tid / kMaxE) % kRankParts, e = tid % kMaxE;
+  if (e >= E || !(set == 0 ? set0 : set1)) return;
+  const double *z = zs + set * E;
+  const double mine = rank_key(z[e]);
+  const int per = (E + kRankParts - 1) / kRankParts;
+  const int o0 = part * per, o1 = min(E, o0 + per);
+  int n = 0;
+  for (int o = o0; o < o1; ++o) {
+    const double zo = rank_key(z[o]);
+    n += (zo > mine || (zo == mine && o < e)) ? 1 : 0;
+  }
+  cnt[set][part][e] = n;
+}
+
+// One wave: lane e < E adds its part counts into its rank, rank r < K writes
+// its expert to out[r] (LDS of this wave).  Returns out[lane] on lanes < K,
+// -1 elsewhere.
+__device__ __forceinline__ int topk_from_parts(const int (*cnt)[kMaxE], int E, int K, int lane, int *out) {
+  if (lane < E) {
+    int rank = 0;
+#pragma unroll
+    for (int p = 0; p < kRankParts; ++p) rank += cnt[p][lane];
+    if (rank < K) out[rank] = lane;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  return lane < K ? out[lane] : -1;
+}
+
 // MR: most gate rows a wave holds at once.  TWO: the demand rows (0..E-1) and
 // the speculative rows (E..2E-1) in two passes, each within MR rows a wave.
 template <int MR, bool TWO>
@@ -482,7 +561,7 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   __shared__ double zs[2 * kMaxE];
   __shared__ int s_top[2][kMaxK];
   __shared__ double red[kWaves];
-  __shared__ double s_rms;
+  __shared__ int s_cnt[2][kRankParts][kMaxE];
   __shared__ uint64_t s_tbase;
   __shared__ int s_demand_ok;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -557,23 +636,20 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   }
   if (phase == 1) return;  // the GEMV launch is done; the next launch reads zbuf
   __syncthreads();
-  if (route_here && tid == 0) {
-    double t = 0.0;
-    for (int w = 0; w < kWaves; ++w) t += red[w];
-    s_rms = sqrt(t / (double)d + 1e-5);
-  }
+  rank_parts(zs, E, route_here, spec, tid, s_cnt);
   __syncthreads();
 
   if (wave == 0 && a.demand) {
     int idreg;
     if (route_here) {
-      idreg = wave_topk_lds(zs, E, a.K, lane, s_top[0]);
+      idreg = topk_from_parts(s_cnt[0], E, a.K, lane, s_top[0]);
       // renormalised softmax over the selected logits z / rms (rank 0 is the max)
-      double zr = (lane < a.K) ? zs[idreg < 0 ? 0 : idreg] : 0.0;
-      const double r = s_rms;
-      const double z0 = __shfl(zr, 0, kWave);
+      const double zr = (lane < a.K) ? zs[idreg < 0 ? 0 : idreg] : 0.0;
+      const double ss = lane_value_d(wave_sum_d_to_lane63(lane < kWaves ? red[lane] : 0.0), kWave - 1);
+      const double r = sqrt(ss / (double)d + 1e-5);
+      const double z0 = lane_value_d(zr, 0);
       const double ex = (lane < a.K) ? exp((zr - z0) / r) : 0.0;
-      const double den = wave_sum_d(ex);
+      const double den = lane_value_d(wave_sum_d_to_lane63(ex), kWave - 1);
       if (lane < a.K) a.route->g[lane] = (float)(ex / den);
       if (lane == 0) a.route->inv_r = (float)(1.0 / r);
     } else {
@@ -603,7 +679,7 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     }
   }
   if (wave == 1 && spec) {
-    const int greg = wave_topk_lds(zs + E, E, a.K, lane, s_top[1]);
+    const int greg = topk_from_parts(s_cnt[1], E, a.K, lane, s_top[1]);
     prefetch_insert(a, greg, lane, s_tbase + (a.demand ? (uint64_t)a.K : 0), tv);
   }
   __syncthreads();

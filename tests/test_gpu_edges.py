@@ -57,6 +57,22 @@ def test_largest_top_k():
     rig.store.close()
 
 
+@pytest.mark.parametrize("dtype,d_model", [("bf16", 1536), ("f32", 768)])
+def test_rows_of_fewer_steps_than_the_up_kernel_width(dtype, d_model):
+    # three 16-byte steps a lane while the up kernel is built for four: the
+    # fourth step must read zeros, not the next row and h past its end
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=2, experts=4, top_k=2, d_model=d_model, d_ff=256,
+                                         dtype=dtype, tokens=10)
+    _say("d_model", d_model, dtype)
+    rig = Rig(cfg)
+    moe = rig.cache(4, "lfu")
+    hs, recs, _ = rig.run(moe, cfg.tokens)
+    worst, _, _ = check_decode(cfg, rig.model, hs, recs, 4, "lfu", tol=_tol(cfg))
+    _say("worst", worst)
+    moe.close()
+    rig.store.close()
+
+
 def test_trace_ring_overflow_keeps_the_newest_records():
     cfg = wl.CONFIGS["tiny-stack"].with_(tokens=16)
     rig = Rig(cfg)
