@@ -123,6 +123,36 @@ def measure_hbm_read(torch, b, nbytes=1 << 30, reps=20):
     return gbps
 
 
+def measure_hbm_window(torch, b, nbytes, span=3 << 30, rounds=3):
+    """One-shot read of `nbytes` by the same probe, one launch a window, the
+    windows rotating over `span` bytes (well beyond the 256 MB MALL) so that
+    every launch reads from HBM: what a single launch of that many bytes costs
+    on this device, ramp and drain included.  Returns (median us, GB/s)."""
+    nbytes -= nbytes % 4096
+    span = max(span, 4 * nbytes)
+    buf = torch.zeros(span, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream().cuda_stream
+    us = []
+    for _ in range(rounds):
+        for i in range(span // nbytes):
+            gbps = b.moe_probe_hbm_read(buf.data_ptr() + i * nbytes, nbytes, 1, stream)
+            us.append(nbytes / gbps / 1e3)
+    del buf
+    us.sort()
+    med = us[len(us) // 2]
+    return med, nbytes / (med * 1e-6) / 1e9
+
+
+def same_bytes_probe(torch, b, nbytes, kernel_us):
+    med, gbps = measure_hbm_window(torch, b, nbytes)
+    log(f"one-shot read of {nbytes} B: {med:.2f} us ({gbps:.1f} GB/s)")
+    return {"bytes": nbytes, "median_us": round(med, 2), "gbps": round(gbps, 1),
+            "roofline_kernel_frac_of_probe": round(med / kernel_us, 4) if kernel_us else None,
+            "is": "the same probe reading the roofline kernel's bytes once per launch, launches rotating "
+                  "over 3 GiB so each reads HBM; the ratio is probe time / kernel time"}
+
+
 def calibrate_counters(torch, nbytes=512 << 20):
     """One plain device-to-device copy of known size (512 MiB read, 512 MiB
     written), so that hardware byte counters collected on this program can be
@@ -555,7 +585,8 @@ def stack_main(args):
                      "reduce_avg_us": round(1e3 * bt["ffn_reduce_ms"] / max(1, bt["ffn_reduce_n"]), 2),
                      "from": f"the {bd_tokens}-token pass with every launch timed"},
         "hbm_read_probe": {"kernel": "hbm_read_probe_kernel", "gbps": round(hbm_probe, 1), "bytes": 1 << 30,
-                           "roofline_kernel_frac_of_probe": round(up_gbps / hbm_probe, 4) if hbm_probe else None},
+                           "roofline_kernel_frac_of_probe": round(up_gbps / hbm_probe, 4) if hbm_probe else None,
+                           "same_bytes": same_bytes_probe(torch, b, up_bytes, up_ms * 1e3)},
         "mfma_bf16_probe_tflops": mfma,
         "link_roofline": {
             "kernel": "fetch_kernel",
@@ -801,6 +832,7 @@ def layer_main(args):
             "bytes": 1 << 30,
             "roofline_kernel_frac_of_probe": round(up_gbps / hbm_probe, 4) if hbm_probe else None,
             "is": "a streaming read with nothing else to do (one workgroup per CU, 8 16-byte loads in flight a lane)",
+            "same_bytes": same_bytes_probe(torch, b, up_bytes, up_ms * 1e3),
         },
         "link_roofline": {
             "kernel": "fetch_kernel",

@@ -225,8 +225,8 @@ int moe_decode_layer(moe_cache_t *c, int layer, float *h, int flags);
 /* moe_decode_layer for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc).  Same arguments, work and results as moe_decode_layer (the
- * same kernels), but the call's scratch (the FFN's top_k x d_ff activations,
- * its partial row sums of d_model rows, the router's logits) lives in a
+ * same kernels), but the call's scratch (the FFN's top_k x d_ff activations
+ * and its partial row sums of d_model rows) lives in a
  * static 4 MiB device array that the library holds on each device until the
  * process ends, instead of the bound workspace; the call allocates nothing
  * (no hipMalloc, no event creation).  Every call on one device shares that

@@ -74,7 +74,11 @@ struct RouterArgs {
   RouteOut *route;
   TraceRec *trace;
   int32_t *err;
-  uint64_t *trace_count;   // records written so far (ring position = count % cap)
+  // Records written so far (ring position = count % cap).  A launch reads
+  // trace_in and writes the new count to trace_out, a second word, so that
+  // the workgroups of one launch never see a count another of them updated.
+  const uint64_t *trace_in;
+  uint64_t *trace_out;
   uint64_t trace_cap;
   uint64_t expert_bytes;
   int layer, L, E, S, K, d, dtype, policy;
@@ -82,8 +86,6 @@ struct RouterArgs {
   int demand;              // 1: route + look up `layer`
   int spec_layer;          // >= 0: guess that layer's experts from h and prefetch
   int pmax;                // prefetch at most this many guesses
-  double *zbuf;            // [2 * kMaxE] gate logits when the GEMV is a launch of its own
-  int phase;               // 0: one launch; 1: GEMV over several workgroups; 2: the rest
 };
 
 struct FfnArgs {
@@ -134,7 +136,8 @@ struct PlanArgs {
   LayerTable *table;
   LayerStats *stats;
   TraceRec *trace;
-  uint64_t *trace_count;
+  const uint64_t *trace_in;  // record count before / after, as in RouterArgs
+  uint64_t *trace_out;
   uint64_t trace_cap;
   int32_t *err;
   uint64_t expert_bytes;

@@ -47,7 +47,7 @@ int fail(int code, const char *fmt, ...) {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Layout {
-  size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, rz = 0, act = 0, part = 0,
+  size_t tables = 0, stats = 0, dlists = 0, plists = 0, route = 0, err = 0, act = 0, part = 0,
          hostptrs = 0, prefill = 0, staging = 0, total = 0;
 };
 
@@ -224,7 +224,11 @@ struct moe_cache {
   FetchList *dl = nullptr, *pl = nullptr;
   RouteOut *route = nullptr;
   int32_t *err = nullptr;
-  uint64_t *trace_count = nullptr;  // device: records written to the trace ring
+  // device: records written to the trace ring, two words; each launch that
+  // writes records reads trace_count[tpar] and writes trace_count[1 - tpar],
+  // and the host flips tpar once it is enqueued
+  uint64_t *trace_count = nullptr;
+  int tpar = 0;
   float *act = nullptr, *part = nullptr;
   uint8_t *prefill_ws = nullptr;
   std::vector<const uint8_t *> host_layer;  // host address of layer l's experts
@@ -442,7 +446,6 @@ static Layout make_layout(const moe_cache *c, const moe_model_desc *d) {
   l.route = take(sizeof(RouteOut));
   l.hostptrs = take(sizeof(void *) * c->L);
   l.err = take(256);
-  l.rz = take(sizeof(double) * 2 * kMaxE);  // router logits of a separate GEMV launch
   l.act = take(sizeof(float) * d->top_k * (size_t)d->d_ff);
   l.part = take(sizeof(float) * (size_t)ffn_down_chunks(d->top_k, d->d_ff, d->dtype) * d->d_model);
   const uint64_t B = expert_bytes(d);
@@ -605,8 +608,8 @@ int moe_cache_reset(moe_cache_t *c) {
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.dlists, 0, sizeof(FetchList) * c->L, c->cs));
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.plists, 0, sizeof(FetchList) * c->L, c->cs));
   HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.route, 0, sizeof(RouteOut), c->cs));
-  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.err, 0, 256, c->cs));
-  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.rz, 0, sizeof(double) * 2 * kMaxE, c->cs));
+  HIP_TRY(c, hipMemsetAsync(c->ws + c->lay.err, 0, 256, c->cs));  // error word and both trace counts
+  c->tpar = 0;
   {
     // the copy kernel dereferences this table: check it survived
     std::vector<const uint8_t *> got(c->L);
@@ -709,15 +712,12 @@ static int issue_fetch(moe_cache *c, FetchList *list, int mirror_idx, hipStream_
 }
 
 // Router (+ fetches, + FFN) for one call.  spec_layer < 0: no speculation.
-// Scratch of one call: FFN activations and partial sums, router logits.
+// Scratch of one call: FFN activations and partial sums.
 struct CallScratch {
   float *act, *part;
-  double *zbuf;
 };
 
-static CallScratch workspace_scratch(moe_cache *c) {
-  return {c->act, c->part, reinterpret_cast<double *>(c->ws + c->lay.rz)};
-}
+static CallScratch workspace_scratch(moe_cache *c) { return {c->act, c->part}; }
 
 static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, int demand,
                          int spec_layer, int pmax, bool ffn, const CallScratch &scr) {
@@ -737,7 +737,8 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.route = c->route;
   a.trace = static_cast<TraceRec *>(c->desc.trace);
   a.err = c->err;
-  a.trace_count = c->trace_count;
+  a.trace_in = c->trace_count + c->tpar;
+  a.trace_out = c->trace_count + (1 - c->tpar);
   a.trace_cap = c->desc.trace ? c->desc.trace_cap : 0;
   a.expert_bytes = c->Bh;  // bytes one fetch moves (counters)
   a.layer = layer;
@@ -752,10 +753,10 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
   a.demand = demand;
   a.spec_layer = spec_layer;
   a.pmax = pmax;
-  a.zbuf = scr.zbuf;
   Launch lr;
   HIP_TRY(c, kernel_span(c, c->cs, &lr, SPAN_ROUTER));
   HIP_TRY(c, launch_router(a, lr));
+  c->tpar ^= 1;
   kernel_span_done(c, SPAN_ROUTER, lr);
   // from the router's end to the FFN's start: the compute stream's wait for
   // the copies that fill this layer's slots
@@ -928,7 +929,8 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   pa.table = c->tables + layer;
   pa.stats = c->stats + layer;
   pa.trace = static_cast<TraceRec *>(c->desc.trace);
-  pa.trace_count = c->trace_count;
+  pa.trace_in = c->trace_count + c->tpar;
+  pa.trace_out = c->trace_count + (1 - c->tpar);
   pa.trace_cap = c->desc.trace ? c->desc.trace_cap : 0;
   pa.err = c->err;
   pa.expert_bytes = c->Bh;  // bytes one fetch moves (counters)
@@ -948,6 +950,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   pa.arena_layer = arena + (size_t)layer * c->S * c->B;
   pa.slot_bytes = c->B;
   HIP_TRY(c, launch_prefill_plan(pa, Launch{c->cs}));
+  c->tpar ^= 1;
   if (device_plan) {
     const double rows = (double)T * c->K;
     Launch lu, ld;
@@ -1296,12 +1299,11 @@ int moe_decode_layer_noalloc(moe_cache_t *c, int layer, float *h, int flags) {
   if (!c->bound || !c->scratch) return fail(MOE_ERR_STATE, "handle is not bound (call moe_cache_bind)");
   const size_t act_bytes = align_up(sizeof(float) * (size_t)c->K * c->dff, 256);
   const size_t part_bytes = align_up(sizeof(float) * (size_t)ffn_down_chunks(c->K, c->dff, c->dtype) * c->d, 256);
-  const size_t z_bytes = sizeof(double) * 2 * kMaxE;
-  if (act_bytes + part_bytes + z_bytes > kNoAllocScratchBytes)
+  if (act_bytes + part_bytes > kNoAllocScratchBytes)
     return fail(MOE_ERR_ARG,
                 "this model needs %zu bytes of decode scratch (top_k * d_ff activations, partial sums of d_model "
                 "rows); the static scratch of moe_decode_layer_noalloc holds %zu: use moe_decode_layer",
-                act_bytes + part_bytes + z_bytes, kNoAllocScratchBytes);
+                act_bytes + part_bytes, kNoAllocScratchBytes);
   int rc = check_ready(c);
   if (rc != MOE_OK) return rc;
   if (c->timing != MOE_TIMING_OFF)
@@ -1310,8 +1312,7 @@ int moe_decode_layer_noalloc(moe_cache_t *c, int layer, float *h, int flags) {
   if (!h || misaligned(h, 16)) return fail(MOE_ERR_ARG, "h must be a non-NULL 16-byte aligned device pointer");
   if (flags & ~MOE_PREFETCH_NEXT) return fail(MOE_ERR_ARG, "unknown flags 0x%x", flags);
   const int spec = (flags & MOE_PREFETCH_NEXT) && layer + 1 < c->L ? layer + 1 : -1;
-  const CallScratch scr{reinterpret_cast<float *>(c->scratch), reinterpret_cast<float *>(c->scratch + act_bytes),
-                        reinterpret_cast<double *>(c->scratch + act_bytes + part_bytes)};
+  const CallScratch scr{reinterpret_cast<float *>(c->scratch), reinterpret_cast<float *>(c->scratch + act_bytes)};
   return enqueue_layer(c, layer, h, nullptr, 1, spec, c->pmax, true, scr);
 }
 
@@ -1402,7 +1403,7 @@ int moe_cache_read_trace(moe_cache_t *c, moe_trace_rec *out, size_t cap, size_t 
   if (dropped) *dropped = 0;
   if (!c->desc.trace) return MOE_OK;
   uint64_t total = 0;
-  HIP_TRY(c, hipMemcpy(&total, c->trace_count, sizeof total, hipMemcpyDeviceToHost));
+  HIP_TRY(c, hipMemcpy(&total, c->trace_count + c->tpar, sizeof total, hipMemcpyDeviceToHost));
   const uint64_t ring = c->desc.trace_cap;
   const uint64_t avail = total < ring ? total : ring;
   const uint64_t start = total - avail;

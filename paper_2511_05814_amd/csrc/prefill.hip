@@ -296,7 +296,10 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
   }
   __syncthreads();
   if (bad) {
-    if (tid == 0) *a.err = ERR_BAD_LIST;
+    if (tid == 0) {
+      *a.err = ERR_BAD_LIST;
+      *a.trace_out = *a.trace_in;
+    }
     return;
   }
   if (wave == 0) {
@@ -320,7 +323,7 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
 
   // table update: lane e = expert e
   LayerTable *T = a.table;
-  const uint64_t tbase = (a.trace && a.trace_cap) ? *a.trace_count : 0;
+  const uint64_t tbase = *a.trace_in;
   const bool in_range = lane < E;
   const int slot0 = in_range ? T->expert_slot[lane] : -1;
   uint32_t count = in_range ? T->count[lane] : 0u;
@@ -439,7 +442,7 @@ __global__ __launch_bounds__(1024) void prefill_plan_kernel(PlanArgs a) {
   if (lane == 0) {
     T->clock = clock1;
     T->lookups = token0 + a.T;
-    if (a.trace && a.trace_cap) *a.trace_count = tbase + E;
+    *a.trace_out = tbase + (a.trace && a.trace_cap ? (uint64_t)E : 0);
     LayerStats *st = a.stats;
     st->v[ST_HITS] += sh;
     st->v[ST_MISSES] += sm;

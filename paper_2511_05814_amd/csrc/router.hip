@@ -1,8 +1,8 @@
 // Router and cache-table kernel for batch-1 decode.
 //
-// One workgroup per call (a two-launch form, the GEMV spread over several
-// workgroups, remains for more gate rows than this build has).  All 16 waves
-// first compute the gate logits
+// One workgroup per role and call: routing and the table lookups of the layer
+// being decoded, and, when speculating, the guess and insertion for the next
+// layer.  All 16 waves of a workgroup first compute the gate logits
 // z = W_g h (Sec. 4.3: the gate is a linear map [len_hidden, num_experts]) for
 // the layer being decoded and, when speculating, for the next layer (Sec. 3.2:
 // the next layer's gate applied to the current hidden state).  Each product
@@ -21,7 +21,7 @@
 // number of ticks since the last use, then last-use tick; then lower slot).
 // Wave 0 serves the demand lookup of this layer, wave 1 the speculative
 // insertion into the next layer's table; the tables are disjoint, so the two
-// run concurrently.
+// run concurrently, in different workgroups when both are asked for.
 #include "common.hpp"
 
 #include <math.h>
@@ -49,14 +49,14 @@ struct GateWork {
   int first = 0, stride = 1;  // this wave's rows: first, first + stride, ...
 };
 
-// Rows r0 .. r1-1 are dealt out one per wave across the grid's workgroups.
+// Rows r0 .. r1-1 are dealt out one per wave, round robin.
 template <int DT>
 __device__ __forceinline__ GateWork gate_work(const RouterArgs &a, int r0, int r1, int wave) {
   constexpr int EPL = DT == 1 ? 8 : 4;  // elements per 16-byte load
   GateWork g;
   g.cpr = (a.d + kWave * EPL - 1) / (kWave * EPL);
-  g.first = r0 + (int)blockIdx.x * kWaves + wave;
-  g.stride = (int)gridDim.x * kWaves;
+  g.first = r0 + wave;
+  g.stride = kWaves;
   g.m = g.first < r1 ? (r1 - g.first + g.stride - 1) / g.stride : 0;
   return g;
 }
@@ -553,9 +553,14 @@ __device__ __forceinline__ int topk_from_parts(const int (*cnt)[kMaxE], int E, i
   return lane < K ? out[lane] : -1;
 }
 
-// MR: most gate rows a wave holds at once.  TWO: the demand rows (0..E-1) and
-// the speculative rows (E..2E-1) in two passes, each within MR rows a wave.
-template <int MR, bool TWO>
+// MR: most gate rows a wave holds at once.  A launch of two workgroups splits
+// the roles: workgroup 0 routes and looks up this layer,
+// workgroup 1 guesses and inserts for the next one (their tables, counters and
+// trace records are disjoint), each with its own copy of h and a GEMV of E
+// rows.  (Both roles in one workgroup, the speculative rows in a second GEMV
+// pass, put that pass on every layer's critical path: 13.7 against 9.7 us a
+// layer at 64 experts.)
+template <int MR>
 __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   __shared__ __align__(16) float hs[kMaxD];
   __shared__ double zs[2 * kMaxE];
@@ -566,26 +571,22 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
   __shared__ int s_demand_ok;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int E = a.E, d = a.d;
-  const bool route_here = a.demand && a.inj_ids == nullptr;
-  const bool spec = a.spec_layer >= 0;
+  // role of this workgroup: 0 demand only, 1 speculation only, -1 both
+  const int role = gridDim.x == 2 ? (int)blockIdx.x : -1;
+  const bool demand = a.demand && role != 1;
+  const bool route_here = demand && a.inj_ids == nullptr;
+  const bool spec = a.spec_layer >= 0 && role != 0;
 
   // Every global read that does not depend on another is issued first: the
-  // tables and counters of waves 0 and 1, the first batch of gate rows (or,
-  // after a separate GEMV launch, its logits), then h.
-  const int phase = a.phase;
+  // tables and counters of waves 0 and 1, the first batch of gate rows, then h.
   TableView tv{};
-  if (phase != 1) {
-    if (wave == 0 && a.demand) tv = load_table(a.tables + a.layer, a.stats + a.layer, lane, E);
-    if (wave == 1 && spec) tv = load_table(a.tables + a.spec_layer, a.stats + a.spec_layer, lane, E);
-  }
+  if (wave == 0 && demand) tv = load_table(a.tables + a.layer, a.stats + a.layer, lane, E);
+  if (wave == 1 && spec) tv = load_table(a.tables + a.spec_layer, a.stats + a.spec_layer, lane, E);
   const int r0 = route_here ? 0 : E, r1 = spec ? 2 * E : E;
-  double zv = 0.0;  // clamped index, not a guarded load (one would be waited for on the spot)
-  if (phase == 2) zv = a.zbuf[min(r0 + tid, 2 * kMaxE - 1)];
   uint4 gv[MR];
   GateWork gw;
-  const int r1a = TWO ? E : r1;  // rows of the first pass
-  if (phase != 2 && (route_here || spec)) {
-    gw = a.dtype == 1 ? gate_work<1>(a, r0, r1a, wave) : gate_work<0>(a, r0, r1a, wave);
+  if (route_here || spec) {
+    gw = a.dtype == 1 ? gate_work<1>(a, r0, r1, wave) : gate_work<0>(a, r0, r1, wave);
     if (gw.m > 0) {
       if (a.dtype == 1)
         gate_load<1, MR>(a, lane, gw, 0, gv);
@@ -594,7 +595,7 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     }
   }
   if (tid == 0) {
-    s_tbase = a.trace ? *a.trace_count : 0;
+    s_tbase = *a.trace_in;
     s_demand_ok = 0;
   }
   if (route_here || spec) {
@@ -610,36 +611,19 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     }
     ss = wave_sum_d(ss);
     if (lane == 0) red[wave] = ss;
-    if (phase == 2 && r0 + tid < r1) zs[r0 + tid] = zv;
     __syncthreads();
-    if (phase != 2) {
-      double *zout = phase == 1 ? a.zbuf : zs;
-      if (gw.m > 0) {  // the same for the whole wave
-        if (a.dtype == 1)
-          gate_logits<1, MR>(a, hs, lane, gw, gv, zout);
-        else
-          gate_logits<0, MR>(a, hs, lane, gw, gv, zout);
-      }
-      if (TWO) {  // the speculative rows
-        const GateWork g2 = a.dtype == 1 ? gate_work<1>(a, E, r1, wave) : gate_work<0>(a, E, r1, wave);
-        if (g2.m > 0) {
-          if (a.dtype == 1) {
-            gate_load<1, MR>(a, lane, g2, 0, gv);
-            gate_logits<1, MR>(a, hs, lane, g2, gv, zout);
-          } else {
-            gate_load<0, MR>(a, lane, g2, 0, gv);
-            gate_logits<0, MR>(a, hs, lane, g2, gv, zout);
-          }
-        }
-      }
+    if (gw.m > 0) {  // the same for the whole wave
+      if (a.dtype == 1)
+        gate_logits<1, MR>(a, hs, lane, gw, gv, zs);
+      else
+        gate_logits<0, MR>(a, hs, lane, gw, gv, zs);
     }
   }
-  if (phase == 1) return;  // the GEMV launch is done; the next launch reads zbuf
   __syncthreads();
   rank_parts(zs, E, route_here, spec, tid, s_cnt);
   __syncthreads();
 
-  if (wave == 0 && a.demand) {
+  if (wave == 0 && demand) {
     int idreg;
     if (route_here) {
       idreg = topk_from_parts(s_cnt[0], E, a.K, lane, s_top[0]);
@@ -683,54 +667,33 @@ __global__ __launch_bounds__(kThreads) void router_kernel(RouterArgs a) {
     prefetch_insert(a, greg, lane, s_tbase + (a.demand ? (uint64_t)a.K : 0), tv);
   }
   __syncthreads();
-  if (tid == 0 && a.trace)
-    *a.trace_count = s_tbase + (s_demand_ok ? (uint64_t)a.K : 0) + (spec ? (uint64_t)a.K : 0);
+  // the demand workgroup (or the only one) advances the count past both roles'
+  // records; the speculative records sit at s_tbase + K either way
+  if (tid == 0 && role != 1)
+    *a.trace_out = s_tbase + (a.trace ? (s_demand_ok ? (uint64_t)a.K : 0) +
+                                            (a.spec_layer >= 0 ? (uint64_t)a.K : 0)
+                                      : 0);
 }
 
 }  // namespace
 
-#ifndef MOE_ROUTER_ONE_LAUNCH_ROWS
-#define MOE_ROUTER_ONE_LAUNCH_ROWS 128
-#endif
-
 hipError_t launch_router(const RouterArgs &a, const Launch &l) {
-  // Up to MOE_ROUTER_ONE_LAUNCH_ROWS gate rows (every case of this build:
-  // at most 64 experts, twice that when speculating) run in one workgroup,
-  // each wave accumulating its up to 4 rows at once.  Beyond that the GEMV is
-  // a launch of its own, one row per wave, and the table work a second one.
-  // (A single launch whose last workgroup took over cost about 7 us in
-  // device-scope fences.)
-  const int rows = (a.demand && a.inj_ids == nullptr ? a.E : 0) + (a.spec_layer >= 0 ? a.E : 0);
-  if (rows <= MOE_ROUTER_ONE_LAUNCH_ROWS) {
-    RouterArgs one = a;
-    one.phase = 0;
-    // beyond 4 rows a wave (64 experts with speculation) the demand and the
-    // speculative rows go in two passes: 8 rows at once would spill
-    const bool two = (rows + kWaves - 1) / kWaves > 4 && a.demand && a.inj_ids == nullptr && a.spec_layer >= 0;
-    const int per_wave = ((two ? a.E : rows) + kWaves - 1) / kWaves;
-    if (per_wave > 4) return hipErrorInvalidValue;  // cannot happen with at most 64 experts
-#define MOE_ROUTER_ONE(MR)                                                          \
-  do {                                                                              \
-    if (two)                                                                        \
-      MOE_LAUNCH((router_kernel<MR, true>), dim3(1), dim3(kThreads), 0, l, one);    \
-    else                                                                            \
-      MOE_LAUNCH((router_kernel<MR, false>), dim3(1), dim3(kThreads), 0, l, one);   \
-  } while (0)
-    if (per_wave <= 1)
-      MOE_ROUTER_ONE(1);
-    else if (per_wave <= 2)
-      MOE_ROUTER_ONE(2);
-    else
-      MOE_ROUTER_ONE(4);
-#undef MOE_ROUTER_ONE
-    return hipGetLastError();
-  }
-  RouterArgs g = a, t = a;
-  g.phase = 1;
-  t.phase = 2;
-  MOE_LAUNCH((router_kernel<1, false>), dim3((rows + kWaves - 1) / kWaves), dim3(kThreads), 0,
-             (Launch{l.s, l.start, nullptr}), g);
-  MOE_LAUNCH((router_kernel<1, false>), dim3(1), dim3(kThreads), 0, (Launch{l.s, nullptr, l.stop}), t);
+  // With routing and speculation both asked for, the two roles run side by
+  // side, one workgroup each; otherwise one workgroup does the call.  Each
+  // role has at most 64 gate rows, 4 a wave.  (One workgroup for both roles,
+  // the speculative rows in a second GEMV pass: 13.7 instead of 9.7 us a
+  // layer at 64 experts; the GEMV spread over many workgroups with the last
+  // one doing the table work cost about 7 us in device-scope fences.)
+  const bool both = a.demand && a.inj_ids == nullptr && a.spec_layer >= 0;
+  if (a.E > 4 * kWaves) return hipErrorInvalidValue;  // cannot happen: at most kMaxE experts
+  const int per_wave = (a.E + kWaves - 1) / kWaves;
+  const dim3 grid(both ? 2 : 1);
+  if (per_wave <= 1)
+    MOE_LAUNCH((router_kernel<1>), grid, dim3(kThreads), 0, l, a);
+  else if (per_wave <= 2)
+    MOE_LAUNCH((router_kernel<2>), grid, dim3(kThreads), 0, l, a);
+  else
+    MOE_LAUNCH((router_kernel<4>), grid, dim3(kThreads), 0, l, a);
   return hipGetLastError();
 }
 
