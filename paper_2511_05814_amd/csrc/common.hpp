@@ -202,9 +202,11 @@ int ffnq_down_chunks(int K, int d_ff);
 hipError_t launch_prefill_gate(const PrefillArgs &a, const Launch &l);
 hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l);
 // grouped GEMMs over tiles of `rows` (64, 128 or 256) sorted pairs by
-// prefill_tile_cols(up) output columns
+// prefill_tile_cols(up) output columns; a_bytes: size of the A operand's
+// buffer (xn for up, act for down)
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l);
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, size_t a_bytes,
+                             const Launch &l);
 // Small-M grouped GEMMs: one tile {job, 0, 0} per expert, each with at most
 // max_rows <= kSkinnyRows rows (the caller's bound: rows beyond 16 are read
 // only when max_rows > 16); a workgroup per (tile, 16 output features).
@@ -215,7 +217,7 @@ hipError_t launch_prefill_skinny_up(const GemmTile *tiles, int ntiles, const Gem
 hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
                                       float *Y, int d, int d_ff, int max_rows, const Launch &l);
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, int rows, const Launch &l);
+                               float *Y, int d, int d_ff, int rows, size_t a_bytes, const Launch &l);
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
                                     int d, int K, const Launch &l);
 int prefill_tile_cols(bool up);  // GEMM output tile columns (act for up, Y for down)

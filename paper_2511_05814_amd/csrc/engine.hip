@@ -1159,13 +1159,15 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
       HIP_TRY(c, launch_prefill_skinny_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff,
                                             skinny[gi], lu));
     else
-      HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, up_rows[gi], lu));
+      HIP_TRY(c, launch_prefill_up(tiles + up_first[gi], up_n[gi], jobs, xn, perm, act, c->d, c->dff, up_rows[gi],
+                                   (size_t)c->max_T * c->d * 2, lu));
     kernel_span_done(c, SPAN_GEMM_UP, lu, group_rows[gi] * up_flop_per_row);
     HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
     if (skinny[gi])
       HIP_TRY(c, launch_prefill_skinny_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, skinny[gi], ld));
     else
-      HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, dn_rows[gi], ld));
+      HIP_TRY(c, launch_prefill_down(tiles + dn_first[gi], dn_n[gi], jobs, act, Y, c->d, c->dff, dn_rows[gi],
+                                     (size_t)c->max_T * c->K * c->dff * 2, ld));
     kernel_span_done(c, SPAN_GEMM_DOWN, ld, group_rows[gi] * down_flop_per_row);
     return MOE_OK;
   };

@@ -697,6 +697,209 @@ __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) v
       }
 }
 
+// 256-row tiles with the operands staged by the memory system itself: every
+// 16-byte load goes straight from global memory into LDS (buffer_load ...
+// lds), so no register holds a slice on its way and no wave spends
+// instructions storing one.  kDmaStages LDS buffers of one 32-deep slice each
+// (32 KB: A 256 x 32, B 256 x 32) form a ring; a step waits for its own
+// slice's loads, meets the other waves at one barrier (after which the buffer
+// multiplied in the previous step is free), issues the loads of the slice
+// kDmaStages - 1 ahead into that buffer and multiplies.  One load instruction
+// of a wave fills 1 KB of LDS, lane i at byte 16 i: 16 rows of 64 bytes.  Lane
+// i therefore fetches the chunk that the swizzle (lds_chunk) puts at its
+// place, chunk (i % 4) ^ ((row / 4) % 4) of row i / 4.  The loads are
+// issued as inline instructions the compiler does not track, so the waits are
+// the kernel's own: before a step, at most the loads of the kDmaStages - 2
+// slices after it may be outstanding.  Rows past a
+// group's end read its last row (not written); a K tail's chunks are fetched
+// from an offset past the buffer's record count, which the hardware turns into
+// zeros.
+#ifndef MOE_DMA_FOUR
+#define MOE_DMA_FOUR 1
+#endif
+constexpr int kDmaStages = MOE_DMA_FOUR ? 4 : 3;
+constexpr int kDmaKs = 32;
+// Offset for a chunk that must read zeros: at or past every record count used
+// here (all below 2^31; the range check admits any dword that starts below the
+// record count, so the offset must clear it, not merely approach it)
+constexpr uint32_t kOobOffset = 0x80000000u;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One wave-wide 16-byte-a-lane load into LDS at lds_base + 16 * lane.  Written
+// as an instruction of its own rather than the compiler's builtin: the
+// compiler tracks loads in flight into LDS per array, loses track across the
+// ring's loop and then waits for all of them before reading any buffer; here
+// the kernel's own waits (wait_vm) are the only ones.  M0 carries the LDS
+// address; the compiler sets M0 itself before any instruction of its own that
+// reads it (none in this kernel: gfx9 LDS instructions do not use it).
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, void *lds_base, uint32_t voff) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t *)lds_base);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "s"(m0), "v"(voff), "s"(r) : "memory");
+}
+
+// s_waitcnt with vmcnt = N and the other counters left alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <bool UP, bool RAGGED>
+__global__ __launch_bounds__(512, 1) void prefill_gemm_dma_kernel(const GemmTile *tiles, const GemmJob *jobs,
+                                                                  const uint16_t *a_src, uint32_t a_bytes,
+                                                                  const int32_t *perm_tok, void *out, int d,
+                                                                  int d_ff) {
+  constexpr int BM = 256, KS = kDmaKs, S = kDmaStages;
+  constexpr int NB = UP ? 2 : 1;
+  constexpr int BN = gemm_cols<UP>();
+  constexpr int WM = 4, WR = BM / WM, WC = BN / 2, MX = WR / 32, NY = WC / 32;
+  constexpr int LOADS = 4;  // load instructions per wave and slice: 2 for A, 2 for B
+  static_assert(NB * BN == 256, "B slice of 256 rows");
+
+  // one array per ring buffer, the A slice (rows 0 .. BM - 1) then the B
+  // slice: the compiler tracks loads in flight into LDS per array, and only a
+  // few arrays at a time
+  __shared__ uint16_t L0[BM + NB * BN][KS], L1[BM + NB * BN][KS], L2[BM + NB * BN][KS];
+#if MOE_DMA_FOUR
+  __shared__ uint16_t L3[BM + NB * BN][KS];
+#endif
+  const GemmTile t = tiles[xcd_tile(blockIdx.x, gridDim.x)];
+  const GemmJob j = jobs[t.job];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int wm = wave / 2, wn = wave % 2;
+  const int K = UP ? d : d_ff;
+  const int N = UP ? d_ff : d;
+  if (j.nrows <= 0) return;  // the plan makes no such tiles
+
+  // this lane's rows and chunks: load instruction i of the wave fills LDS
+  // rows 32 wave + 16 i .. + 15 of the A slice and of the B slice
+  const int prow0 = 32 * wave + lane / 4;  // + 16 i
+  const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(a_src), 0, a_bytes,
+                                                                        0x00020000);
+  const int nb = min(BN, N - t.n0);
+  __amdgpu_buffer_rsrc_t brs[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    brs[b] = rows_rsrc(j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)t.n0 * K,
+                       (uint32_t)nb * K * 2);
+  uint32_t aoff[2], boff[2];
+  int achunk[2], bchunk[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = prow0 + 16 * i;  // row of the A slice (0..255) and of the B slice (0..255)
+    const int c = (lane % 4) ^ ((r / 4) % 4);
+    const int m = min(t.m0 + r, j.nrows - 1);
+    const size_t arow = UP ? (size_t)perm_tok[j.row0 + m] * d : (size_t)(j.row0 + m) * d_ff;
+    aoff[i] = (uint32_t)(arow * 2) + 16u * c;
+    achunk[i] = c;
+    const int br = r % BN;
+    boff[i] = (uint32_t)min(br, nb - 1) * K * 2 + 16u * c;
+    bchunk[i] = c;
+  }
+  const int bmat0 = (32 * wave) / BN, bmat1 = (32 * wave + 16) / BN;  // B matrix of each instruction
+
+  auto issue = [&](int k0, uint16_t (*As)[KS], uint16_t (*Bs)[KS]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const bool oob_a = RAGGED && k0 + 8 * achunk[i] >= K;
+      dma16(ars, &As[32 * wave + 16 * i][0], oob_a ? kOobOffset : aoff[i] + 2u * k0);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const bool oob_b = RAGGED && k0 + 8 * bchunk[i] >= K;
+      const __amdgpu_buffer_rsrc_t r = (i == 0 ? bmat0 : bmat1) == 0 ? brs[0] : brs[NB - 1];
+      dma16(r, &Bs[32 * wave + 16 * i][0], oob_b ? kOobOffset : boff[i] + 2u * k0);
+    }
+  };
+
+  floatx16 c[NB][MX][NY];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int x = 0; x < MX; ++x)
+#pragma unroll
+      for (int y = 0; y < NY; ++y)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) c[b][x][y][i] = 0.0f;
+
+  auto mma = [&](const uint16_t (*As)[KS], const uint16_t (*Bs)[KS]) {
+#pragma unroll
+    for (int h = 0; h < KS / 16; ++h) {
+      bf16x8 af[MX];
+#pragma unroll
+      for (int x = 0; x < MX; ++x) af[x] = lds_frag32<KS>(As, wm * WR + x * 32 + lane % 32, lane, h);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        bf16x8 bf[NY];
+#pragma unroll
+        for (int y = 0; y < NY; ++y) bf[y] = lds_frag32<KS>(Bs + b * BN, wn * WC + y * 32 + lane % 32, lane, h);
+#pragma unroll
+        for (int x = 0; x < MX; ++x)
+#pragma unroll
+          for (int y = 0; y < NY; ++y)
+            c[b][x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[x], bf[y], c[b][x][y], 0, 0, 0);
+      }
+    }
+  };
+
+  const int nk = (K + KS - 1) / KS;
+  // slices 0 .. S - 2 in flight before the first step
+  issue(0, L0, L0 + BM);
+  if (1 < nk) issue(KS, L1, L1 + BM);
+#if MOE_DMA_FOUR
+  if (2 < nk) issue(2 * KS, L2, L2 + BM);
+#endif
+  // step s: buffer s % S; the slice S - 1 ahead goes to buffer (s - 1) % S
+#define MOE_DMA_STEP(U, AC, BC, AN, BN_)                                        \
+  {                                                                             \
+    const int s = s0 + U;                                                       \
+    if (s < nk) {                                                               \
+      __builtin_amdgcn_sched_barrier(0);                                        \
+      if (s + S - 2 < nk)                                                       \
+        wait_vm<LOADS *(S - 2)>();                                              \
+      else                                                                      \
+        wait_vm<0>();                                                           \
+      __builtin_amdgcn_s_barrier();                                             \
+      __builtin_amdgcn_sched_barrier(0);                                        \
+      if (s + S - 1 < nk) issue((s + S - 1) * KS, AN, BN_);                     \
+      mma(AC, BC);                                                              \
+    }                                                                           \
+  }
+  for (int s0 = 0; s0 < nk; s0 += S) {
+#if MOE_DMA_FOUR
+    MOE_DMA_STEP(0, L0, L0 + BM, L3, L3 + BM)
+    MOE_DMA_STEP(1, L1, L1 + BM, L0, L0 + BM)
+    MOE_DMA_STEP(2, L2, L2 + BM, L1, L1 + BM)
+    MOE_DMA_STEP(3, L3, L3 + BM, L2, L2 + BM)
+#else
+    MOE_DMA_STEP(0, L0, L0 + BM, L2, L2 + BM)
+    MOE_DMA_STEP(1, L1, L1 + BM, L0, L0 + BM)
+    MOE_DMA_STEP(2, L2, L2 + BM, L1, L1 + BM)
+#endif
+  }
+#undef MOE_DMA_STEP
+  // lane i holds column i % 32 of each 32 x 32 block, rows 8 (v / 4) + 4 (i / 32) + v % 4
+#pragma unroll
+  for (int x = 0; x < MX; ++x)
+#pragma unroll
+    for (int y = 0; y < NY; ++y)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int m = t.m0 + wm * WR + x * 32 + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
+        if (m >= j.nrows) continue;
+        const int n = t.n0 + wn * WC + y * 32 + lane % 32;
+        if (n < N) {
+          if (UP)
+            static_cast<uint16_t *>(out)[(size_t)(j.row0 + m) * N + n] =
+                f32_to_bf16_rne(silu(c[0][x][y][i]) * c[NB - 1][x][y][i]);
+          else
+            static_cast<float *>(out)[(size_t)(j.row0 + m) * N + n] = c[0][x][y][i];
+        }
+      }
+}
+
 // Small-M grouped GEMM: groups whose experts have at most kSkinnyRows rows
 // (batched decode).  The tiled kernel above stages 128-row slices through LDS
 // and, with a handful of rows per expert, streams the weights at a few TB/s
@@ -910,9 +1113,25 @@ hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l) {
   return hipGetLastError();
 }
 
+#ifndef MOE_GEMM_DMA
+#define MOE_GEMM_DMA 1
+#endif
+// the LDS-DMA kernel addresses its A operand with 32-bit offsets below kOobOffset
+static bool dma_fits(size_t a_bytes) { return MOE_GEMM_DMA && a_bytes > 0 && a_bytes < kOobOffset; }
+
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
-                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, const Launch &l) {
+                             const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, size_t a_bytes,
+                             const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
+  if (rows == 256 && dma_fits(a_bytes)) {
+    if (d % kDmaKs == 0)
+      MOE_LAUNCH((prefill_gemm_dma_kernel<true, false>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, xn,
+                 (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff);
+    else
+      MOE_LAUNCH((prefill_gemm_dma_kernel<true, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, xn,
+                 (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff);
+    return hipGetLastError();
+  }
 #define MOE_GEMM_UP(BM, TH, RG)                                                                                   \
   MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, BM, TH, kKStep, RG>), dim3(ntiles), dim3(TH), 0, l, tiles, jobs, xn, \
              perm_tok, (void *)act, d, d_ff)
@@ -968,8 +1187,17 @@ hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const G
 }
 
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, int rows, const Launch &l) {
+                               float *Y, int d, int d_ff, int rows, size_t a_bytes, const Launch &l) {
   if (ntiles <= 0) return hipSuccess;
+  if (rows == 256 && dma_fits(a_bytes)) {
+    if (d_ff % kDmaKs == 0)
+      MOE_LAUNCH((prefill_gemm_dma_kernel<false, false>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, act,
+                 (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff);
+    else
+      MOE_LAUNCH((prefill_gemm_dma_kernel<false, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, act,
+                 (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff);
+    return hipGetLastError();
+  }
 #define MOE_GEMM_DOWN(BM, TH, RG)                                                                                  \
   MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, BM, TH, kKStep, RG>), dim3(ntiles), dim3(TH), 0, l, tiles, jobs, act, \
              (const int32_t *)nullptr, (void *)Y, d, d_ff)
