@@ -719,6 +719,13 @@ __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) v
 #endif
 constexpr int kDmaStages = MOE_DMA_FOUR ? 4 : 3;
 constexpr int kDmaKs = 32;
+#ifndef MOE_GEMM_DMA_WAVES
+#define MOE_GEMM_DMA_WAVES 8
+#endif
+// 8 waves (two a SIMD), 64 x 64 wave tiles.  Four waves with 128 x 64 tiles
+// (a quarter fewer LDS reads per MFMA, the accumulators in AGPRs) measured
+// slower on MI355X: 659 against 694 TFLOP/s in the 64-expert up projection.
+constexpr int kDmaWaves = MOE_GEMM_DMA_WAVES;
 // Offset for a chunk that must read zeros: at or past every record count used
 // here (all below 2^31; the range check admits any dword that starts below the
 // record count, so the offset must clear it, not merely approach it)
@@ -745,16 +752,19 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <bool UP, bool RAGGED>
-__global__ __launch_bounds__(512, 1) void prefill_gemm_dma_kernel(const GemmTile *tiles, const GemmJob *jobs,
+template <bool UP, bool RAGGED, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(const GemmTile *tiles, const GemmJob *jobs,
                                                                   const uint16_t *a_src, uint32_t a_bytes,
                                                                   const int32_t *perm_tok, void *out, int d,
                                                                   int d_ff) {
   constexpr int BM = 256, KS = kDmaKs, S = kDmaStages;
   constexpr int NB = UP ? 2 : 1;
   constexpr int BN = gemm_cols<UP>();
-  constexpr int WM = 4, WR = BM / WM, WC = BN / 2, MX = WR / 32, NY = WC / 32;
-  constexpr int LOADS = 4;  // load instructions per wave and slice: 2 for A, 2 for B
+  constexpr int WM = WAVES / 2, WR = BM / WM, WC = BN / 2, MX = WR / 32, NY = WC / 32;
+  constexpr int IPW = 16 / WAVES;   // load instructions per wave and slice for A, and as many for B
+  constexpr int RPW = BM / WAVES;   // slice rows a wave fills (16 per instruction)
+  constexpr int LOADS = 2 * IPW;
+  static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
   static_assert(NB * BN == 256, "B slice of 256 rows");
 
   // one array per ring buffer, the A slice (rows 0 .. BM - 1) then the B
@@ -774,8 +784,8 @@ __global__ __launch_bounds__(512, 1) void prefill_gemm_dma_kernel(const GemmTile
   if (j.nrows <= 0) return;  // the plan makes no such tiles
 
   // this lane's rows and chunks: load instruction i of the wave fills LDS
-  // rows 32 wave + 16 i .. + 15 of the A slice and of the B slice
-  const int prow0 = 32 * wave + lane / 4;  // + 16 i
+  // rows RPW wave + 16 i .. + 15 of the A slice and of the B slice
+  const int prow0 = RPW * wave + lane / 4;  // + 16 i
   const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(a_src), 0, a_bytes,
                                                                         0x00020000);
   const int nb = min(BN, N - t.n0);
@@ -784,10 +794,10 @@ __global__ __launch_bounds__(512, 1) void prefill_gemm_dma_kernel(const GemmTile
   for (int b = 0; b < NB; ++b)
     brs[b] = rows_rsrc(j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)t.n0 * K,
                        (uint32_t)nb * K * 2);
-  uint32_t aoff[2], boff[2];
-  int achunk[2], bchunk[2];
+  uint32_t aoff[IPW], boff[IPW];
+  int achunk[IPW], bchunk[IPW], bmat[IPW];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < IPW; ++i) {
     const int r = prow0 + 16 * i;  // row of the A slice (0..255) and of the B slice (0..255)
     const int c = (lane % 4) ^ ((r / 4) % 4);
     const int m = min(t.m0 + r, j.nrows - 1);
@@ -797,20 +807,20 @@ __global__ __launch_bounds__(512, 1) void prefill_gemm_dma_kernel(const GemmTile
     const int br = r % BN;
     boff[i] = (uint32_t)min(br, nb - 1) * K * 2 + 16u * c;
     bchunk[i] = c;
+    bmat[i] = (RPW * wave + 16 * i) / BN;  // B matrix of the instruction (uniform)
   }
-  const int bmat0 = (32 * wave) / BN, bmat1 = (32 * wave + 16) / BN;  // B matrix of each instruction
 
   auto issue = [&](int k0, uint16_t (*As)[KS], uint16_t (*Bs)[KS]) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < IPW; ++i) {
       const bool oob_a = RAGGED && k0 + 8 * achunk[i] >= K;
-      dma16(ars, &As[32 * wave + 16 * i][0], oob_a ? kOobOffset : aoff[i] + 2u * k0);
+      dma16(ars, &As[RPW * wave + 16 * i][0], oob_a ? kOobOffset : aoff[i] + 2u * k0);
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < IPW; ++i) {
       const bool oob_b = RAGGED && k0 + 8 * bchunk[i] >= K;
-      const __amdgpu_buffer_rsrc_t r = (i == 0 ? bmat0 : bmat1) == 0 ? brs[0] : brs[NB - 1];
-      dma16(r, &Bs[32 * wave + 16 * i][0], oob_b ? kOobOffset : boff[i] + 2u * k0);
+      const __amdgpu_buffer_rsrc_t r = bmat[i] == 0 ? brs[0] : brs[NB - 1];
+      dma16(r, &Bs[RPW * wave + 16 * i][0], oob_b ? kOobOffset : boff[i] + 2u * k0);
     }
   };
 
@@ -1125,10 +1135,10 @@ hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *j
   if (ntiles <= 0) return hipSuccess;
   if (rows == 256 && dma_fits(a_bytes)) {
     if (d % kDmaKs == 0)
-      MOE_LAUNCH((prefill_gemm_dma_kernel<true, false>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, xn,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<true, false, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
                  (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff);
     else
-      MOE_LAUNCH((prefill_gemm_dma_kernel<true, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, xn,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<true, true, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
                  (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff);
     return hipGetLastError();
   }
@@ -1191,10 +1201,10 @@ hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob 
   if (ntiles <= 0) return hipSuccess;
   if (rows == 256 && dma_fits(a_bytes)) {
     if (d_ff % kDmaKs == 0)
-      MOE_LAUNCH((prefill_gemm_dma_kernel<false, false>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, act,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<false, false, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
                  (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff);
     else
-      MOE_LAUNCH((prefill_gemm_dma_kernel<false, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, act,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<false, true, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
                  (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff);
     return hipGetLastError();
   }
