@@ -227,15 +227,23 @@ __global__ __launch_bounds__(kThreads) void ffnq_up_kernel(FfnArgs a, int G) {
 // costs one v_perm_b32, which forms the LDS address (nibble << 8 | lane << 2,
 // plus 64 KB for pairs 16..31) straight from the byte holding the nibble, one
 // LDS read and one add: with the byte masks and the per-group scale and zero
-// about 1.4 vector instructions a weight instead of 2.7, so the kernel is
-// bound by streaming the codes rather than by the vector ALUs.  The sums
-// differ from the direct form only in rounding (one rounding per table
-// entry).  One workgroup of 16 waves per CU; each wave walks rows of both
-// ranks (W1 and W3 of a row together), the codes of the next two rows in
-// flight while it works on the current one.
+// about 1.4 vector instructions a weight instead of 2.7.  The sums differ
+// from the direct form only in rounding (one rounding per table entry).  One
+// workgroup of 16 waves per CU; each wave walks rows of both ranks (W1 and W3
+// of a row together), loading the codes of its next row (kQAhead) as it
+// finishes one.
 constexpr int kLutThreads = 1024;
 constexpr int kLutWaves = kLutThreads / kWave;
 constexpr int kLutPairs = kLaneCols / 2;  // column pairs per lane
+#ifndef MOE_FFNQ_AHEAD
+#define MOE_FFNQ_AHEAD 1
+#endif
+// Rows (items) whose codes a wave loads ahead of the one it works on.  One:
+// the kernels are bound by vector-ALU and LDS issue, the 16 waves of a CU keep
+// enough loads in flight between them, and every row held ahead costs
+// registers and instructions (at the Mixtral shape, up/down: 21.9/13.2 us with
+// one, 23.8/13.3 with two, 26.1/13.7 with three, 34.0/16.3 with six).
+constexpr int kQAhead = MOE_FFNQ_AHEAD;
 
 // Writes the table for x_c = scale * src[c] over columns c < n of every
 // lane's 64 (zeros past n), then returns this lane's four group sums of x
@@ -318,22 +326,23 @@ __global__ __launch_bounds__(kLutThreads, 1) void ffnq_up_lut_kernel(FfnArgs a) 
     u[0] = load_unit(qmat(base, d_ff, d), row, col);
     u[1] = load_unit(qmat(base + mbytes, d_ff, d), row, col);
   };
-  // the first two items' codes are on their way while the table is built
-  QUnit u0[2], u1[2];
-  load_item(first, u0);
-  load_item(first + stride, u1);
+  // the first kQAhead items' codes are on their way while the table is built;
+  // the ring of item slots is unrolled, so slot q stays in the same registers
+  QUnit u[kQAhead][2];
+#pragma unroll
+  for (int q = 0; q < kQAhead; ++q) load_item(first + q * stride, u[q]);
   float xs64[4];
   lut_build(tab, a.h, d, a.route->inv_r, lane, wave, xs64);
-  for (int it = first; it < nitems; it += stride) {
-    QUnit u2[2];
-    load_item(it + 2 * stride, u2);
-    const float a1 = wave_sum_to_lane63(lut_dot(tab, u0[0], lane, xs64));
-    const float a3 = wave_sum_to_lane63(lut_dot(tab, u0[1], lane, xs64));
-    if (lane == kWave - 1) a.act[it] = silu(a1) * a3;  // item it = rank * d_ff + row
+  for (int it0 = first; it0 < nitems; it0 += kQAhead * stride) {
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
-      u0[m] = u1[m];
-      u1[m] = u2[m];
+    for (int q = 0; q < kQAhead; ++q) {
+      const int it = it0 + q * stride;  // item it = rank * d_ff + row
+      if (it < nitems) {                // the same for the whole wave
+        const float a1 = wave_sum_to_lane63(lut_dot(tab, u[q][0], lane, xs64));
+        const float a3 = wave_sum_to_lane63(lut_dot(tab, u[q][1], lane, xs64));
+        if (lane == kWave - 1) a.act[it] = silu(a1) * a3;
+      }
+      load_item(it + kQAhead * stride, u[q]);  // past the end: the last item again (from cache), unused
     }
   }
 }
@@ -364,16 +373,21 @@ __global__ __launch_bounds__(kLutThreads, 1) void ffnq_down_lut_kernel(FfnArgs a
   const QMat w2 = qmat(base + 2 * ((size_t)d_ff * d / 16 * 7), d, d_ff);
   const int col = c0 + lane * kLaneCols;  // load_unit clamps columns past d_ff (those x are zero)
   const int first = row_lo + wave;
-  QUnit u0 = load_unit(w2, min(first, row_hi - 1), col);
-  QUnit u1 = load_unit(w2, min(first + kLutWaves, row_hi - 1), col);
+  QUnit u[kQAhead];
+#pragma unroll
+  for (int q = 0; q < kQAhead; ++q) u[q] = load_unit(w2, min(first + q * kLutWaves, row_hi - 1), col);
   float xs64[4];
   lut_build(tab, a.act + (size_t)rank * d_ff + c0, d_ff - c0, a.route->g[rank], lane, wave, xs64);
-  for (int r = first; r < row_hi; r += kLutWaves) {
-    const QUnit u2 = load_unit(w2, min(r + 2 * kLutWaves, row_hi - 1), col);
-    const float s = wave_sum_to_lane63(lut_dot(tab, u0, lane, xs64));
-    if (lane == kWave - 1) a.part[(size_t)ch * d + r] = s;
-    u0 = u1;
-    u1 = u2;
+  for (int r0 = first; r0 < row_hi; r0 += kQAhead * kLutWaves) {
+#pragma unroll
+    for (int q = 0; q < kQAhead; ++q) {
+      const int r = r0 + q * kLutWaves;
+      if (r < row_hi) {  // the same for the whole wave
+        const float s = wave_sum_to_lane63(lut_dot(tab, u[q], lane, xs64));
+        if (lane == kWave - 1) a.part[(size_t)ch * d + r] = s;
+      }
+      u[q] = load_unit(w2, min(r + kQAhead * kLutWaves, row_hi - 1), col);  // past the end: the last row again
+    }
   }
 }
 
