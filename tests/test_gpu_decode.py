@@ -107,6 +107,58 @@ def test_delayed_copy_stream_still_correct(tiny, mode):
         moe.close()
 
 
+@pytest.mark.parametrize("mode", ["kernel", "split", "dma"])
+def test_poisoned_slots_are_never_read_before_their_copies(tiny, mode):
+    # Every slot a copy is about to fill is overwritten with NaN bytes just
+    # before the layer call that issues the copy: a speculative copy's slot on
+    # the copy stream (after the compute stream's earlier work, then a long
+    # spin), a demand copy's slot on the stream that carries demand copies (the
+    # compute stream, or the copy stream in DMA mode).  A kernel that read a
+    # slot before the copy filling it finished would meet NaN (or the evicted
+    # expert) and carry it into h; with every wait in place the outputs and the
+    # trace are those of the unpoisoned run, bit for bit.
+    from collections import defaultdict
+    from oracle.cache import F_HIT, F_ISSUED, KIND_ACCESS, KIND_PREFETCH
+
+    cfg = tiny.cfg
+    fm = {"kernel": b.MOE_FETCH_KERNEL, "split": b.MOE_FETCH_SPLIT, "dma": b.MOE_FETCH_DMA}[mode]
+    T, S = 16, 4
+    ref = tiny.cache(S, "lru", prefetch_max=2, fetch_mode=fm)
+    _, recs0, H0 = tiny.run(ref, T, flags=b.MOE_PREFETCH_NEXT)
+    ref.close()
+    spec, demand = defaultdict(list), defaultdict(list)  # (token, calling layer) -> [(layer, slot)]
+    for kind, tok, layer, _rank, _e, flags, slot, _v in recs0:
+        if kind == KIND_PREFETCH and flags & F_ISSUED:
+            spec[(tok, layer - 1)].append((layer, slot))
+        elif kind == KIND_ACCESS and not flags & F_HIT:
+            demand[(tok, layer)].append((layer, slot))
+    assert spec and demand  # both kinds of copy happen in this run
+    _say(f"poisoned slots, {mode}: {sum(map(len, spec.values()))} speculative, "
+         f"{sum(map(len, demand.values()))} demand")
+    moe = tiny.cache(S, "lru", prefetch_max=2, fetch_mode=fm)
+    arena = moe.arena.view(cfg.layers, S, cfg.expert_bytes)
+    H = torch.from_numpy(wl.hidden_states(cfg, T)).to("cuda")
+    with torch.cuda.stream(moe.compute):
+        for t in range(T):
+            for l in range(cfg.layers):
+                moe.copy.wait_stream(moe.compute)
+                with torch.cuda.stream(moe.copy):
+                    for layer, slot in spec[(t, l)] + (demand[(t, l)] if mode == "dma" else []):
+                        arena[layer, slot].fill_(255)
+                    torch.cuda._sleep(200000)
+                if mode != "dma":
+                    for layer, slot in demand[(t, l)]:
+                        arena[layer, slot].fill_(255)
+                b.moe_decode_layer(moe.handle, l, H[t].data_ptr(), b.MOE_PREFETCH_NEXT)
+    moe.sync()
+    recs, _ = moe.trace_records()
+    assert recs == recs0
+    out = H.cpu().numpy()
+    assert np.isfinite(out).all()
+    assert out.tobytes() == H0.tobytes()
+    moe.close()
+
+
 def test_reset_replays_identically(tiny):
     _say("reset replay")
     moe = tiny.cache(4, "lfu")
