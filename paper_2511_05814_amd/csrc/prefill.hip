@@ -652,6 +652,9 @@ __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) v
     }
   };
   const int nk = (K + KS - 1) / KS;
+  // a wave whose rows all lie past the group's end stages and waits with the
+  // others but skips its products
+  const bool rows_here = t.m0 + wm * WR < j.nrows;
   gload(0, 0);
   lstore(0, 0, 0);
 #pragma unroll
@@ -662,7 +665,7 @@ __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) v
 #pragma unroll
     for (int u = 0; u < P; ++u) {
       const int s = i + u;  // slice multiplied now, out of LDS buffer s & 1
-      mma(s & 1);
+      if (rows_here) mma(s & 1);
       lstore(u, (s & 1) ^ 1, (s + 1) * KS);            // slice s + 1 lives in slot s % P = u
       gload(u, min(s + 1 + P, nk - 1) * KS);           // slot u is free again
       __syncthreads();
@@ -672,7 +675,7 @@ __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) v
   for (int u = 0; u < P; ++u) {  // the last nk - i <= P steps; their slices are all loaded
     const int s = i + u;
     if (s < nk) {
-      mma(s & 1);
+      if (rows_here) mma(s & 1);
       if (s + 1 < nk) lstore(u, (s & 1) ^ 1, (s + 1) * KS);
       __syncthreads();
     }
@@ -855,6 +858,11 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   };
 
   const int nk = (K + KS - 1) / KS;
+  // A wave whose rows all lie past the group's end (the last tile of an
+  // expert) still stages its share of every slice and meets the others at the
+  // barriers, but skips its products: its SIMD's matrix core then serves the
+  // other wave on it alone.
+  const bool rows_here = t.m0 + wm * WR < j.nrows;
   // slices 0 .. S - 2 in flight before the first step
   issue(0, L0, L0 + BM);
   if (1 < nk) issue(KS, L1, L1 + BM);
@@ -874,7 +882,7 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
       __builtin_amdgcn_s_barrier();                                             \
       __builtin_amdgcn_sched_barrier(0);                                        \
       if (s + S - 1 < nk) issue((s + S - 1) * KS, AN, BN_);                     \
-      mma(AC, BC);                                                              \
+      if (rows_here) mma(AC, BC);                                               \
     }                                                                           \
   }
   for (int s0 = 0; s0 < nk; s0 += S) {
