@@ -90,13 +90,21 @@ def test_trace_ring_overflow_keeps_the_newest_records():
     rig.store.close()
 
 
-def test_zero_hidden_state_ties_to_the_lowest_ids():
+@pytest.mark.parametrize("experts,top_k,d_model,slots,flags", [
+    (8, 2, None, 4, 0),
+    # with speculation (both roles, two workgroups), 16 and 64 experts
+    (16, 2, 128, 4, b.MOE_PREFETCH_NEXT),
+    (64, 8, 2048, 16, b.MOE_PREFETCH_NEXT),
+])
+def test_zero_hidden_state_ties_to_the_lowest_ids(experts, top_k, d_model, slots, flags):
     # h = 0: every logit is exactly 0, the tie rule picks experts 0..K-1, the
     # combine weights are uniform and the layer output is exactly zero
-    cfg = wl.CONFIGS["tiny-stack"].with_(dtype="bf16", tokens=3)
+    cfg = wl.CONFIGS["tiny-stack"].with_(dtype="bf16", tokens=3, experts=experts, top_k=top_k,
+                                         d_model=d_model or wl.CONFIGS["tiny-stack"].d_model)
+    _say("zero h", experts, top_k, cfg.d_model)
     rig = Rig(cfg)
-    moe = rig.cache(4, "lfu")
-    hs, recs, H = rig.run(moe, 3, h0=np.zeros((3, cfg.d_model), np.float32))
+    moe = rig.cache(slots, "lfu", prefetch_max=2 if flags else 0)
+    hs, recs, H = rig.run(moe, 3, flags=flags, h0=np.zeros((3, cfg.d_model), np.float32))
     assert np.all(H == 0.0)
     for r in recs:
         assert r[4] == r[3]  # rank r -> expert r
