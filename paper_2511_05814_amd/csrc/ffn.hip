@@ -28,10 +28,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
 constexpr int kUpRows = 2;     // rows per wave (register path)
-#ifndef MOE_FFN_UP_ROWS_NARROW
-#define MOE_FFN_UP_ROWS_NARROW 2
-#endif
-constexpr int kUpRowsNarrow = MOE_FFN_UP_ROWS_NARROW;  // the same for d <= 2048 (2 or 4)
 constexpr int kUpLdsRows = 1;  // row pairs per wave on the wide-model path
 constexpr int kReduceThreads = 64;
 constexpr int kFusedThreads = 512;  // fused down: eight waves, one rank each
@@ -376,15 +372,13 @@ void launch_up_steps(bool ragged, const FfnArgs &a, const Launch &l) {
     MOE_LAUNCH((ffn_up_kernel<DT, STEPS, RPW, false>), grid, dim3(kThreads), 0, l, a);
 }
 
+// (four rows a wave at d <= 2048 measured no faster than two)
 template <int DT, int STEPS>
 void launch_up_rows(bool ragged, const FfnArgs &a, const Launch &l) {
   // rows of fewer than STEPS whole steps (d = 1536 in bf16 on the 4-step
   // kernel) take the ragged form, which reads zeros past d
   ragged = ragged || a.d != STEPS * kWave * Elem<DT>::kVec;
-  if (a.d <= 2048 && kUpRowsNarrow == 4)
-    launch_up_steps<DT, STEPS, 4>(ragged, a, l);
-  else
-    launch_up_steps<DT, STEPS, kUpRows>(ragged, a, l);
+  launch_up_steps<DT, STEPS, kUpRows>(ragged, a, l);
 }
 
 template <int DT>
