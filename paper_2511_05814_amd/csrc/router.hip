@@ -2,10 +2,10 @@
 //
 // One workgroup per role and call: routing and the table lookups of the layer
 // being decoded, and, when speculating, the guess and insertion for the next
-// layer.  All 16 waves of a workgroup first compute the gate logits
-// z = W_g h (Sec. 4.3: the gate is a linear map [len_hidden, num_experts]) for
-// the layer being decoded and, when speculating, for the next layer (Sec. 3.2:
-// the next layer's gate applied to the current hidden state).  Each product
+// layer.  All 16 waves of a workgroup first compute its role's gate logits
+// z = W_g h (Sec. 4.3: the gate is a linear map [len_hidden, num_experts]):
+// for the layer being decoded, or for the next layer (Sec. 3.2: the next
+// layer's gate applied to the current hidden state).  Each product
 // of a bf16/fp32 weight and an fp32 activation is exact in fp64, and the sums
 // are accumulated in fp64 so that the top-K decision is the one an fp64
 // evaluation makes.
