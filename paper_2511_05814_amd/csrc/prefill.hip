@@ -703,22 +703,21 @@ __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) v
 // 256-row tiles with the operands staged by the memory system itself: every
 // 16-byte load goes straight from global memory into LDS (buffer_load ...
 // lds), so no register holds a slice on its way and no wave spends
-// instructions storing one.  kDmaStages LDS buffers of one 32-deep slice each
-// (32 KB: A 256 x 32, B 256 x 32) form a ring; a step waits for its own
-// slice's loads, meets the other waves at one barrier (after which the buffer
-// multiplied in the previous step is free), issues the loads of the slice
-// kDmaStages - 1 ahead into that buffer and multiplies.  One load instruction
-// of a wave fills 1 KB of LDS, lane i at byte 16 i: 16 rows of 64 bytes.  Lane
-// i therefore fetches the chunk that the swizzle (lds_chunk) puts at its
-// place, chunk (i % 4) ^ ((row / 4) % 4) of row i / 4.  The loads are
-// issued as inline instructions the compiler does not track, so the waits are
-// the kernel's own: before a step, at most the loads of the kDmaStages - 2
-// slices after it may be outstanding.  Rows past a
-// group's end read its last row (not written); a K tail's chunks are fetched
-// from an offset past the buffer's record count, which the hardware turns into
-// zeros.
-constexpr int kDmaStages = 4;  // three slices in flight measured slower (678 against 739 TFLOP/s up)
-constexpr int kDmaKs = 32;
+// instructions storing one.  Two LDS buffers of one 64-deep slice each (64 KB:
+// A 256 rows, B 256 rows) alternate: a step waits for its own slice's loads,
+// meets the other waves at one barrier (after which the buffer multiplied in
+// the previous step is free), issues the next slice's loads into that buffer
+// and multiplies.  (Four buffers of 32-deep slices kept three slices in
+// flight but met at twice as many barriers: 5-8% slower.)  One load
+// instruction of a wave fills 1 KB of LDS, lane i at byte 16 i: 8 rows of 128
+// bytes, so lane i fetches the chunk that the swizzle (lds_chunk) puts at its
+// place, chunk (i % 8) ^ ((row / 2) % 8) of row i / 8.  The loads are issued
+// as inline instructions the compiler does not track, so the waits are the
+// kernel's own.  Rows past a group's end read its last row (not written); a K
+// tail's chunks are fetched from an offset past the buffer's record count,
+// which the hardware turns into zeros.
+constexpr int kDmaStages = 2;
+constexpr int kDmaKs = 64;
 #ifndef MOE_GEMM_DMA_WAVES
 #define MOE_GEMM_DMA_WAVES 8
 #endif
@@ -761,15 +760,16 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   constexpr int NB = UP ? 2 : 1;
   constexpr int BN = gemm_cols<UP>();
   constexpr int WM = WAVES / 2, WR = BM / WM, WC = BN / 2, MX = WR / 32, NY = WC / 32;
-  constexpr int IPW = 16 / WAVES;   // load instructions per wave and slice for A, and as many for B
-  constexpr int RPW = BM / WAVES;   // slice rows a wave fills (16 per instruction)
+  constexpr int CPR = KS / 8, RPI = kWave / CPR;  // 16-byte chunks a row; rows one load instruction fills
+  constexpr int IPW = BM / RPI / WAVES;          // load instructions per wave and slice for A, and as many for B
+  constexpr int RPW = BM / WAVES;                // slice rows a wave fills
   constexpr int LOADS = 2 * IPW;
   static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
   static_assert(NB * BN == 256, "B slice of 256 rows");
 
   // one array per ring buffer: the A slice (rows 0 .. BM - 1), then the B slice
-  __shared__ uint16_t L0[BM + NB * BN][KS], L1[BM + NB * BN][KS], L2[BM + NB * BN][KS], L3[BM + NB * BN][KS];
-  static_assert(S == 4, "the steps below are unrolled for four buffers");
+  __shared__ uint16_t L0[BM + NB * BN][KS], L1[BM + NB * BN][KS];
+  static_assert(S == 2, "the steps below are unrolled for two buffers");
   const GemmTile t = tiles[xcd_tile(blockIdx.x, gridDim.x)];
   const GemmJob j = jobs[t.job];
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
@@ -780,8 +780,8 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   if (j.nrows <= 0) return;  // the plan makes no such tiles
 
   // this lane's rows and chunks: load instruction i of the wave fills LDS
-  // rows RPW wave + 16 i .. + 15 of the A slice and of the B slice
-  const int prow0 = RPW * wave + lane / 4;  // + 16 i
+  // rows RPW wave + RPI i .. + RPI - 1 of the A slice and of the B slice
+  const int prow0 = RPW * wave + lane / CPR;  // + RPI i
   const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(a_src), 0, a_bytes,
                                                                         0x00020000);
   const int nb = min(BN, N - t.n0);
@@ -794,8 +794,8 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   int achunk[IPW], bchunk[IPW], bmat[IPW];
 #pragma unroll
   for (int i = 0; i < IPW; ++i) {
-    const int r = prow0 + 16 * i;  // row of the A slice (0..255) and of the B slice (0..255)
-    const int c = (lane % 4) ^ ((r / 4) % 4);
+    const int r = prow0 + RPI * i;  // row of the A slice (0..255) and of the B slice (0..255)
+    const int c = lds_chunk<KS>(r, lane % CPR);  // the chunk the swizzle puts at this lane's place
     const int m = min(t.m0 + r, j.nrows - 1);
     const size_t arow = UP ? (size_t)perm_tok[j.row0 + m] * d : (size_t)(j.row0 + m) * d_ff;
     aoff[i] = (uint32_t)(arow * 2) + 16u * c;
@@ -803,20 +803,20 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
     const int br = r % BN;
     boff[i] = (uint32_t)min(br, nb - 1) * K * 2 + 16u * c;
     bchunk[i] = c;
-    bmat[i] = (RPW * wave + 16 * i) / BN;  // B matrix of the instruction (uniform)
+    bmat[i] = (RPW * wave + RPI * i) / BN;  // B matrix of the instruction (uniform)
   }
 
   auto issue = [&](int k0, uint16_t (*As)[KS], uint16_t (*Bs)[KS]) {
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const bool oob_a = RAGGED && k0 + 8 * achunk[i] >= K;
-      dma16(ars, &As[RPW * wave + 16 * i][0], oob_a ? kOobOffset : aoff[i] + 2u * k0);
+      dma16(ars, &As[RPW * wave + RPI * i][0], oob_a ? kOobOffset : aoff[i] + 2u * k0);
     }
 #pragma unroll
     for (int i = 0; i < IPW; ++i) {
       const bool oob_b = RAGGED && k0 + 8 * bchunk[i] >= K;
       const __amdgpu_buffer_rsrc_t r = bmat[i] == 0 ? brs[0] : brs[NB - 1];
-      dma16(r, &Bs[RPW * wave + 16 * i][0], oob_b ? kOobOffset : boff[i] + 2u * k0);
+      dma16(r, &Bs[RPW * wave + RPI * i][0], oob_b ? kOobOffset : boff[i] + 2u * k0);
     }
   };
 
@@ -858,8 +858,6 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   const bool rows_here = t.m0 + wm * WR < j.nrows;
   // slices 0 .. S - 2 in flight before the first step
   issue(0, L0, L0 + BM);
-  if (1 < nk) issue(KS, L1, L1 + BM);
-  if (2 < nk) issue(2 * KS, L2, L2 + BM);
   // step s: buffer s % S; the slice S - 1 ahead goes to buffer (s - 1) % S
 #define MOE_DMA_STEP(U, AC, BC, AN, BN_)                                        \
   {                                                                             \
@@ -877,10 +875,8 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
     }                                                                           \
   }
   for (int s0 = 0; s0 < nk; s0 += S) {
-    MOE_DMA_STEP(0, L0, L0 + BM, L3, L3 + BM)
+    MOE_DMA_STEP(0, L0, L0 + BM, L1, L1 + BM)
     MOE_DMA_STEP(1, L1, L1 + BM, L0, L0 + BM)
-    MOE_DMA_STEP(2, L2, L2 + BM, L1, L1 + BM)
-    MOE_DMA_STEP(3, L3, L3 + BM, L2, L2 + BM)
   }
 #undef MOE_DMA_STEP
   // lane i holds column i % 32 of each 32 x 32 block, rows 8 (v / 4) + 4 (i / 32) + v % 4
