@@ -572,7 +572,9 @@ int moe_cache_bind(moe_cache_t *c, const moe_model_desc *d) {
   HIP_TRY0(pool_pinned(c->dev, 3 * sizeof(FetchList), reinterpret_cast<void **>(&c->mirror), &c->mirror_bytes));
   if (c->max_T > 0) {
     c->play = prefill_layout(c->K, c->d, c->dff, c->E, c->S, c->max_T, c->B, coded_store(c->host_format) ? c->Bh : 0);
-    HIP_TRY0(pool_pinned(c->dev, sizeof(PrefillPlan) * kMaxE, reinterpret_cast<void **>(&c->h_plan), &c->plan_bytes));
+    // the plan of every expert, then the device's error word
+    HIP_TRY0(pool_pinned(c->dev, sizeof(PrefillPlan) * kMaxE + sizeof(int32_t), reinterpret_cast<void **>(&c->h_plan),
+                         &c->plan_bytes));
     HIP_TRY0(pool_pinned(c->dev,
                          sizeof(GemmJob) * kMaxE + sizeof(GemmTile) * (size_t)c->play.tile_cap +
                              sizeof(FetchList) * kPrefillLists,
@@ -789,10 +791,10 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
     if (demand) HIP_TRY(c, hipMemcpyAsync(&c->mirror[0], c->dl + layer, sizeof(FetchList), hipMemcpyDeviceToHost, c->cs));
     if (spec_layer >= 0)
       HIP_TRY(c, hipMemcpyAsync(&c->mirror[1], c->pl + spec_layer, sizeof(FetchList), hipMemcpyDeviceToHost, c->cs));
-    HIP_TRY(c, hipStreamSynchronize(c->cs));
-    int32_t e = 0;
-    HIP_TRY(c, hipMemcpy(&e, c->err, sizeof e, hipMemcpyDeviceToHost));
-    if (e != ERR_NONE) return MOE_OK;  // reported at the next synchronising call
+    int32_t *err_mirror = reinterpret_cast<int32_t *>(&c->mirror[2]);
+    HIP_TRY(c, hipMemcpyAsync(err_mirror, c->err, sizeof(int32_t), hipMemcpyDeviceToHost, c->cs));
+    HIP_TRY(c, hipStreamSynchronize(c->cs));  // one wait for the lists and the error word
+    if (*err_mirror != ERR_NONE) return MOE_OK;  // reported at the next synchronising call
   }
   if (demand && !no_copies) {
     // a slot the router just took may still be receiving a speculative copy
@@ -966,11 +968,14 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     c->last_prefill_T = T;
     return MOE_OK;  // routing errors surface at the next synchronising call
   }
+  // one wait for both the plan and the error word (a second, synchronous
+  // read of the word cost another round trip of about 30 us per layer)
+  int32_t *h_err = reinterpret_cast<int32_t *>(c->h_plan + kMaxE);
   HIP_TRY(c, hipMemcpyAsync(c->h_plan, plan, sizeof(PrefillPlan) * c->E, hipMemcpyDeviceToHost, c->cs));
+  HIP_TRY(c, hipMemcpyAsync(h_err, c->err, sizeof(int32_t), hipMemcpyDeviceToHost, c->cs));
   HIP_TRY(c, hipStreamSynchronize(c->cs));
   {
-    int32_t e = 0;
-    HIP_TRY(c, hipMemcpy(&e, c->err, sizeof e, hipMemcpyDeviceToHost));
+    const int32_t e = *h_err;
     if (e != ERR_NONE) {
       c->sticky = MOE_ERR_HIP;
       return fail(MOE_ERR_HIP, "prefill routing produced an invalid expert id (code %d)", e);
@@ -1146,8 +1151,10 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     c->sticky = MOE_ERR_HIP;
     return fail(MOE_ERR_HIP, "prefill fetch-list overflow");
   }
-  HIP_TRY(c, hipMemcpyAsync(jobs, hj, sizeof(GemmJob) * kMaxE, hipMemcpyHostToDevice, c->cs));
-  if (nt > 0) HIP_TRY(c, hipMemcpyAsync(tiles, ht, sizeof(GemmTile) * nt, hipMemcpyHostToDevice, c->cs));
+  // the jobs and the tiles after them, in one copy: the two lie back to back
+  // in the pinned schedule and in the workspace
+  static_assert(sizeof(GemmJob) * kMaxE % 256 == 0, "tiles follow the jobs in the workspace");
+  HIP_TRY(c, hipMemcpyAsync(jobs, hj, sizeof(GemmJob) * kMaxE + sizeof(GemmTile) * nt, hipMemcpyHostToDevice, c->cs));
   if (nl > 0) HIP_TRY(c, hipMemcpyAsync(dlists, hl, sizeof(FetchList) * nl, hipMemcpyHostToDevice, c->cs));
 
   const double up_flop_per_row = 4.0 * c->d * c->dff, down_flop_per_row = 2.0 * c->d * c->dff;
@@ -1238,8 +1245,10 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
                                   host + (size_t)e * c->B, c->B, hipMemcpyHostToDevice, q));
     }
   }
-  HIP_TRY(c, hipEventRecord(evF, q));
-  HIP_TRY(c, hipStreamWaitEvent(c->cs, evF, 0));
+  if (!batches.empty() || !unrouted_new.empty()) {  // copies were issued on the copy stream
+    HIP_TRY(c, hipEventRecord(evF, q));
+    HIP_TRY(c, hipStreamWaitEvent(c->cs, evF, 0));
+  }
   HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, Launch{c->cs}));
   HIP_TRY(c, span_end(c, c->cs, SPAN_PREFILL, tp));
   // later decode calls on this layer need no extra wait: the compute stream
