@@ -143,10 +143,17 @@ struct PlanArgs {
   uint64_t expert_bytes;
   int T, K, E, S, layer, policy;
   int aging;  // aged LFU: lookup-clock ticks per halving of a count
-  // Batches planned on the device (every expert resident, small-M GEMMs):
-  // the kernel also writes one GEMM job and tile per expert; nullptr otherwise.
+  // Batches planned on the device (a slot for every expert): the kernel also
+  // writes one GEMM job per expert; nullptr otherwise.  Small batches
+  // (ntiles == nullptr) take one small-M tile per expert.  Large ones take
+  // tile lists of tile_rows rows by up_cols / dn_cols columns, ordered (expert,
+  // column block, row block): the up list at tiles[0 ..], the down list at
+  // tiles[dn_first ..], at most up_cap and dn_cap tiles, their lengths
+  // written to ntiles[0] and ntiles[1].
   GemmJob *jobs;
   GemmTile *tiles;
+  int32_t *ntiles;
+  int tile_rows, up_cols, dn_cols, up_cb, dn_cb, dn_first, up_cap, dn_cap;
   const uint8_t *arena_layer;  // this layer's slots
   uint64_t slot_bytes;
 };
@@ -203,10 +210,11 @@ hipError_t launch_prefill_gate(const PrefillArgs &a, const Launch &l);
 hipError_t launch_prefill_plan(const PlanArgs &a, const Launch &l);
 // grouped GEMMs over tiles of `rows` (64, 128 or 256) sorted pairs by
 // prefill_tile_cols(up) output columns; a_bytes: size of the A operand's
-// buffer (xn for up, act for down)
+// buffer (xn for up, act for down).  With dev_ntiles, the list's length is
+// read on the device (at most ntiles, the grid; the surplus workgroups exit).
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, size_t a_bytes,
-                             const Launch &l);
+                             const Launch &l, const int32_t *dev_ntiles = nullptr);
 // Small-M grouped GEMMs: one tile {job, 0, 0} per expert, each with at most
 // max_rows <= kSkinnyRows rows (the caller's bound: rows beyond 16 are read
 // only when max_rows > 16); a workgroup per (tile, 16 output features).
@@ -217,7 +225,8 @@ hipError_t launch_prefill_skinny_up(const GemmTile *tiles, int ntiles, const Gem
 hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
                                       float *Y, int d, int d_ff, int max_rows, const Launch &l);
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, int rows, size_t a_bytes, const Launch &l);
+                               float *Y, int d, int d_ff, int rows, size_t a_bytes, const Launch &l,
+                               const int32_t *dev_ntiles = nullptr);
 hipError_t launch_prefill_unpermute(float *H, const float *Y, const float *g, const int32_t *pos_of, int T,
                                     int d, int K, const Launch &l);
 int prefill_tile_cols(bool up);  // GEMM output tile columns (act for up, Y for down)

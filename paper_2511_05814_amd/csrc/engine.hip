@@ -160,7 +160,7 @@ namespace moe {
 // Prefill workspace for batches of up to T tokens (offsets from its base).
 struct PrefillLayout {
   size_t ids = 0, g = 0, inv_r = 0, xn = 0, perm = 0, pos = 0, plan = 0, jobs = 0, tiles = 0, act = 0,
-         y = 0, staging = 0, coded = 0, lists = 0, total = 0;
+         y = 0, staging = 0, coded = 0, lists = 0, ntiles = 0, total = 0;
   int tile_cap = 0;  // GEMM tiles the schedule can hold
   int ring = 0;      // staging slots for experts streamed through the batch
 };
@@ -198,6 +198,7 @@ static PrefillLayout prefill_layout(int K, int d, int d_ff, int E, int S, int T,
   p.staging = take((size_t)p.ring * B);
   p.coded = take(Bh ? (size_t)(p.ring / 2) * Bh : 0);
   p.lists = take(Bh ? sizeof(FetchList) * kPrefillLists : 0);
+  p.ntiles = take(2 * sizeof(int32_t));  // lengths of device-written tile lists
   p.total = off;
   return p;
 }
@@ -209,6 +210,7 @@ struct moe_cache {
   bool pooled = false;   // holds runtime objects taken from the process pool
   moe_model_desc desc{};
   int K = 0, d = 0, dff = 0, dtype = 0, pmax = 0, fetch_mode = 0, max_T = 0;
+  int cus = 0;           // compute units of the device (prefill tile sizing), read on first use
   uint64_t B = 0;        // bytes of one expert in an HBM slot
   int host_format = 0;   // MOE_HOST_*
   uint64_t Bh = 0;       // stride of one expert in the host store (bytes a miss moves)
@@ -879,6 +881,19 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
 
 namespace moe {
 
+// compute units of the handle's device (read once)
+static int device_cus(moe_cache *c) {
+  if (c->cus <= 0) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    (void)hipGetLastError();
+    c->cus = cus;
+  }
+  return c->cus;
+}
+
 // Batched prefill of one layer.  Routing and the cache decision run on the
 // device; the host then waits for the plan (a few hundred bytes), because it
 // has to issue one copy per streamed expert and size the grouped GEMMs:
@@ -889,6 +904,9 @@ namespace moe {
 //   compute: wait C_j -> GEMMs of batch j -> event G_j
 //   copy:    newcomers nobody routed (wait A) -> event F; compute waits F
 //   compute: unpermute (h += sum_r g Y)
+// With a slot for every expert nothing is streamed, and the plan kernel also
+// plans the GEMMs (one small-M tile per expert for small batches, the tall
+// tile lists for large ones), so the host waits for nothing.
 int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   const PrefillLayout &p = c->play;
   uint8_t *base = c->prefill_ws;
@@ -947,12 +965,51 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   // kSkinnyRows tokens every expert's rows fit the small-M GEMMs: the plan
   // kernel then writes the GEMM jobs itself and the host does not wait for it.
   const bool device_plan = c->S == c->E && T <= kSkinnyRows;
-  pa.jobs = device_plan ? jobs : nullptr;
-  pa.tiles = device_plan ? tiles : nullptr;
+  // A larger batch with a slot for every expert, when 256-row tiles give every
+  // CU two tiles whatever the routing (the rule the host applies below picks
+  // them then): the plan kernel writes both tile lists and the GEMMs read
+  // their lengths, so the host waits for nothing.  The grids cover the longest
+  // lists any routing can give.
+  const int up_cols = prefill_tile_cols(true), down_cols = prefill_tile_cols(false);
+  const int up_cb = (c->dff + up_cols - 1) / up_cols, dn_cb = (c->d + down_cols - 1) / down_cols;
+  const long pairs = (long)T * c->K;
+  const int tall_cap_rows = (int)((pairs + 255) / 256) + c->E;  // bounds the sum of ceil(n_e / 256)
+  const int up_cap = tall_cap_rows * up_cb, dn_cap = tall_cap_rows * dn_cb;
+  const bool device_tall = c->S == c->E && !device_plan && (pairs / 256) * std::min(up_cb, dn_cb) >= 2L * device_cus(c) &&
+                           up_cap + dn_cap <= p.tile_cap;
+  int32_t *dev_ntiles = reinterpret_cast<int32_t *>(base + p.ntiles);
+  pa.jobs = device_plan || device_tall ? jobs : nullptr;
+  pa.tiles = device_plan || device_tall ? tiles : nullptr;
+  pa.ntiles = device_tall ? dev_ntiles : nullptr;
+  pa.tile_rows = 256;
+  pa.up_cols = up_cols;
+  pa.dn_cols = down_cols;
+  pa.up_cb = up_cb;
+  pa.dn_cb = dn_cb;
+  pa.dn_first = up_cap;
+  pa.up_cap = up_cap;
+  pa.dn_cap = dn_cap;
   pa.arena_layer = arena + (size_t)layer * c->S * c->B;
   pa.slot_bytes = c->B;
   HIP_TRY(c, launch_prefill_plan(pa, Launch{c->cs}));
   c->tpar ^= 1;
+  if (device_tall) {
+    const double rows = (double)pairs;
+    Launch lu, ld;
+    HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_GEMM_UP));
+    HIP_TRY(c, launch_prefill_up(tiles, up_cap, jobs, xn, perm, act, c->d, c->dff, 256, (size_t)c->max_T * c->d * 2, lu,
+                                 dev_ntiles));
+    kernel_span_done(c, SPAN_GEMM_UP, lu, rows * 4.0 * c->d * c->dff);
+    HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
+    HIP_TRY(c, launch_prefill_down(tiles + up_cap, dn_cap, jobs, act, Y, c->d, c->dff, 256,
+                                   (size_t)c->max_T * c->K * c->dff * 2, ld, dev_ntiles + 1));
+    kernel_span_done(c, SPAN_GEMM_DOWN, ld, rows * 2.0 * c->d * c->dff);
+    HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, Launch{c->cs}));
+    HIP_TRY(c, span_end(c, c->cs, SPAN_PREFILL, tp));
+    c->last_route_kind = 2;
+    c->last_prefill_T = T;
+    return MOE_OK;  // routing errors surface at the next synchronising call
+  }
   if (device_plan) {
     const double rows = (double)T * c->K;
     Launch lu, ld;
@@ -1035,15 +1092,7 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   // block's weights are read once for all of the expert's row blocks by
   // workgroups that run at the same time on one XCD (the kernel hands each
   // XCD a contiguous stretch of this list).
-  const int up_cols = prefill_tile_cols(true), down_cols = prefill_tile_cols(false);
-  int cus = 0;
-  {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-      cus = 256;
-    (void)hipGetLastError();
-  }
+  const int cus = device_cus(c);
   int nt = 0;
   bool overflow = false;  // checked before each write: ht is a fixed-size pinned buffer
   auto add_tiles = [&](const std::vector<int> &group, int ncols, int cols, int &first, int &count, int &rows) {

@@ -291,6 +291,7 @@ constexpr int kPlanAhead = 8;
 
 __global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PlanArgs a) {
   __shared__ int cnt[kMaxE], cur[kMaxE], lastp[kMaxE], offs[kMaxE];
+  __shared__ int tfirst[2][kMaxE], trows[kMaxE], tlen[2];  // tile lists (when a.ntiles)
   __shared__ int bad;
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int E = a.E, P = a.T * a.K;
@@ -302,7 +303,7 @@ __global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PlanArgs a) 
   if (tid == 0) bad = 0;
   if (a.jobs && tid < E) {  // empty until the table step below fills them in
     a.jobs[tid] = GemmJob{nullptr, 0, 0};
-    a.tiles[tid] = GemmTile{tid, 0, 0, 0};
+    if (!a.ntiles) a.tiles[tid] = GemmTile{tid, 0, 0, 0};
   }
   __syncthreads();
   for (int p0 = tid; p0 < P; p0 += kPlanAhead * kPlanThreads) {
@@ -342,8 +343,55 @@ __global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(PlanArgs a) 
       if (lane >= o) incl += v;
     }
     if (lane < E) offs[lane] = incl - c;
+    if (a.ntiles) {
+      // expert e's tiles: rt row blocks in each column block; the lists'
+      // first tile of each expert by the same scan
+      const int rt = (c + a.tile_rows - 1) / a.tile_rows;
+      int iu = rt * a.up_cb, id = rt * a.dn_cb;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int vu = __shfl_up(iu, o, kWave), vd = __shfl_up(id, o, kWave);
+        if (lane >= o) {
+          iu += vu;
+          id += vd;
+        }
+      }
+      if (lane < E) {
+        trows[lane] = rt;
+        tfirst[0][lane] = iu - rt * a.up_cb;
+        tfirst[1][lane] = id - rt * a.dn_cb;
+      }
+      if (lane == kWave - 1) {
+        const bool fits = iu <= a.up_cap && id <= a.dn_cap;  // the host's bound holds for any counts
+        tlen[0] = fits ? iu : 0;
+        tlen[1] = fits ? id : 0;
+        a.ntiles[0] = tlen[0];
+        a.ntiles[1] = tlen[1];
+        if (!fits) *a.err = ERR_BAD_LIST;
+      }
+    }
   }
   __syncthreads();
+  if (a.ntiles) {
+    // tile i of a list belongs to the last expert whose first tile is <= i
+    const int nup = tlen[0], n_all = tlen[0] + tlen[1];
+    for (int i = tid; i < n_all; i += kPlanThreads) {
+      const int list = i < nup ? 0 : 1;
+      const int li = list == 0 ? i : i - nup;
+      int lo = 0, hi = E - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (tfirst[list][mid] <= li)
+          lo = mid;
+        else
+          hi = mid - 1;
+      }
+      const int k = li - tfirst[list][lo], rt = trows[lo];
+      const int cb = k / rt, mb = k - cb * rt;
+      a.tiles[(list == 0 ? 0 : a.dn_first) + li] =
+          GemmTile{lo, mb * a.tile_rows, cb * (list == 0 ? a.up_cols : a.dn_cols), 0};
+    }
+  }
   for (int p0 = tid; p0 < P; p0 += kPlanAhead * kPlanThreads) {
     int ev[kPlanAhead];
 #pragma unroll
@@ -569,6 +617,12 @@ __device__ __forceinline__ int xcd_tile(int b, int n) {
   return x * per + min(x, rem) + i;
 }
 
+// Tiles in the launch's list: the grid, or the length the plan kernel wrote
+// (never more than the grid, which the host sized for the longest list).
+__device__ __forceinline__ int tile_count(const int32_t *dev_ntiles) {
+  return dev_ntiles ? min(*dev_ntiles, (int)gridDim.x) : (int)gridDim.x;
+}
+
 // Output columns of a tile: 128 against W1 and W3 (the up projection keeps
 // two accumulators per output), 256 against W2, so both hold the same number
 // of accumulators and stage the same bytes per step.
@@ -580,7 +634,7 @@ constexpr int gemm_cols() {
 template <bool UP, int P, int BM, int THREADS, int KS, bool RAGGED>
 __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) void prefill_gemm_kernel(
     const GemmTile *tiles, const GemmJob *jobs, const uint16_t *a_src, const int32_t *perm_tok, void *out, int d,
-    int d_ff) {
+    int d_ff, const int32_t *dev_ntiles) {
   constexpr int NB = UP ? 2 : 1;         // B matrices: W1 and W3, or W2
   constexpr int BN = gemm_cols<UP>();    // output columns of the tile
   constexpr int WM = THREADS / kWave / 2;  // waves along M (two along N)
@@ -595,7 +649,9 @@ __global__ __launch_bounds__(THREADS, THREADS == 512 ? 1 : (BM == 64 ? 3 : 2)) v
   static_assert(WR % 32 == 0 && BM % SR == 0 && BN % SR == 0, "tile shape");
   __shared__ uint16_t As[2][BM][KS];
   __shared__ uint16_t Bs[2][NB][BN][KS];
-  const GemmTile t = tiles[xcd_tile(blockIdx.x, gridDim.x)];
+  const int nt = tile_count(dev_ntiles);
+  if ((int)blockIdx.x >= nt) return;  // a surplus workgroup of a device-sized list
+  const GemmTile t = tiles[xcd_tile(blockIdx.x, nt)];
   const GemmJob j = jobs[t.job];
   const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const int wm = wave / 2, wn = wave % 2;
@@ -784,7 +840,7 @@ template <bool UP, bool RAGGED, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(const GemmTile *tiles, const GemmJob *jobs,
                                                                   const uint16_t *a_src, uint32_t a_bytes,
                                                                   const int32_t *perm_tok, void *out, int d,
-                                                                  int d_ff) {
+                                                                  int d_ff, const int32_t *dev_ntiles) {
   constexpr int BM = 256, KS = kDmaKs, S = kDmaStages;
   constexpr int NB = UP ? 2 : 1;
   constexpr int BN = gemm_cols<UP>();
@@ -799,7 +855,9 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   // one array per ring buffer: the A slice (rows 0 .. BM - 1), then the B slice
   __shared__ uint16_t L0[BM + NB * BN][KS], L1[BM + NB * BN][KS];
   static_assert(S == 2, "the steps below are unrolled for two buffers");
-  const GemmTile t = tiles[xcd_tile(blockIdx.x, gridDim.x)];
+  const int nt = tile_count(dev_ntiles);
+  if ((int)blockIdx.x >= nt) return;  // a surplus workgroup of a device-sized list
+  const GemmTile t = tiles[xcd_tile(blockIdx.x, nt)];
   const GemmJob j = jobs[t.job];
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -1149,28 +1207,28 @@ static bool dma_fits(size_t a_bytes) { return MOE_GEMM_DMA && a_bytes > 0 && a_b
 
 hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *xn,
                              const int32_t *perm_tok, uint16_t *act, int d, int d_ff, int rows, size_t a_bytes,
-                             const Launch &l) {
+                             const Launch &l, const int32_t *dev_ntiles) {
   if (ntiles <= 0) return hipSuccess;
   if (rows == 256 && dma_fits(a_bytes)) {
     if (d % kDmaKs == 0)
       MOE_LAUNCH((prefill_gemm_dma_kernel<true, false, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
-                 (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff);
+                 (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff, dev_ntiles);
     else
       MOE_LAUNCH((prefill_gemm_dma_kernel<true, true, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
-                 (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff);
+                 (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff, dev_ntiles);
     return hipGetLastError();
   }
 #define MOE_GEMM_UP(BM, TH, RG)                                                                                   \
   MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStages, BM, TH, kKStep, RG>), dim3(ntiles), dim3(TH), 0, l, tiles, jobs, xn, \
-             perm_tok, (void *)act, d, d_ff)
+             perm_tok, (void *)act, d, d_ff, dev_ntiles)
 #define MOE_GEMM_UP_TALL(RG)                                                                                     \
   MOE_LAUNCH((prefill_gemm_kernel<true, kGemmStagesTall, 256, 512, kKsTall, RG>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, \
-             xn, perm_tok, (void *)act, d, d_ff)
+             xn, perm_tok, (void *)act, d, d_ff, dev_ntiles)
   // a K not a multiple of the tall slice takes 32-deep slices three ahead
   // (the 64-deep kernel with its K-tail handling would spill registers)
 #define MOE_GEMM_UP_TALL_RAGGED()                                                                                   \
   MOE_LAUNCH((prefill_gemm_kernel<true, 3, 256, 512, kKStep, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, xn, \
-             perm_tok, (void *)act, d, d_ff)
+             perm_tok, (void *)act, d, d_ff, dev_ntiles)
   const bool ragged = d % kKStep != 0;
   if (rows == 64) {
     if (ragged) MOE_GEMM_UP(64, 256, true); else MOE_GEMM_UP(64, 256, false);
@@ -1215,26 +1273,27 @@ hipError_t launch_prefill_skinny_down(const GemmTile *tiles, int ntiles, const G
 }
 
 hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob *jobs, const uint16_t *act,
-                               float *Y, int d, int d_ff, int rows, size_t a_bytes, const Launch &l) {
+                               float *Y, int d, int d_ff, int rows, size_t a_bytes, const Launch &l,
+                               const int32_t *dev_ntiles) {
   if (ntiles <= 0) return hipSuccess;
   if (rows == 256 && dma_fits(a_bytes)) {
     if (d_ff % kDmaKs == 0)
       MOE_LAUNCH((prefill_gemm_dma_kernel<false, false, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
-                 (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff);
+                 (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff, dev_ntiles);
     else
       MOE_LAUNCH((prefill_gemm_dma_kernel<false, true, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
-                 (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff);
+                 (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff, dev_ntiles);
     return hipGetLastError();
   }
 #define MOE_GEMM_DOWN(BM, TH, RG)                                                                                  \
   MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStages, BM, TH, kKStep, RG>), dim3(ntiles), dim3(TH), 0, l, tiles, jobs, act, \
-             (const int32_t *)nullptr, (void *)Y, d, d_ff)
+             (const int32_t *)nullptr, (void *)Y, d, d_ff, dev_ntiles)
 #define MOE_GEMM_DOWN_TALL(RG)                                                                                     \
   MOE_LAUNCH((prefill_gemm_kernel<false, kGemmStagesTall, 256, 512, kKsTall, RG>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, \
-             act, (const int32_t *)nullptr, (void *)Y, d, d_ff)
+             act, (const int32_t *)nullptr, (void *)Y, d, d_ff, dev_ntiles)
 #define MOE_GEMM_DOWN_TALL_RAGGED()                                                                                  \
   MOE_LAUNCH((prefill_gemm_kernel<false, 3, 256, 512, kKStep, true>), dim3(ntiles), dim3(512), 0, l, tiles, jobs, act, \
-             (const int32_t *)nullptr, (void *)Y, d, d_ff)
+             (const int32_t *)nullptr, (void *)Y, d, d_ff, dev_ntiles)
   const bool ragged = d_ff % kKStep != 0;
   if (rows == 64) {
     if (ragged) MOE_GEMM_DOWN(64, 256, true); else MOE_GEMM_DOWN(64, 256, false);

@@ -116,6 +116,23 @@ def test_tall_tiles_with_a_k_tail():
     rig.store.close()
 
 
+def test_device_planned_tall_tiles():
+    # 4096 tokens of top-2 over 8 experts, every expert resident, with
+    # d = 4104 and d_ff = 2056: 256-row tiles give every CU two tiles whatever
+    # the routing (32 row blocks x 17 column blocks each way), so the plan
+    # kernel writes both tile lists and the GEMMs read their lengths on the
+    # device; both GEMMs have a K tail (4104 and 2056 are not multiples of 64)
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=1, experts=8, top_k=2, d_model=4104, d_ff=2056,
+                                         dtype="bf16", tokens=2, prefill_tokens=4096)
+    _say("device-planned tall tiles", cfg)
+    rig = Rig(cfg)
+    moe = rig.cache(8, "lfu", max_prefill_tokens=4096)
+    _, _, worst, _ = prefill_and_check(rig, moe, "lfu", 8, 4096, list(range(0, 4096, 97)) + [4095])
+    _say("worst", worst)
+    moe.close()
+    rig.store.close()
+
+
 @pytest.mark.parametrize("T", [5, 64])
 def test_small_prefill_fine_grained(T):
     # small prefills at the 64-expert shape (d = 2048): a partial and a full
