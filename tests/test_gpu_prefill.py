@@ -133,6 +133,20 @@ def test_device_planned_tall_tiles():
     rig.store.close()
 
 
+def test_device_planned_tall_tiles_64_experts():
+    # the 64-expert shape with a slot for every expert and 4096 tokens of
+    # top-8: one device-planned tall-tile launch per projection (the lists
+    # span 64 experts; d_ff = 1408 leaves a partial last column tile)
+    cfg = wl.CONFIGS["fine-grained"].with_(layers=2, tokens=2, prefill_tokens=4096)
+    _say("device-planned tall tiles, 64 experts", cfg)
+    rig = Rig(cfg)
+    moe = rig.cache(64, "lfu", max_prefill_tokens=4096)
+    _, _, worst, _ = prefill_and_check(rig, moe, "lfu", 64, 4096, list(range(0, 4096, 131)) + [4095])
+    _say("worst", worst)
+    moe.close()
+    rig.store.close()
+
+
 @pytest.mark.parametrize("T", [5, 64])
 def test_small_prefill_fine_grained(T):
     # small prefills at the 64-expert shape (d = 2048): a partial and a full
