@@ -1142,36 +1142,52 @@ __global__ __launch_bounds__(256) void prefill_skinny_kernel(const GemmTile *til
 
 // ---------------------------------------------------------------------------
 // 4. h_t += sum_r g_tr Y[pos(t, r)], ranks in order
+constexpr int kUnpermRanks = 8;  // ranks whose rows are loaded before the first is added
+constexpr int kUnpermSteps = 2;  // four-column steps per lane and pass
+
 __global__ __launch_bounds__(256) void prefill_unpermute_kernel(float *H, const float *Y, const float *g,
                                                                 const int32_t *pos_of, int T, int d, int K) {
   const int t = blockIdx.x;
   if (t >= T) return;
-  // four columns per lane per step, the steps' loads issued together (clamped
-  // to the row, so none waits behind a branch); ranks added in order
-  constexpr int kAhead = 4;
-  for (int c0 = threadIdx.x * 4; c0 < d; c0 += kAhead * 256 * 4) {
-    float4 y[kAhead], h[kAhead];
+  // A workgroup per token.  Every rank's row is loaded before the first is
+  // added, so a pass waits for its positions once and for the rows once (one
+  // rank after another, each wait was two trips to memory).  Loads are
+  // clamped to a valid rank and column, so none waits behind a branch; ranks
+  // are added in order, and a rank past K adds nothing (selected, not
+  // multiplied by zero).
+  for (int c0 = threadIdx.x * 4; c0 < d; c0 += kUnpermSteps * 256 * 4) {
+    float4 y[kUnpermSteps], h[kUnpermSteps];
 #pragma unroll
-    for (int u = 0; u < kAhead; ++u) {
+    for (int u = 0; u < kUnpermSteps; ++u) {
       y[u] = make_float4(0.f, 0.f, 0.f, 0.f);
       h[u] = *reinterpret_cast<const float4 *>(H + (size_t)t * d + min(c0 + u * 1024, d - 4));
     }
-    for (int r = 0; r < K; ++r) {
-      const float gr = g[(size_t)t * K + r];
-      const float *yr = Y + (size_t)pos_of[(size_t)t * K + r] * d;
-      float4 v[kAhead];
+    for (int r0 = 0; r0 < K; r0 += kUnpermRanks) {
+      float4 v[kUnpermRanks][kUnpermSteps];
+      float gr[kUnpermRanks];
 #pragma unroll
-      for (int u = 0; u < kAhead; ++u) v[u] = *reinterpret_cast<const float4 *>(yr + min(c0 + u * 1024, d - 4));
+      for (int i = 0; i < kUnpermRanks; ++i) {
+        const int r = min(r0 + i, K - 1);
+        gr[i] = g[(size_t)t * K + r];
+        const float *yr = Y + (size_t)pos_of[(size_t)t * K + r] * d;
 #pragma unroll
-      for (int u = 0; u < kAhead; ++u) {
-        y[u].x = fmaf(gr, v[u].x, y[u].x);
-        y[u].y = fmaf(gr, v[u].y, y[u].y);
-        y[u].z = fmaf(gr, v[u].z, y[u].z);
-        y[u].w = fmaf(gr, v[u].w, y[u].w);
+        for (int u = 0; u < kUnpermSteps; ++u)
+          v[i][u] = *reinterpret_cast<const float4 *>(yr + min(c0 + u * 1024, d - 4));
+      }
+#pragma unroll
+      for (int i = 0; i < kUnpermRanks; ++i) {
+        const bool live = r0 + i < K;
+#pragma unroll
+        for (int u = 0; u < kUnpermSteps; ++u) {
+          y[u].x = live ? fmaf(gr[i], v[i][u].x, y[u].x) : y[u].x;
+          y[u].y = live ? fmaf(gr[i], v[i][u].y, y[u].y) : y[u].y;
+          y[u].z = live ? fmaf(gr[i], v[i][u].z, y[u].z) : y[u].z;
+          y[u].w = live ? fmaf(gr[i], v[i][u].w, y[u].w) : y[u].w;
+        }
       }
     }
 #pragma unroll
-    for (int u = 0; u < kAhead; ++u) {
+    for (int u = 0; u < kUnpermSteps; ++u) {
       const int c = c0 + u * 1024;
       if (c < d) {
         float4 o = h[u];
