@@ -881,6 +881,8 @@ static int enqueue_layer(moe_cache *c, int layer, float *h, const int32_t *inj, 
 
 namespace moe {
 
+constexpr int kTallRows = 256;  // rows of a device-planned tile
+
 // compute units of the handle's device (read once)
 static int device_cus(moe_cache *c) {
   if (c->cus <= 0) {
@@ -973,15 +975,15 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
   const int up_cols = prefill_tile_cols(true), down_cols = prefill_tile_cols(false);
   const int up_cb = (c->dff + up_cols - 1) / up_cols, dn_cb = (c->d + down_cols - 1) / down_cols;
   const long pairs = (long)T * c->K;
-  const int tall_cap_rows = (int)((pairs + 255) / 256) + c->E;  // bounds the sum of ceil(n_e / 256)
+  const int tall_cap_rows = (int)((pairs + kTallRows - 1) / kTallRows) + c->E;  // bounds the sum of ceil(n_e / rows)
   const int up_cap = tall_cap_rows * up_cb, dn_cap = tall_cap_rows * dn_cb;
-  const bool device_tall = c->S == c->E && !device_plan && (pairs / 256) * std::min(up_cb, dn_cb) >= 2L * device_cus(c) &&
+  const bool device_tall = c->S == c->E && !device_plan && (pairs / kTallRows) * std::min(up_cb, dn_cb) >= 2L * device_cus(c) &&
                            up_cap + dn_cap <= p.tile_cap;
   int32_t *dev_ntiles = reinterpret_cast<int32_t *>(base + p.ntiles);
   pa.jobs = device_plan || device_tall ? jobs : nullptr;
   pa.tiles = device_plan || device_tall ? tiles : nullptr;
   pa.ntiles = device_tall ? dev_ntiles : nullptr;
-  pa.tile_rows = 256;
+  pa.tile_rows = kTallRows;
   pa.up_cols = up_cols;
   pa.dn_cols = down_cols;
   pa.up_cb = up_cb;
@@ -997,11 +999,11 @@ int prefill_enqueue(moe_cache *c, int layer, float *H, int T) {
     const double rows = (double)pairs;
     Launch lu, ld;
     HIP_TRY(c, kernel_span(c, c->cs, &lu, SPAN_GEMM_UP));
-    HIP_TRY(c, launch_prefill_up(tiles, up_cap, jobs, xn, perm, act, c->d, c->dff, 256, (size_t)c->max_T * c->d * 2, lu,
+    HIP_TRY(c, launch_prefill_up(tiles, up_cap, jobs, xn, perm, act, c->d, c->dff, kTallRows, (size_t)c->max_T * c->d * 2, lu,
                                  dev_ntiles));
     kernel_span_done(c, SPAN_GEMM_UP, lu, rows * 4.0 * c->d * c->dff);
     HIP_TRY(c, kernel_span(c, c->cs, &ld, SPAN_GEMM_DOWN));
-    HIP_TRY(c, launch_prefill_down(tiles + up_cap, dn_cap, jobs, act, Y, c->d, c->dff, 256,
+    HIP_TRY(c, launch_prefill_down(tiles + up_cap, dn_cap, jobs, act, Y, c->d, c->dff, kTallRows,
                                    (size_t)c->max_T * c->K * c->dff * 2, ld, dev_ntiles + 1));
     kernel_span_done(c, SPAN_GEMM_DOWN, ld, rows * 2.0 * c->d * c->dff);
     HIP_TRY(c, launch_prefill_unpermute(H, Y, g, pos, T, c->d, c->K, Launch{c->cs}));

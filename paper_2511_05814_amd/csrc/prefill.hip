@@ -836,21 +836,21 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <bool UP, bool RAGGED, int WAVES>
-__global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(const GemmTile *tiles, const GemmJob *jobs,
-                                                                  const uint16_t *a_src, uint32_t a_bytes,
-                                                                  const int32_t *perm_tok, void *out, int d,
-                                                                  int d_ff, const int32_t *dev_ntiles) {
-  constexpr int BM = 256, KS = kDmaKs, S = kDmaStages;
+template <bool UP, bool RAGGED, int WAVES, int BM, int KS>
+__global__ __launch_bounds__(WAVES * kWave, BM == 256 ? 1 : 2) void prefill_gemm_dma_kernel(
+    const GemmTile *tiles, const GemmJob *jobs, const uint16_t *a_src, uint32_t a_bytes, const int32_t *perm_tok,
+    void *out, int d, int d_ff, const int32_t *dev_ntiles) {
+  constexpr int S = kDmaStages;
   constexpr int NB = UP ? 2 : 1;
   constexpr int BN = gemm_cols<UP>();
   constexpr int WM = WAVES / 2, WR = BM / WM, WC = BN / 2, MX = WR / 32, NY = WC / 32;
   constexpr int CPR = KS / 8, RPI = kWave / CPR;  // 16-byte chunks a row; rows one load instruction fills
-  constexpr int IPW = BM / RPI / WAVES;          // load instructions per wave and slice for A, and as many for B
-  constexpr int RPW = BM / WAVES;                // slice rows a wave fills
-  constexpr int LOADS = 2 * IPW;
+  constexpr int RPA = BM / WAVES, RPB = NB * BN / WAVES;  // A and B slice rows a wave fills
+  constexpr int IPA = RPA / RPI, IPB = RPB / RPI;          // its load instructions per slice
+  constexpr int LOADS = IPA + IPB;
   static_assert(WAVES == 4 || WAVES == 8, "four or eight waves");
   static_assert(NB * BN == 256, "B slice of 256 rows");
+  static_assert(RPA % RPI == 0 && RPB % RPI == 0 && WR % 32 == 0, "slice rows per wave");
 
   // one array per ring buffer: the A slice (rows 0 .. BM - 1), then the B slice
   __shared__ uint16_t L0[BM + NB * BN][KS], L1[BM + NB * BN][KS];
@@ -867,8 +867,8 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   if (j.nrows <= 0) return;  // the plan makes no such tiles
 
   // this lane's rows and chunks: load instruction i of the wave fills LDS
-  // rows RPW wave + RPI i .. + RPI - 1 of the A slice and of the B slice
-  const int prow0 = RPW * wave + lane / CPR;  // + RPI i
+  // rows RPA wave + RPI i .. + RPI - 1 of the A slice, or RPB wave + RPI i ..
+  // of the B slice
   const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(a_src), 0, a_bytes,
                                                                         0x00020000);
   const int nb = min(BN, N - t.n0);
@@ -877,33 +877,37 @@ __global__ __launch_bounds__(WAVES * kWave, 1) void prefill_gemm_dma_kernel(cons
   for (int b = 0; b < NB; ++b)
     brs[b] = rows_rsrc(j.w + (UP ? (size_t)b * d_ff * d : 2 * (size_t)d_ff * d) + (size_t)t.n0 * K,
                        (uint32_t)nb * K * 2);
-  uint32_t aoff[IPW], boff[IPW];
-  int achunk[IPW], bchunk[IPW], bmat[IPW];
+  uint32_t aoff[IPA], boff[IPB];
+  int achunk[IPA], bchunk[IPB], bmat[IPB];
 #pragma unroll
-  for (int i = 0; i < IPW; ++i) {
-    const int r = prow0 + RPI * i;  // row of the A slice (0..255) and of the B slice (0..255)
-    const int c = lds_chunk<KS>(r, lane % CPR);  // the chunk the swizzle puts at this lane's place
+  for (int i = 0; i < IPA; ++i) {
+    const int r = RPA * wave + lane / CPR + RPI * i;  // row of the A slice (0 .. BM - 1)
+    const int c = lds_chunk<KS>(r, lane % CPR);       // the chunk the swizzle puts at this lane's place
     const int m = min(t.m0 + r, j.nrows - 1);
     const size_t arow = UP ? (size_t)perm_tok[j.row0 + m] * d : (size_t)(j.row0 + m) * d_ff;
     aoff[i] = (uint32_t)(arow * 2) + 16u * c;
     achunk[i] = c;
-    const int br = r % BN;
-    boff[i] = (uint32_t)min(br, nb - 1) * K * 2 + 16u * c;
+  }
+#pragma unroll
+  for (int i = 0; i < IPB; ++i) {
+    const int r = RPB * wave + lane / CPR + RPI * i;  // row of the B slice (0..255)
+    const int c = lds_chunk<KS>(r, lane % CPR);
+    boff[i] = (uint32_t)min(r % BN, nb - 1) * K * 2 + 16u * c;
     bchunk[i] = c;
-    bmat[i] = (RPW * wave + RPI * i) / BN;  // B matrix of the instruction (uniform)
+    bmat[i] = (RPB * wave + RPI * i) / BN;  // B matrix of the instruction (uniform)
   }
 
   auto issue = [&](int k0, uint16_t (*As)[KS], uint16_t (*Bs)[KS]) {
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
+    for (int i = 0; i < IPA; ++i) {
       const bool oob_a = RAGGED && k0 + 8 * achunk[i] >= K;
-      dma16(ars, &As[RPW * wave + RPI * i][0], oob_a ? kOobOffset : aoff[i] + 2u * k0);
+      dma16(ars, &As[RPA * wave + RPI * i][0], oob_a ? kOobOffset : aoff[i] + 2u * k0);
     }
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) {
+    for (int i = 0; i < IPB; ++i) {
       const bool oob_b = RAGGED && k0 + 8 * bchunk[i] >= K;
       const __amdgpu_buffer_rsrc_t r = bmat[i] == 0 ? brs[0] : brs[NB - 1];
-      dma16(r, &Bs[RPW * wave + RPI * i][0], oob_b ? kOobOffset : boff[i] + 2u * k0);
+      dma16(r, &Bs[RPB * wave + RPI * i][0], oob_b ? kOobOffset : boff[i] + 2u * k0);
     }
   };
 
@@ -1227,10 +1231,10 @@ hipError_t launch_prefill_up(const GemmTile *tiles, int ntiles, const GemmJob *j
   if (ntiles <= 0) return hipSuccess;
   if (rows == 256 && dma_fits(a_bytes)) {
     if (d % kDmaKs == 0)
-      MOE_LAUNCH((prefill_gemm_dma_kernel<true, false, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<true, false, kDmaWaves, 256, kDmaKs>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
                  (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff, dev_ntiles);
     else
-      MOE_LAUNCH((prefill_gemm_dma_kernel<true, true, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<true, true, kDmaWaves, 256, kDmaKs>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, xn,
                  (uint32_t)a_bytes, perm_tok, (void *)act, d, d_ff, dev_ntiles);
     return hipGetLastError();
   }
@@ -1294,10 +1298,10 @@ hipError_t launch_prefill_down(const GemmTile *tiles, int ntiles, const GemmJob 
   if (ntiles <= 0) return hipSuccess;
   if (rows == 256 && dma_fits(a_bytes)) {
     if (d_ff % kDmaKs == 0)
-      MOE_LAUNCH((prefill_gemm_dma_kernel<false, false, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<false, false, kDmaWaves, 256, kDmaKs>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
                  (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff, dev_ntiles);
     else
-      MOE_LAUNCH((prefill_gemm_dma_kernel<false, true, kDmaWaves>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
+      MOE_LAUNCH((prefill_gemm_dma_kernel<false, true, kDmaWaves, 256, kDmaKs>), dim3(ntiles), dim3(kDmaWaves * kWave), 0, l, tiles, jobs, act,
                  (uint32_t)a_bytes, (const int32_t *)nullptr, (void *)Y, d, d_ff, dev_ntiles);
     return hipGetLastError();
   }
