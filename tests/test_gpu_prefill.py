@@ -177,6 +177,23 @@ def test_device_planned_batches(T):
     rig.store.close()
 
 
+@pytest.mark.parametrize("slots,T", [(16, 300), (64, 32)])
+def test_prefill_largest_top_k(slots, T):
+    # top-16 over 64 experts, so the un-permute adds each token's ranks in two
+    # batches of eight: with 16 slots the batch streams experts (planned on the
+    # host), with a slot for every expert and 32 tokens it is planned on the
+    # device (small-M tiles, up to 32 rows an expert)
+    cfg = wl.CONFIGS["tiny-stack"].with_(layers=2, experts=64, top_k=16, d_model=128, d_ff=256,
+                                         dtype="bf16", tokens=2, prefill_tokens=T)
+    _say("prefill top-16", slots, T)
+    rig = Rig(cfg)
+    moe = rig.cache(slots, "lfu", max_prefill_tokens=T)
+    _, _, worst, _ = prefill_and_check(rig, moe, "lfu", slots, T, list(range(0, T, 3)) + [T - 1])
+    _say("worst", worst)
+    moe.close()
+    rig.store.close()
+
+
 def test_prefill_rejects_bad_token_counts():
     cfg = wl.CONFIGS["tiny-stack"].with_(layers=1, dtype="bf16", d_model=64, d_ff=64)
     rig = Rig(cfg)
