@@ -14,16 +14,20 @@
 //              last tick; LRU: last use; ties: resident first, lower id);
 //              kept experts keep their slots, newcomers take the
 //              freed slots in ascending order
-//   3. experts the host schedules: grouped GEMMs (MFMA bf16, fp32 accumulate)
-//              on experts resident at the start, while the copy stream streams
-//              every other routed expert (into its new slot, or a staging ring)
-//              followed by the grouped GEMMs on those
+//   3. experts grouped GEMMs (MFMA bf16, fp32 accumulate) on experts resident
+//              at the start, while the copy stream streams every other routed
+//              expert (into its new slot, or a staging ring) followed by the
+//              grouped GEMMs on those; the host schedules them from the plan,
+//              except with a slot for every expert, where the plan kernel
+//              writes the GEMM jobs and tiles itself
 //   4. unpermute  h_t += sum_r g_tr Y[pos(t, r)] in rank order (no atomics)
 //
 // The gate GEMM and the grouped GEMMs are dense contractions, so they run on
 // the matrix cores: the gate on the fp64 ones (exact products, fp64 sums),
-// the expert GEMMs (rows = pairs routed to one expert) on bf16 ones with a
-// 128 x 128 output tile per workgroup, four waves of 64 x 64 each.
+// the expert GEMMs (rows = pairs routed to one expert) on bf16 ones, each
+// wave holding 64 x 64 output blocks: 256-row tiles of eight waves staged by
+// LDS DMA for large launches, 128- or 64-row tiles of four waves otherwise,
+// and a small-M kernel for groups of at most 32 rows.
 #include "common.hpp"
 #include "moe_offload.h"
 
